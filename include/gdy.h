@@ -1,0 +1,201 @@
+/*
+ * gdy.h -- C-ABI of libgdy: many independent dense GEMMs on one MI355X,
+ * run either one after another or concurrently under a dynamic selector.
+ *
+ * Method: GOLDYLOC (Pati, Aga, Jayasena, Sinclair), "Global Optimizations &
+ * Lightweight Dynamic Logic for Concurrency", arXiv 2409.02227.
+ *   - GEMM definition: Sec. 2.1.2 -- C (M x N) from A (M x K) and B, with
+ *     2*M*N*K flops; T1/T2 say whether A and B are used transposed.
+ *   - GO-Kernels: Sec. 4.2 -- per GEMM shape, one kernel tuned for
+ *     isolated execution plus one per concurrency degree (CD), found by
+ *     tuning under resource constraints (fewer CUs).
+ *   - Dynamic logic: Sec. 4.3 -- given the pending independent GEMMs,
+ *     predict a CD from per-GEMM features with a multi-class logistic
+ *     regression (Eq. 1), run min(CD, available) of them together, and
+ *     bind each to the GO-Kernel tuned for that CD.
+ *   - Execution configurations: Sec. 5.5 -- sequential, default (all
+ *     GEMMs at once with isolation-tuned kernels), GO-Kernels, GOLDYLOC.
+ *   - Heterogeneous sets: Sec. 6.7 -- GEMMs run together only if all of
+ *     them prefer that CD; otherwise they are split into smaller sets.
+ *
+ * Storage reading (the paper fixes no base layout): every matrix is
+ * row-major with a leading dimension in elements.
+ *   op(A)(i,k) = A[i*lda + k]  (trans_a = 0)   or A[k*lda + i] (trans_a = 1)
+ *   op(B)(k,j) = B[k*ldb + j]  (trans_b = 0)   or B[j*ldb + k] (trans_b = 1)
+ *   C[i*ldc + j] = round(scale_a * scale_b * sum_k op(A)(i,k) op(B)(k,j))
+ * with fp32 accumulation, alpha = 1 apart from the fp8 scales, beta = 0
+ * (C is overwritten) and round-to-nearest-even into the output type.
+ *
+ * Supported (a_type, b_type, c_type): (F16, F16, F16), (BF16, BF16, BF16),
+ * (FP8_E4M3, FP8_E4M3, BF16).  FP8_E4M3 is the OCP "E4M3FN" encoding
+ * (bias 7, largest finite 448, no infinities).
+ *
+ * Ownership: all matrices are device buffers owned by the caller, who keeps
+ * them alive until the origin stream passes the work.  The library owns its
+ * stream pool, events and plan state.  No call allocates device memory
+ * after gdy_create.
+ *
+ * Errors: every call returns a gdy_status; nothing is thrown across the ABI.
+ * gdy_execute validates all descriptors before launching anything (all or
+ * nothing); gdy_last_error() gives a message for the most recent failure.
+ * A context is not thread-safe: use one per host thread, or lock.
+ *
+ * Environment: HIP maps streams onto GPU_MAX_HW_QUEUES hardware queues per
+ * process (4 by default); set it to at least the largest CD (16) before the
+ * process first touches HIP, or concurrent GEMMs share queues and serialise.
+ */
+#ifndef GDY_H
+#define GDY_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GDY_MAX_GEMMS 256   /* most GEMMs in one submission                   */
+#define GDY_N_CD 5          /* CD classes 1, 2, 4, 8, 16 (Sec. 4.3)           */
+#define GDY_N_FEATURES 18   /* M, N, K, then (#WGs, occupancy, #waves) per CD */
+
+typedef enum {
+  GDY_OK = 0,
+  GDY_ERR_INVALID_ARG = 1, /* null pointer, negative size, bad ld, bad mode, bad scale */
+  GDY_ERR_UNSUPPORTED = 2, /* dtype triple, alignment or extent the kernels cannot take */
+  GDY_ERR_ALIAS = 3,       /* a C range overlaps an A, B or C range of the submission */
+  GDY_ERR_TOO_MANY = 4,    /* n > GDY_MAX_GEMMS                                      */
+  GDY_ERR_TABLE = 5,       /* GO table unreadable or built for another device/catalogue */
+  GDY_ERR_HIP = 6,         /* a HIP runtime call failed                              */
+  GDY_ERR_NOMEM = 7        /* host allocation failed                                 */
+} gdy_status;
+
+typedef enum { GDY_F16 = 1, GDY_BF16 = 2, GDY_FP8_E4M3 = 3 } gdy_dtype;
+
+/* Execution configurations (Sec. 5.5). */
+typedef enum {
+  GDY_SEQUENTIAL = 0, /* isolation-tuned kernel per GEMM, one after another on the origin stream */
+  GDY_DEFAULT = 1,    /* isolation-tuned kernels, all n GEMMs at once, one stream each           */
+  GDY_GO = 2,         /* GO-Kernels for CD = n (or forced_cd), all at once                      */
+  GDY_SELECTOR = 3,   /* GOLDYLOC: predicted CD per GEMM, grouping, GO-Kernels per group        */
+  GDY_FORCED = 4      /* each GEMM's `variant`, round-robin over forced_cd streams (tuning)     */
+} gdy_mode;
+
+/* One GEMM of a submission. */
+typedef struct {
+  int64_t m, n, k;                  /* sizes; m or n == 0 is a no-op, k == 0 writes zeros   */
+  int32_t a_type, b_type, c_type;   /* gdy_dtype values                                     */
+  int32_t trans_a, trans_b;         /* T1, T2: 0 or 1 (see storage reading above)          */
+  const void* a; int64_t lda;       /* device pointers; leading dimensions in elements      */
+  const void* b; int64_t ldb;
+  void* c;       int64_t ldc;       /* ldc >= n                                             */
+  float scale_a, scale_b;           /* fp8 per-tensor scales; must be 1.0f for 16-bit types */
+  int32_t tenant;                   /* caller's tag, reported back in per-kernel timings    */
+  int32_t variant;                  /* GDY_FORCED: variant id to use; otherwise ignored     */
+} gdy_gemm;
+
+/* A plan: how a submission is grouped, streamed and bound to variants. */
+typedef struct {
+  int32_t n;                            /* GEMMs planned                                   */
+  int32_t cd;                           /* largest number of GEMMs launched together       */
+  int32_t n_groups;                     /* groups run one after another                    */
+  int32_t fallback;                     /* 1: no GO table, isolated heuristics were used    */
+  int32_t order[GDY_MAX_GEMMS];         /* launch order: order[t] is a GEMM index          */
+  int32_t group_of[GDY_MAX_GEMMS];      /* group of GEMM i                                 */
+  int32_t stream_of[GDY_MAX_GEMMS];     /* pool stream slot of GEMM i (-1: origin stream)  */
+  int32_t variant_of[GDY_MAX_GEMMS];    /* variant id bound to GEMM i (-1: not launched)   */
+  int32_t pred_cd[GDY_MAX_GEMMS];       /* selector: min(predicted CD, n) of GEMM i, else 0 */
+  int32_t group_size[GDY_MAX_GEMMS];    /* size of group g (first n_groups entries)        */
+} gdy_plan_t;
+
+/* Static description of one catalogue variant (a kernel plus its grid cap). */
+typedef struct {
+  char name[64];
+  int32_t dtype, trans_a, trans_b;
+  int32_t bm, bn, bk;       /* macro tile                                              */
+  int32_t waves;            /* waves per workgroup                                     */
+  int32_t mfma;             /* MFMA block edge (32 or 16)                              */
+  int32_t lds_bytes;        /* LDS per workgroup                                       */
+  int32_t vgprs;            /* registers per lane reported by the runtime              */
+  int32_t occupancy;        /* workgroups resident per CU (runtime occupancy query)    */
+  int32_t grid_cap_cus;     /* 0: one workgroup per tile; else grid = cap * occupancy  */
+} gdy_variant_desc;
+
+typedef struct gdy_ctx gdy_ctx;
+
+/*
+ * Create a context on HIP device `device`.  Loads the catalogue, queries
+ * each kernel's occupancy, creates `max_streams` (1..64; 0 means 16) pool
+ * streams at default priority and their events.  `table_path` names a GO
+ * table written by the offline tuner (NULL or "" = none: SELECTOR and GO
+ * modes then fall back to isolated heuristics and report fallback = 1).
+ * A table built for another device or catalogue returns GDY_ERR_TABLE.
+ * `use_cu_masks` != 0 also creates CU-masked pools for the resource
+ * constraints GPU/2, GPU/4 and GPU/8 (used by the tuner).  On error *out is
+ * NULL.
+ */
+gdy_status gdy_create(gdy_ctx** out, int device, const char* table_path, int32_t max_streams,
+                      int32_t use_cu_masks);
+
+/*
+ * Resource constraint for subsequent launches (Sec. 4.2.1 "RC tuning"):
+ * 0 = whole GPU; 128, 64 or 32 = run on the CU-masked pool restricted to
+ * that many CUs (needs use_cu_masks at create).  Other values:
+ * GDY_ERR_INVALID_ARG.
+ */
+gdy_status gdy_set_rc(gdy_ctx* ctx, int32_t budget_cus);
+
+/* Destroy a context: synchronises its streams, then frees streams and events. */
+void gdy_destroy(gdy_ctx* ctx);
+
+/*
+ * Plan a submission without touching device memory (pointers are validated
+ * for null/alias only and never dereferenced).  Sec. 4.3 dynamic logic for
+ * SELECTOR; see gdy_mode for the others.  forced_cd: GO and FORCED modes
+ * (0 = n); ignored otherwise.
+ */
+gdy_status gdy_plan(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode,
+                    int32_t forced_cd, gdy_plan_t* out);
+
+/*
+ * Plan and launch a submission.  Asynchronous to the host: the work is
+ * ordered after what is already on `hip_stream` (a hipStream_t; NULL is the
+ * null stream) and `hip_stream` is ordered after all of it when this
+ * returns.  `out` (nullable) receives the plan.  On GDY_ERR_HIP the streams
+ * are still joined back to the origin stream.
+ */
+gdy_status gdy_execute(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode,
+                       int32_t forced_cd, void* hip_stream, gdy_plan_t* out);
+
+/*
+ * Per-kernel timing.  When enabled, every launch of gdy_execute records a
+ * start and a stop event on the stream it runs on (hipExtLaunchKernel), and
+ * a submission start event on the origin stream.  After the caller has
+ * synchronised, gdy_last_kernel_times fills start_ms[i] / end_ms[i]
+ * (milliseconds from the submission start) for GEMM i of the last
+ * submission; GEMMs that launched nothing get -1.
+ */
+gdy_status gdy_set_timing(gdy_ctx* ctx, int32_t enable);
+gdy_status gdy_last_kernel_times(gdy_ctx* ctx, float* start_ms, float* end_ms, int32_t n);
+
+/* Features of one GEMM (Sec. 4.3): M, N, K, then for each CD class
+ * 1, 2, 4, 8, 16 the bound variant's #WGs, occupancy and #waves. */
+gdy_status gdy_features(gdy_ctx* ctx, const gdy_gemm* gemm, double* out_features);
+
+/* Catalogue queries.  Variant ids are 0 .. gdy_variant_count()-1. */
+int32_t gdy_variant_count(gdy_ctx* ctx);
+gdy_status gdy_variant_info(gdy_ctx* ctx, int32_t id, gdy_variant_desc* out);
+int32_t gdy_variant_find(gdy_ctx* ctx, const char* name); /* -1 if absent */
+/* Isolated (CD 1) variant the library binds to a GEMM, from the table or heuristics. */
+int32_t gdy_isolated_variant(gdy_ctx* ctx, const gdy_gemm* gemm);
+/* FNV-1a hash of the catalogue's variant names, as stored in GO tables. */
+uint64_t gdy_catalogue_hash(gdy_ctx* ctx);
+/* Number of compute units of the context's device. */
+int32_t gdy_device_cus(gdy_ctx* ctx);
+
+const char* gdy_status_string(gdy_status s);
+const char* gdy_last_error(gdy_ctx* ctx); /* valid until the next call on ctx; "" if none */
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GDY_H */

@@ -1,0 +1,925 @@
+// gdy.cpp -- host runtime of libgdy: catalogue, validation, features,
+// dynamic selector, GO table, concurrent launcher and the C-ABI.
+//
+// GOLDYLOC (arXiv 2409.02227) places its dynamic logic in the GPU's
+// command processor, which inspects the heads of all queues, computes
+// per-GEMM features, predicts a concurrency degree (CD) and rewrites each
+// kernel packet to point at the GO-Kernel for that CD (Sec. 4.4).  The
+// command processor of an MI355X is not programmable by users either, so
+// the same logic runs here on the host, between the caller's submission
+// and the kernel launches: it costs a few hundred multiply-adds per GEMM.
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <fstream>
+#include <sstream>
+#include <string>
+#include <vector>
+
+#include "gdy.h"
+#include "gdy_internal.h"
+
+using namespace gdy;
+
+namespace {
+
+const int kCD[GDY_N_CD] = {1, 2, 4, 8, 16};  // CD classes of the predictor (Sec. 4.3)
+const int kCaps[] = {0, 128, 64, 32};         // grid caps in CUs: GPU, GPU/2, GPU/4, GPU/8
+const int kNumCaps = 4;
+const int kRcBudgets[] = {128, 64, 32};       // CU-masked pools for resource constraints
+
+struct Kernel {
+  const KernelDesc* d;
+  int occupancy;  // workgroups per CU
+  int vgprs;
+};
+
+struct Variant {
+  int kernel;
+  int cap;  // grid cap in CUs, 0 = none
+  std::string name;
+};
+
+struct TableEntry {
+  int dtype, ta, tb, mlog;
+  int64_t n, k;
+  int v[GDY_N_CD];
+};
+
+struct Table {
+  bool loaded = false;
+  bool has_lr = false;
+  std::vector<TableEntry> entries;
+  double xmin[GDY_N_FEATURES], xmax[GDY_N_FEATURES];
+  double w[GDY_N_FEATURES][GDY_N_CD];
+  double b[GDY_N_CD];
+};
+
+int elem_size(int dt) { return dt == DT_FP8 ? 1 : 2; }
+
+int ceil_log2(int64_t x) {
+  int l = 0;
+  while (l < 62 && ((int64_t)1 << l) < x) ++l;
+  return l;
+}
+
+uint64_t fnv1a(const std::string& s, uint64_t h) {
+  for (unsigned char c : s) {
+    h ^= c;
+    h *= 1099511628211ull;
+  }
+  return h;
+}
+
+}  // namespace
+
+struct gdy_ctx {
+  int device = 0;
+  int cus = 0;
+  std::string arch;
+  std::vector<Kernel> kernels;
+  std::vector<Variant> variants;
+  uint64_t cat_hash = 0;
+  std::vector<hipStream_t> pool;                   // whole GPU
+  std::vector<std::vector<hipStream_t>> rc_pools;  // one per kRcBudgets entry
+  int rc = 0;                                      // active CU budget, 0 = whole GPU
+  std::vector<hipEvent_t> done;                    // one per stream slot
+  hipEvent_t fork_ev = nullptr;
+  bool timing = false;
+  hipEvent_t sub_start = nullptr;
+  std::vector<hipEvent_t> t_start, t_stop;
+  int last_n = 0;
+  std::vector<char> last_launched;
+  Table table;
+  std::string err;
+};
+
+namespace {
+
+gdy_status fail(gdy_ctx* ctx, gdy_status s, const char* fmt, ...) {
+  if (ctx) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    ctx->err = buf;
+  }
+  return s;
+}
+
+#define HIP_TRY(ctx, call)                                                                    \
+  do {                                                                                        \
+    hipError_t e_ = (call);                                                                   \
+    if (e_ != hipSuccess)                                                                     \
+      return fail(ctx, GDY_ERR_HIP, "%s failed: %s", #call, hipGetErrorString(e_));          \
+  } while (0)
+
+// ---------------------------------------------------------------------------
+// Geometry of one launch
+// ---------------------------------------------------------------------------
+struct Geometry {
+  int tiles_m, tiles_n, tiles, grid;
+};
+
+Geometry geometry(const gdy_ctx* ctx, int vid, const gdy_gemm& g) {
+  const Variant& v = ctx->variants[vid];
+  const Kernel& k = ctx->kernels[v.kernel];
+  Geometry geo;
+  geo.tiles_m = (int)((g.m + k.d->bm - 1) / k.d->bm);
+  geo.tiles_n = (int)((g.n + k.d->bn - 1) / k.d->bn);
+  geo.tiles = geo.tiles_m * geo.tiles_n;
+  geo.grid = geo.tiles;
+  if (v.cap > 0) geo.grid = std::min(geo.tiles, v.cap * std::max(k.occupancy, 1));
+  return geo;
+}
+
+bool variant_fits(const gdy_ctx* ctx, int vid, const gdy_gemm& g) {
+  if (vid < 0 || vid >= (int)ctx->variants.size()) return false;
+  const KernelDesc* d = ctx->kernels[ctx->variants[vid].kernel].d;
+  return d->dtype == g.a_type && d->ta == g.trans_a && d->tb == g.trans_b;
+}
+
+// Isolated heuristic used when no GO table is loaded: estimate each
+// uncapped tile's time as max(tile area / 128, tile perimeter) per wave of
+// workgroups and take the cheapest.
+int heuristic_variant(const gdy_ctx* ctx, const gdy_gemm& g) {
+  int best = -1;
+  double best_t = 0;
+  for (int vid = 0; vid < (int)ctx->variants.size(); ++vid) {
+    const Variant& v = ctx->variants[vid];
+    if (v.cap != 0 || !variant_fits(ctx, vid, g)) continue;
+    const Kernel& k = ctx->kernels[v.kernel];
+    const Geometry geo = geometry(ctx, vid, g);
+    const double slots = (double)ctx->cus * std::max(k.occupancy, 1);
+    const double waves = std::ceil(std::max(geo.tiles, 1) / slots);
+    const double per = std::max(k.d->bm * (double)k.d->bn / 128.0, (double)(k.d->bm + k.d->bn));
+    const double t = waves * per;
+    if (best < 0 || t < best_t) {
+      best = vid;
+      best_t = t;
+    }
+  }
+  return best;
+}
+
+// GO table lookup: nearest tuned shape bucket (same dtype and layout) in
+// log2 space, then the variant stored for CD class ci.
+int table_variant(const gdy_ctx* ctx, const gdy_gemm& g, int ci) {
+  const Table& t = ctx->table;
+  const int mlog = ceil_log2(std::max<int64_t>(g.m, 1));
+  const double ln = std::log2((double)std::max<int64_t>(g.n, 1));
+  const double lk = std::log2((double)std::max<int64_t>(g.k, 1));
+  int best = -1;
+  double best_d = 0;
+  for (size_t i = 0; i < t.entries.size(); ++i) {
+    const TableEntry& e = t.entries[i];
+    if (e.dtype != g.a_type || e.ta != g.trans_a || e.tb != g.trans_b) continue;
+    const double d = std::fabs((double)(e.mlog - mlog)) + std::fabs(std::log2((double)e.n) - ln) +
+                     std::fabs(std::log2((double)e.k) - lk);
+    if (best < 0 || d < best_d) {
+      best = (int)i;
+      best_d = d;
+    }
+  }
+  if (best < 0) return -1;
+  return t.entries[best].v[ci];
+}
+
+// Variant bound to GEMM g for CD class ci (0 = isolated).
+int bind_variant(const gdy_ctx* ctx, const gdy_gemm& g, int ci, bool* fallback) {
+  if (ctx->table.loaded) {
+    const int v = table_variant(ctx, g, ci);
+    if (v >= 0) return v;
+  }
+  if (fallback) *fallback = true;
+  return heuristic_variant(ctx, g);
+}
+
+// CD class whose tuned kernel serves a group of s GEMMs: nearest class in
+// log2, ties upward; with integers, between 2^j and 2^(j+1) go up iff
+// s^2 >= 2^(2j+1).
+int class_for_size(int s) {
+  if (s <= 1) return 0;
+  for (int j = 0; j + 1 < GDY_N_CD; ++j) {
+    const int lo = kCD[j], hi = kCD[j + 1];
+    if (s == lo) return j;
+    if (s < hi) return ((int64_t)s * s >= 2LL * lo * lo) ? j + 1 : j;
+  }
+  return GDY_N_CD - 1;
+}
+
+// Sec. 4.3 features: M, N, K and, per CD class, (#WGs, occupancy, #waves)
+// of the kernel bound for that class; #waves = #WGs / (CUs * occupancy).
+void features(const gdy_ctx* ctx, const gdy_gemm& g, double* x) {
+  x[0] = (double)g.m;
+  x[1] = (double)g.n;
+  x[2] = (double)g.k;
+  for (int ci = 0; ci < GDY_N_CD; ++ci) {
+    const int vid = bind_variant(ctx, g, ci, nullptr);
+    double wgs = 0, occ = 0, waves = 0;
+    if (vid >= 0) {
+      const Geometry geo = geometry(ctx, vid, g);
+      occ = ctx->kernels[ctx->variants[vid].kernel].occupancy;
+      wgs = geo.grid;
+      waves = occ > 0 ? wgs / ((double)ctx->cus * occ) : 0.0;
+    }
+    x[3 + 3 * ci + 0] = wgs;
+    x[3 + 3 * ci + 1] = occ;
+    x[3 + 3 * ci + 2] = waves;
+  }
+}
+
+// Eq. 1: P = softmax(x W + b) over CD classes; the most probable class is
+// the argmax of the linear scores (softmax is monotone).  Features are
+// min-max normalised with the training minima and maxima.  Ties go to the
+// smaller CD.  Returns the CD value (1..16).
+int predict_cd(const gdy_ctx* ctx, const double* x) {
+  const Table& t = ctx->table;
+  double xn[GDY_N_FEATURES];
+  for (int i = 0; i < GDY_N_FEATURES; ++i) {
+    const double span = t.xmax[i] - t.xmin[i];
+    xn[i] = span > 0 ? (x[i] - t.xmin[i]) / span : 0.0;
+  }
+  int best = 0;
+  double best_s = 0;
+  for (int c = 0; c < GDY_N_CD; ++c) {
+    double s = t.b[c];
+    for (int i = 0; i < GDY_N_FEATURES; ++i) s += xn[i] * t.w[i][c];
+    if (c == 0 || s > best_s) {
+      best = c;
+      best_s = s;
+    }
+  }
+  return kCD[best];
+}
+
+// ---------------------------------------------------------------------------
+// Validation (all or nothing, before any launch)
+// ---------------------------------------------------------------------------
+struct Extent {
+  uintptr_t lo, hi;  // [lo, hi) in bytes; empty when lo == hi
+};
+
+bool stored_extent(int64_t rows, int64_t cols, int64_t ld, int es, int64_t* bytes) {
+  if (rows == 0 || cols == 0) {
+    *bytes = 0;
+    return true;
+  }
+  *bytes = ((rows - 1) * ld + cols) * es;
+  // the kernels form 32-bit byte offsets up to 256 rows past the edge
+  return (rows + 256) * ld * es + 1024 < (int64_t)INT32_MAX;
+}
+
+gdy_status validate_one(gdy_ctx* ctx, const gdy_gemm& g, int i, Extent* ea, Extent* eb,
+                        Extent* ec) {
+  *ea = *eb = *ec = Extent{0, 0};
+  if (g.m < 0 || g.n < 0 || g.k < 0)
+    return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: negative size", i);
+  const bool t16 = (g.a_type == GDY_F16 && g.b_type == GDY_F16 && g.c_type == GDY_F16) ||
+                   (g.a_type == GDY_BF16 && g.b_type == GDY_BF16 && g.c_type == GDY_BF16);
+  const bool t8 = g.a_type == GDY_FP8_E4M3 && g.b_type == GDY_FP8_E4M3 && g.c_type == GDY_BF16;
+  if (!t16 && !t8)
+    return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: unsupported dtype triple (%d,%d,%d)", i,
+                g.a_type, g.b_type, g.c_type);
+  if ((g.trans_a != 0 && g.trans_a != 1) || (g.trans_b != 0 && g.trans_b != 1))
+    return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: trans flags must be 0 or 1", i);
+  if (!std::isfinite(g.scale_a) || !std::isfinite(g.scale_b))
+    return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: non-finite scale", i);
+  if (t16 && (g.scale_a != 1.0f || g.scale_b != 1.0f))
+    return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: scales must be 1 for 16-bit inputs", i);
+  if (g.m == 0 || g.n == 0) return GDY_OK;  // no-op
+  const int es = elem_size(g.a_type);
+  if (!g.c) return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: null C", i);
+  if (g.ldc < g.n) return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: ldc < n", i);
+  if ((uintptr_t)g.c % 2) return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: C not 2-byte aligned", i);
+  int64_t cb;
+  if (!stored_extent(g.m, g.n, g.ldc, 2, &cb))
+    return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: C extent too large", i);
+  ec->lo = (uintptr_t)g.c;
+  ec->hi = ec->lo + (uintptr_t)cb;
+  if (g.k == 0) return GDY_OK;
+  if (!g.a || !g.b) return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: null A or B", i);
+  if (g.lda < (g.trans_a ? g.m : g.k)) return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: lda too small", i);
+  if (g.ldb < (g.trans_b ? g.k : g.n)) return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: ldb too small", i);
+  if (es == 2 && (((uintptr_t)g.a | (uintptr_t)g.b) % 2))
+    return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: A or B not element aligned", i);
+  int64_t ab, bb;
+  const bool oka = g.trans_a ? stored_extent(g.k, g.m, g.lda, es, &ab) : stored_extent(g.m, g.k, g.lda, es, &ab);
+  const bool okb = g.trans_b ? stored_extent(g.n, g.k, g.ldb, es, &bb) : stored_extent(g.k, g.n, g.ldb, es, &bb);
+  if (!oka || !okb) return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: A or B extent too large", i);
+  ea->lo = (uintptr_t)g.a;
+  ea->hi = ea->lo + (uintptr_t)ab;
+  eb->lo = (uintptr_t)g.b;
+  eb->hi = eb->lo + (uintptr_t)bb;
+  return GDY_OK;
+}
+
+bool overlap(const Extent& x, const Extent& y) {
+  return x.lo < x.hi && y.lo < y.hi && x.lo < y.hi && y.lo < x.hi;
+}
+
+gdy_status validate(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode) {
+  if (n < 0) return fail(ctx, GDY_ERR_INVALID_ARG, "n < 0");
+  if (n > GDY_MAX_GEMMS) return fail(ctx, GDY_ERR_TOO_MANY, "n = %d > %d", n, GDY_MAX_GEMMS);
+  if (n > 0 && !gemms) return fail(ctx, GDY_ERR_INVALID_ARG, "null gemm array");
+  if (mode < GDY_SEQUENTIAL || mode > GDY_FORCED) return fail(ctx, GDY_ERR_INVALID_ARG, "bad mode %d", mode);
+  std::vector<Extent> ea(n), eb(n), ec(n);
+  for (int i = 0; i < n; ++i) {
+    gdy_status s = validate_one(ctx, gemms[i], i, &ea[i], &eb[i], &ec[i]);
+    if (s != GDY_OK) return s;
+    if (mode == GDY_FORCED && gemms[i].m > 0 && gemms[i].n > 0 &&
+        !variant_fits(ctx, gemms[i].variant, gemms[i]))
+      return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: variant %d does not fit its dtype/layout", i,
+                  gemms[i].variant);
+  }
+  // independence: no output range may overlap any operand or output range
+  for (int i = 0; i < n; ++i) {
+    if (ec[i].lo == ec[i].hi) continue;
+    for (int j = 0; j < n; ++j) {
+      if (overlap(ec[i], ea[j]) || overlap(ec[i], eb[j]) || (j != i && overlap(ec[i], ec[j])))
+        return fail(ctx, GDY_ERR_ALIAS, "gemm %d: C overlaps an operand or output of gemm %d", i, j);
+    }
+  }
+  return GDY_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Planning
+// ---------------------------------------------------------------------------
+void plan_reset(gdy_plan_t* p, int n) {
+  std::memset(p, 0, sizeof *p);
+  p->n = n;
+  for (int i = 0; i < GDY_MAX_GEMMS; ++i) {
+    p->order[i] = -1;
+    p->group_of[i] = -1;
+    p->stream_of[i] = -1;
+    p->variant_of[i] = -1;
+  }
+}
+
+bool active(const gdy_gemm& g) { return g.m > 0 && g.n > 0; }
+
+int pool_size(const gdy_ctx* ctx) {
+  if (ctx->rc == 0) return (int)ctx->pool.size();
+  for (size_t r = 0; r < ctx->rc_pools.size(); ++r)
+    if (kRcBudgets[r] == ctx->rc) return (int)ctx->rc_pools[r].size();
+  return (int)ctx->pool.size();
+}
+
+void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int forced_cd,
+               gdy_plan_t* p) {
+  plan_reset(p, n);
+  bool fb = false;
+  const int S = pool_size(ctx);
+  std::vector<int> live;
+  for (int i = 0; i < n; ++i)
+    if (active(g[i])) live.push_back(i);
+  const int L = (int)live.size();
+
+  if (mode == GDY_SEQUENTIAL || (mode == GDY_SELECTOR && L <= 1)) {
+    // Sec. 5.5 sequential; a lone GEMM keeps the isolated kernel (Sec. 4.4)
+    for (int t = 0; t < L; ++t) {
+      const int i = live[t];
+      p->order[t] = i;
+      p->group_of[i] = 0;
+      p->stream_of[i] = -1;
+      p->variant_of[i] = bind_variant(ctx, g[i], 0, &fb);
+    }
+    p->n_groups = L > 0 ? 1 : 0;
+    p->group_size[0] = L;
+    p->cd = L > 0 ? 1 : 0;
+    p->fallback = (fb || !ctx->table.loaded) ? 1 : 0;
+    return;
+  }
+
+  if (mode == GDY_DEFAULT || mode == GDY_GO || mode == GDY_FORCED) {
+    int cd = L;
+    if ((mode == GDY_GO || mode == GDY_FORCED) && forced_cd > 0) cd = std::min(forced_cd, std::max(L, 1));
+    cd = std::max(1, std::min(cd, S));
+    const int ci = class_for_size(mode == GDY_GO && forced_cd > 0 ? forced_cd : L);
+    for (int t = 0; t < L; ++t) {
+      const int i = live[t];
+      p->order[t] = i;
+      p->group_of[i] = 0;
+      p->stream_of[i] = t % cd;
+      if (mode == GDY_DEFAULT)
+        p->variant_of[i] = bind_variant(ctx, g[i], 0, &fb);
+      else if (mode == GDY_GO)
+        p->variant_of[i] = bind_variant(ctx, g[i], ci, &fb);
+      else
+        p->variant_of[i] = g[i].variant;
+    }
+    p->n_groups = L > 0 ? 1 : 0;
+    p->group_size[0] = L;
+    p->cd = L > 0 ? cd : 0;
+    p->fallback = (mode != GDY_FORCED && (fb || !ctx->table.loaded)) ? 1 : 0;
+    return;
+  }
+
+  // GDY_SELECTOR (Sec. 4.3, Sec. 6.7): per-GEMM CD = min(predicted, n);
+  // sort by it (descending, stable); greedily form groups whose size never
+  // exceeds any member's CD; groups run one after another, each GEMM of a
+  // group on its own stream, bound to the GO-Kernel tuned for the group's
+  // size.  Without a trained predictor every GEMM keeps CD 1.
+  std::vector<int> pred(n, 0);
+  for (int t = 0; t < L; ++t) {
+    const int i = live[t];
+    int cd = 1;
+    if (ctx->table.loaded && ctx->table.has_lr) {
+      double x[GDY_N_FEATURES];
+      features(ctx, g[i], x);
+      cd = predict_cd(ctx, x);
+    } else {
+      fb = true;
+    }
+    pred[i] = std::min(cd, L);
+    p->pred_cd[i] = pred[i];
+  }
+  std::vector<int> ord(live);
+  std::stable_sort(ord.begin(), ord.end(), [&](int a, int b) { return pred[a] > pred[b]; });
+  int grp = -1, gsize = 0, gcap = 0;
+  std::vector<int> start;  // first position of each group in ord
+  for (int t = 0; t < L; ++t) {
+    const int i = ord[t];
+    const int cap = std::min(pred[i], S);
+    if (grp < 0 || gsize + 1 > std::min(gcap, cap)) {
+      ++grp;
+      start.push_back(t);
+      gsize = 0;
+      gcap = cap;
+    }
+    gcap = std::min(gcap, cap);
+    p->order[t] = i;
+    p->group_of[i] = grp;
+    p->stream_of[i] = gsize;
+    ++gsize;
+    p->group_size[grp] = gsize;
+  }
+  p->n_groups = grp + 1;
+  p->cd = 0;
+  for (int q = 0; q < p->n_groups; ++q) p->cd = std::max(p->cd, p->group_size[q]);
+  for (int t = 0; t < L; ++t) {
+    const int i = ord[t];
+    const int s = p->group_size[p->group_of[i]];
+    p->variant_of[i] = bind_variant(ctx, g[i], class_for_size(s), &fb);
+    if (s == 1) p->stream_of[i] = 0;
+  }
+  p->fallback = fb ? 1 : 0;
+}
+
+// ---------------------------------------------------------------------------
+// Launching
+// ---------------------------------------------------------------------------
+bool vec_ok(const void* ptr, int64_t ld, int es, bool kcontiguous) {
+  const uintptr_t a = (uintptr_t)ptr;
+  if (kcontiguous || es == 2) return a % 16 == 0 && (ld * es) % 16 == 0;
+  return a % 8 == 0 && (ld * es) % 8 == 0;  // fp8 k-major operand: 8-byte row vectors
+}
+
+KArgs make_args(const gdy_ctx* ctx, int vid, const gdy_gemm& g, Geometry* geo_out) {
+  const Kernel& k = ctx->kernels[ctx->variants[vid].kernel];
+  const Geometry geo = geometry(ctx, vid, g);
+  const int es = elem_size(g.a_type);
+  KArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.a = (const uint8_t*)g.a;
+  a.b = (const uint8_t*)g.b;
+  a.c = (uint8_t*)g.c;
+  a.m = g.m;
+  a.n = g.n;
+  a.k = g.k;
+  a.lda = g.lda;
+  a.ldb = g.ldb;
+  a.ldc = g.ldc;
+  a.scale = g.scale_a * g.scale_b;  // one fp32 rounding
+  int64_t ab = 0, bb = 0, cb = 0;
+  if (g.k > 0) {
+    if (g.trans_a) stored_extent(g.k, g.m, g.lda, es, &ab); else stored_extent(g.m, g.k, g.lda, es, &ab);
+    if (g.trans_b) stored_extent(g.n, g.k, g.ldb, es, &bb); else stored_extent(g.k, g.n, g.ldb, es, &bb);
+  }
+  stored_extent(g.m, g.n, g.ldc, 2, &cb);
+  a.a_bytes = (int32_t)ab;
+  a.b_bytes = (int32_t)bb;
+  a.c_bytes = (int32_t)cb;
+  a.tiles_m = geo.tiles_m;
+  a.tiles_n = geo.tiles_n;
+  a.a_vec = g.k > 0 && vec_ok(g.a, g.lda, es, g.trans_a == 0);
+  a.b_vec = g.k > 0 && vec_ok(g.b, g.ldb, es, g.trans_b == 1);
+  a.group_m = 8;
+  a.xcd_remap = 1;
+  (void)k;
+  if (geo_out) *geo_out = geo;
+  return a;
+}
+
+hipStream_t slot_stream(const gdy_ctx* ctx, int slot) {
+  if (ctx->rc == 0) return ctx->pool[slot];
+  for (size_t r = 0; r < ctx->rc_pools.size(); ++r)
+    if (kRcBudgets[r] == ctx->rc) return ctx->rc_pools[r][slot];
+  return ctx->pool[slot];
+}
+
+gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, hipStream_t origin) {
+  gdy_status st = GDY_OK;
+  const int n = p.n;
+  ctx->last_n = n;
+  ctx->last_launched.assign(n, 0);
+  if (ctx->timing) HIP_TRY(ctx, hipEventRecord(ctx->sub_start, origin));
+
+  // launch order is p.order; groups are contiguous in it
+  std::vector<int> prev_slots;  // slots used by the previous group
+  bool forked = false;
+  int t = 0;
+  int L = 0;
+  while (L < GDY_MAX_GEMMS && p.order[L] >= 0) ++L;
+  for (int grp = 0; grp < p.n_groups; ++grp) {
+    std::vector<int> slots;
+    const int t0 = t;
+    while (t < L && p.group_of[p.order[t]] == grp) {
+      const int s = p.stream_of[p.order[t]];
+      if (s >= 0 && std::find(slots.begin(), slots.end(), s) == slots.end()) slots.push_back(s);
+      ++t;
+    }
+    // order this group's streams after the origin (first group) or the
+    // previous group
+    for (int s : slots) {
+      hipStream_t hs = slot_stream(ctx, s);
+      if (grp == 0 || prev_slots.empty()) {
+        if (!forked) {
+          HIP_TRY(ctx, hipEventRecord(ctx->fork_ev, origin));
+          forked = true;
+        }
+        HIP_TRY(ctx, hipStreamWaitEvent(hs, ctx->fork_ev, 0));
+      } else {
+        for (int q : prev_slots)
+          if (q != s) HIP_TRY(ctx, hipStreamWaitEvent(hs, ctx->done[q], 0));
+      }
+    }
+    for (int u = t0; u < t && st == GDY_OK; ++u) {
+      const int i = p.order[u];
+      const int vid = p.variant_of[i];
+      const Kernel& k = ctx->kernels[ctx->variants[vid].kernel];
+      Geometry geo;
+      KArgs args = make_args(ctx, vid, g[i], &geo);
+      void* argv[] = {&args};
+      hipStream_t hs = p.stream_of[i] >= 0 ? slot_stream(ctx, p.stream_of[i]) : origin;
+      hipError_t e = hipExtLaunchKernel(k.d->func, dim3(std::max(geo.grid, 1)), dim3(k.d->waves * 64),
+                                        argv, 0, hs, ctx->timing ? ctx->t_start[i] : nullptr,
+                                        ctx->timing ? ctx->t_stop[i] : nullptr, 0);
+      if (e != hipSuccess) {
+        st = fail(ctx, GDY_ERR_HIP, "launch of %s for gemm %d failed: %s",
+                  ctx->variants[vid].name.c_str(), i, hipGetErrorString(e));
+        break;
+      }
+      ctx->last_launched[i] = 1;
+    }
+    for (int s : slots) HIP_TRY(ctx, hipEventRecord(ctx->done[s], slot_stream(ctx, s)));
+    if (!slots.empty()) prev_slots = slots;
+    if (st != GDY_OK) break;
+  }
+  // join: the origin waits for the streams of the last group that used the pool
+  for (int s : prev_slots) HIP_TRY(ctx, hipStreamWaitEvent(origin, ctx->done[s], 0));
+  return st;
+}
+
+gdy_status load_table(gdy_ctx* ctx, const char* path) {
+  std::ifstream f(path);
+  if (!f) return fail(ctx, GDY_ERR_TABLE, "cannot open GO table %s", path);
+  Table t;
+  std::string line, tag;
+  int have_min = 0, have_max = 0, have_w = 0, have_b = 0;
+  bool header = false;
+  while (std::getline(f, line)) {
+    if (line.empty() || line[0] == '#') continue;
+    std::istringstream in(line);
+    in >> tag;
+    if (tag == "gdy-go-table") {
+      int ver = 0;
+      in >> ver;
+      if (ver != 1) return fail(ctx, GDY_ERR_TABLE, "GO table version %d unsupported", ver);
+      header = true;
+    } else if (tag == "device") {
+      std::string arch, cus_tag;
+      int cus = 0;
+      in >> arch >> cus_tag >> cus;
+      if (arch != ctx->arch || cus != ctx->cus)
+        return fail(ctx, GDY_ERR_TABLE, "GO table is for %s/%d CUs, device is %s/%d", arch.c_str(),
+                    cus, ctx->arch.c_str(), ctx->cus);
+    } else if (tag == "catalogue") {
+      std::string hex;
+      in >> hex;
+      const uint64_t h = std::strtoull(hex.c_str(), nullptr, 16);
+      if (h != ctx->cat_hash)
+        return fail(ctx, GDY_ERR_TABLE, "GO table catalogue %s does not match library %016llx",
+                    hex.c_str(), (unsigned long long)ctx->cat_hash);
+    } else if (tag == "lr_min" || tag == "lr_max" || tag == "lr_b") {
+      double* dst = tag == "lr_min" ? t.xmin : tag == "lr_max" ? t.xmax : t.b;
+      const int cnt = tag == "lr_b" ? GDY_N_CD : GDY_N_FEATURES;
+      for (int i = 0; i < cnt; ++i)
+        if (!(in >> dst[i])) return fail(ctx, GDY_ERR_TABLE, "short %s row", tag.c_str());
+      (tag == "lr_min" ? have_min : tag == "lr_max" ? have_max : have_b) = 1;
+    } else if (tag == "lr_w") {
+      for (int i = 0; i < GDY_N_FEATURES; ++i)
+        for (int c = 0; c < GDY_N_CD; ++c)
+          if (!(in >> t.w[i][c])) return fail(ctx, GDY_ERR_TABLE, "short lr_w row");
+      have_w = 1;
+    } else if (tag == "entry") {
+      TableEntry e;
+      in >> e.dtype >> e.ta >> e.tb >> e.mlog >> e.n >> e.k;
+      if (!in || e.n <= 0 || e.k <= 0) return fail(ctx, GDY_ERR_TABLE, "bad entry line: %s", line.c_str());
+      for (int c = 0; c < GDY_N_CD; ++c) {
+        std::string name;
+        in >> name;
+        int vid = -1;
+        for (size_t v = 0; v < ctx->variants.size(); ++v)
+          if (ctx->variants[v].name == name) vid = (int)v;
+        if (vid < 0) return fail(ctx, GDY_ERR_TABLE, "GO table names unknown variant %s", name.c_str());
+        const KernelDesc* d = ctx->kernels[ctx->variants[vid].kernel].d;
+        if (d->dtype != e.dtype || d->ta != e.ta || d->tb != e.tb)
+          return fail(ctx, GDY_ERR_TABLE, "variant %s does not match its entry", name.c_str());
+        e.v[c] = vid;
+      }
+      t.entries.push_back(e);
+    } else {
+      return fail(ctx, GDY_ERR_TABLE, "unknown GO table line: %s", line.c_str());
+    }
+  }
+  if (!header) return fail(ctx, GDY_ERR_TABLE, "%s is not a GO table", path);
+  t.has_lr = have_min && have_max && have_w && have_b;
+  t.loaded = true;
+  ctx->table = t;
+  return GDY_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C-ABI
+// ---------------------------------------------------------------------------
+extern "C" {
+
+const char* gdy_status_string(gdy_status s) {
+  switch (s) {
+    case GDY_OK: return "ok";
+    case GDY_ERR_INVALID_ARG: return "invalid argument";
+    case GDY_ERR_UNSUPPORTED: return "unsupported";
+    case GDY_ERR_ALIAS: return "output aliases another buffer";
+    case GDY_ERR_TOO_MANY: return "too many gemms";
+    case GDY_ERR_TABLE: return "GO table error";
+    case GDY_ERR_HIP: return "HIP error";
+    case GDY_ERR_NOMEM: return "out of host memory";
+  }
+  return "unknown status";
+}
+
+const char* gdy_last_error(gdy_ctx* ctx) { return ctx ? ctx->err.c_str() : "null context"; }
+
+static void destroy_streams(gdy_ctx* ctx) {
+  for (hipStream_t s : ctx->pool) (void)hipStreamDestroy(s);
+  for (auto& pl : ctx->rc_pools)
+    for (hipStream_t s : pl) (void)hipStreamDestroy(s);
+  for (hipEvent_t e : ctx->done) (void)hipEventDestroy(e);
+  for (hipEvent_t e : ctx->t_start) (void)hipEventDestroy(e);
+  for (hipEvent_t e : ctx->t_stop) (void)hipEventDestroy(e);
+  if (ctx->fork_ev) (void)hipEventDestroy(ctx->fork_ev);
+  if (ctx->sub_start) (void)hipEventDestroy(ctx->sub_start);
+  ctx->pool.clear();
+  ctx->rc_pools.clear();
+  ctx->done.clear();
+  ctx->t_start.clear();
+  ctx->t_stop.clear();
+  ctx->fork_ev = ctx->sub_start = nullptr;
+}
+
+static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, int32_t max_streams,
+                              int32_t use_cu_masks) {
+  HIP_TRY(ctx, hipSetDevice(device));
+  hipDeviceProp_t prop;
+  HIP_TRY(ctx, hipGetDeviceProperties(&prop, device));
+  ctx->device = device;
+  ctx->cus = prop.multiProcessorCount;
+  ctx->arch = prop.gcnArchName;
+  ctx->arch = ctx->arch.substr(0, ctx->arch.find(':'));
+
+  const KernelDesc* tabs[3];
+  int counts[3];
+  counts[0] = kernels_bf16(&tabs[0]);
+  counts[1] = kernels_f16(&tabs[1]);
+  counts[2] = kernels_fp8(&tabs[2]);
+  uint64_t h = 1469598103934665603ull;
+  for (int t = 0; t < 3; ++t) {
+    for (int i = 0; i < counts[t]; ++i) {
+      Kernel k;
+      k.d = &tabs[t][i];
+      int occ = 0;
+      HIP_TRY(ctx, hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, k.d->func, k.d->waves * 64, 0));
+      hipFuncAttributes attr;
+      HIP_TRY(ctx, hipFuncGetAttributes(&attr, k.d->func));
+      k.occupancy = occ;
+      k.vgprs = attr.numRegs;
+      const int kid = (int)ctx->kernels.size();
+      ctx->kernels.push_back(k);
+      for (int c = 0; c < kNumCaps; ++c) {
+        Variant v;
+        v.kernel = kid;
+        v.cap = kCaps[c];
+        v.name = std::string(k.d->name) + "_c" + std::to_string(kCaps[c]);
+        h = fnv1a(v.name, h);
+        h = fnv1a("\n", h);
+        ctx->variants.push_back(v);
+      }
+    }
+  }
+  ctx->cat_hash = h;
+
+  int S = max_streams <= 0 ? 16 : max_streams;
+  if (S > 64) return fail(ctx, GDY_ERR_INVALID_ARG, "max_streams %d > 64", S);
+  for (int s = 0; s < S; ++s) {
+    hipStream_t st;
+    HIP_TRY(ctx, hipStreamCreateWithFlags(&st, hipStreamNonBlocking));
+    ctx->pool.push_back(st);
+    hipEvent_t e;
+    HIP_TRY(ctx, hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    ctx->done.push_back(e);
+  }
+  if (use_cu_masks) {
+    const int words = (ctx->cus + 31) / 32;
+    for (int budget : kRcBudgets) {
+      std::vector<uint32_t> mask(words, 0u);
+      for (int cu = 0; cu < std::min(budget, ctx->cus); ++cu) mask[cu / 32] |= 1u << (cu % 32);
+      std::vector<hipStream_t> pl;
+      for (int s = 0; s < S; ++s) {
+        hipStream_t st;
+        HIP_TRY(ctx, hipExtStreamCreateWithCUMask(&st, (uint32_t)words, mask.data()));
+        pl.push_back(st);
+      }
+      ctx->rc_pools.push_back(pl);
+    }
+  }
+  HIP_TRY(ctx, hipEventCreateWithFlags(&ctx->fork_ev, hipEventDisableTiming));
+  HIP_TRY(ctx, hipEventCreate(&ctx->sub_start));
+  for (int i = 0; i < GDY_MAX_GEMMS; ++i) {
+    hipEvent_t a, b;
+    HIP_TRY(ctx, hipEventCreate(&a));
+    HIP_TRY(ctx, hipEventCreate(&b));
+    ctx->t_start.push_back(a);
+    ctx->t_stop.push_back(b);
+  }
+  if (table_path && table_path[0]) {
+    gdy_status s = load_table(ctx, table_path);
+    if (s != GDY_OK) return s;
+  }
+  return GDY_OK;
+}
+
+gdy_status gdy_create(gdy_ctx** out, int device, const char* table_path, int32_t max_streams,
+                      int32_t use_cu_masks) {
+  if (!out) return GDY_ERR_INVALID_ARG;
+  *out = nullptr;
+  gdy_ctx* ctx = new (std::nothrow) gdy_ctx;
+  if (!ctx) return GDY_ERR_NOMEM;
+  gdy_status s;
+  try {
+    s = create_impl(ctx, device, table_path, max_streams, use_cu_masks);
+  } catch (...) {
+    s = GDY_ERR_NOMEM;
+  }
+  if (s != GDY_OK) {
+    fprintf(stderr, "gdy_create: %s\n", ctx->err.c_str());
+    destroy_streams(ctx);
+    delete ctx;
+    return s;
+  }
+  *out = ctx;
+  return GDY_OK;
+}
+
+void gdy_destroy(gdy_ctx* ctx) {
+  if (!ctx) return;
+  for (hipStream_t s : ctx->pool) (void)hipStreamSynchronize(s);
+  for (auto& pl : ctx->rc_pools)
+    for (hipStream_t s : pl) (void)hipStreamSynchronize(s);
+  destroy_streams(ctx);
+  delete ctx;
+}
+
+gdy_status gdy_set_rc(gdy_ctx* ctx, int32_t budget_cus) {
+  if (!ctx) return GDY_ERR_INVALID_ARG;
+  if (budget_cus == 0) {
+    ctx->rc = 0;
+    return GDY_OK;
+  }
+  for (size_t r = 0; r < ctx->rc_pools.size(); ++r)
+    if (kRcBudgets[r] == budget_cus) {
+      ctx->rc = budget_cus;
+      return GDY_OK;
+    }
+  return fail(ctx, GDY_ERR_INVALID_ARG, "no CU-masked pool for %d CUs", budget_cus);
+}
+
+gdy_status gdy_plan(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode, int32_t forced_cd,
+                    gdy_plan_t* out) {
+  if (!ctx || !out) return GDY_ERR_INVALID_ARG;
+  ctx->err.clear();
+  try {
+    gdy_status s = validate(ctx, gemms, n, mode);
+    if (s != GDY_OK) return s;
+    make_plan(ctx, gemms, n, mode, forced_cd, out);
+  } catch (...) {
+    return fail(ctx, GDY_ERR_NOMEM, "host allocation failed");
+  }
+  for (int i = 0; i < n; ++i)
+    if (active(gemms[i]) && out->variant_of[i] < 0)
+      return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: no kernel for its dtype/layout", i);
+  return GDY_OK;
+}
+
+gdy_status gdy_execute(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode, int32_t forced_cd,
+                       void* hip_stream, gdy_plan_t* out) {
+  if (!ctx) return GDY_ERR_INVALID_ARG;
+  gdy_plan_t local;
+  gdy_plan_t* p = out ? out : &local;
+  gdy_status s = gdy_plan(ctx, gemms, n, mode, forced_cd, p);
+  if (s != GDY_OK) return s;
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != ctx->device) HIP_TRY(ctx, hipSetDevice(ctx->device));
+  try {
+    return launch_plan(ctx, gemms, *p, (hipStream_t)hip_stream);
+  } catch (...) {
+    return fail(ctx, GDY_ERR_NOMEM, "host allocation failed");
+  }
+}
+
+gdy_status gdy_set_timing(gdy_ctx* ctx, int32_t enable) {
+  if (!ctx) return GDY_ERR_INVALID_ARG;
+  ctx->timing = enable != 0;
+  return GDY_OK;
+}
+
+gdy_status gdy_last_kernel_times(gdy_ctx* ctx, float* start_ms, float* end_ms, int32_t n) {
+  if (!ctx || n < 0 || (n > 0 && (!start_ms || !end_ms))) return GDY_ERR_INVALID_ARG;
+  if (!ctx->timing) return fail(ctx, GDY_ERR_INVALID_ARG, "timing is off");
+  for (int i = 0; i < n; ++i) {
+    start_ms[i] = end_ms[i] = -1.f;
+    if (i >= ctx->last_n || !ctx->last_launched[i]) continue;
+    HIP_TRY(ctx, hipEventElapsedTime(&start_ms[i], ctx->sub_start, ctx->t_start[i]));
+    HIP_TRY(ctx, hipEventElapsedTime(&end_ms[i], ctx->sub_start, ctx->t_stop[i]));
+  }
+  return GDY_OK;
+}
+
+gdy_status gdy_features(gdy_ctx* ctx, const gdy_gemm* gemm, double* out_features) {
+  if (!ctx || !gemm || !out_features) return GDY_ERR_INVALID_ARG;
+  gdy_status s = validate(ctx, gemm, 1, GDY_SELECTOR);
+  if (s != GDY_OK) return s;
+  features(ctx, *gemm, out_features);
+  return GDY_OK;
+}
+
+int32_t gdy_variant_count(gdy_ctx* ctx) { return ctx ? (int32_t)ctx->variants.size() : 0; }
+
+gdy_status gdy_variant_info(gdy_ctx* ctx, int32_t id, gdy_variant_desc* out) {
+  if (!ctx || !out || id < 0 || id >= (int32_t)ctx->variants.size()) return GDY_ERR_INVALID_ARG;
+  const Variant& v = ctx->variants[id];
+  const Kernel& k = ctx->kernels[v.kernel];
+  std::memset(out, 0, sizeof *out);
+  std::snprintf(out->name, sizeof out->name, "%s", v.name.c_str());
+  out->dtype = k.d->dtype;
+  out->trans_a = k.d->ta;
+  out->trans_b = k.d->tb;
+  out->bm = k.d->bm;
+  out->bn = k.d->bn;
+  out->bk = k.d->bk;
+  out->waves = k.d->waves;
+  out->mfma = k.d->mfma;
+  out->lds_bytes = k.d->lds_bytes;
+  out->vgprs = k.vgprs;
+  out->occupancy = k.occupancy;
+  out->grid_cap_cus = v.cap;
+  return GDY_OK;
+}
+
+int32_t gdy_variant_find(gdy_ctx* ctx, const char* name) {
+  if (!ctx || !name) return -1;
+  for (size_t v = 0; v < ctx->variants.size(); ++v)
+    if (ctx->variants[v].name == name) return (int32_t)v;
+  return -1;
+}
+
+int32_t gdy_isolated_variant(gdy_ctx* ctx, const gdy_gemm* gemm) {
+  if (!ctx || !gemm) return -1;
+  return bind_variant(ctx, *gemm, 0, nullptr);
+}
+
+uint64_t gdy_catalogue_hash(gdy_ctx* ctx) { return ctx ? ctx->cat_hash : 0; }
+
+int32_t gdy_device_cus(gdy_ctx* ctx) { return ctx ? ctx->cus : 0; }
+
+}  // extern "C"

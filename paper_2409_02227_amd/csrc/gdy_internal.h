@@ -1,0 +1,50 @@
+// gdy_internal.h -- structures shared by the GO-Kernel instantiation units
+// and the host runtime of libgdy (not part of the public C-ABI).
+#pragma once
+#include <stdint.h>
+
+namespace gdy {
+
+// Element types, numerically equal to the public gdy_dtype values.
+enum : int { DT_F16 = 1, DT_BF16 = 2, DT_FP8 = 3 };
+
+// Kernel arguments, passed by value.  Sizes and leading dimensions are in
+// elements; the storage reading is row-major with op(A)(i,k) = A[i*lda+k]
+// (or A[k*lda+i] when A is used transposed) and op(B)(k,j) = B[k*ldb+j]
+// (or B[j*ldb+k] when transposed).
+struct KArgs {
+  const uint8_t* a;
+  const uint8_t* b;
+  uint8_t* c;
+  int64_t m, n, k;
+  int64_t lda, ldb, ldc;
+  float scale;        // sa*sb rounded once in fp32 (1 for 16-bit inputs)
+  int32_t a_bytes;    // extent of each operand in bytes (< 2^31): reads and
+  int32_t b_bytes;    // writes outside it are dropped by the buffer unit
+  int32_t c_bytes;
+  int32_t tiles_m;    // ceil(m / BM)
+  int32_t tiles_n;    // ceil(n / BN)
+  int32_t a_vec;      // 1: A base and rows are aligned for vector loads
+  int32_t b_vec;      // 1: same for B
+  int32_t group_m;    // tile-order swizzle: tile rows per group
+  int32_t xcd_remap;  // 1: keep consecutive tiles on one XCD
+};
+
+// Compile-time description of one instantiated kernel.
+struct KernelDesc {
+  const char* name;   // e.g. "bf16_nn_256x256_w8_m32"
+  int dtype;          // DT_*
+  int ta, tb;         // transposed use of A / B
+  int bm, bn, bk;     // macro tile (bk in elements)
+  int waves;          // waves per workgroup
+  int mfma;           // 32 -> 32x32 MFMA blocks, 16 -> 16x16 blocks
+  int lds_bytes;      // static LDS per workgroup
+  const void* func;   // __global__ entry, launched with hipExtLaunchKernel
+};
+
+// Each instantiation unit exports its table.
+int kernels_bf16(const KernelDesc** out);
+int kernels_f16(const KernelDesc** out);
+int kernels_fp8(const KernelDesc** out);
+
+}  // namespace gdy

@@ -1,0 +1,470 @@
+// go_kernel.h -- the GO-Kernel template: one dense GEMM per launch on CDNA4
+// MFMA, with LDS-staged, double-buffered macro-tiles.
+//
+// GOLDYLOC (Sec. 2.1.3 and Sec. 4.2) treats a GEMM kernel as a tiled loop:
+// each workgroup owns one C tile and walks K, staging operand tiles in LDS;
+// tile size, workgroup count, occupancy and memory traffic are the features
+// that decide how well kernels share the GPU when several run at once.  The
+// GO-Kernel family exposes exactly those knobs as template parameters
+// (macro tile, waves per workgroup, MFMA block shape) and launch parameters
+// (grid cap, tile order), so the offline tuner can pick one per GEMM shape
+// and concurrency degree.
+//
+// Layout in LDS: both operands are stored "K-contiguous", i.e. as
+// [row][k] with 128 bytes of K per row (64 16-bit or 128 fp8 elements) and
+// a 144-byte row stride (16 bytes of padding so 16 consecutive rows of an
+// MFMA fragment read fall on distinct banks).  Operands that are
+// K-contiguous in global memory (A untransposed, B transposed) are copied
+// 16 bytes at a time; the others (B untransposed, A transposed) are loaded
+// as small k x 8 blocks and transposed in registers on the way to LDS.
+//
+// One K step: every wave loads its A and B fragments from LDS and issues
+// FM x FN MFMAs into fp32 accumulators.  The next K tile is fetched from
+// global memory into registers before the MFMAs and written to the other
+// LDS buffer after them; one barrier per K tile.
+//
+// Epilogue: acc * scale (fp8 per-tensor scales, 1 otherwise), rounded to
+// nearest-even into bf16 (bf16 and fp8 inputs) or fp16 (fp16 inputs), and
+// stored with bounds checks.  beta = 0: C is overwritten.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "gdy_internal.h"
+
+namespace gdy {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kRowBytes = 128;  // bytes of K held per LDS row
+constexpr int kStride = 144;    // LDS row stride in bytes
+
+template <int DT> struct ElemSize;
+template <> struct ElemSize<DT_BF16> { static constexpr int v = 2; };
+template <> struct ElemSize<DT_F16> { static constexpr int v = 2; };
+template <> struct ElemSize<DT_FP8> { static constexpr int v = 1; };
+
+// ---------------------------------------------------------------------------
+// MFMA wrappers.  Frag is one lane's operand fragment (FB bytes of K for one
+// row of A or one column of B); Acc is one lane's share of an MM x MM block.
+// Output layout (CDNA matrix-core convention): for 32x32 blocks, accumulator
+// r of lane l is row 8*(r/4) + 4*(l/32) + r%4, column l%32; for 16x16
+// blocks, row 4*(l/16) + r, column l%16.  Lanes l and l' with l%MM equal
+// hold the same row of A (column of B) at different K offsets; A and B use
+// the same K assignment, so any consistent lane->K mapping is a valid sum.
+// ---------------------------------------------------------------------------
+template <int DT, int MM> struct Mma;
+
+template <> struct Mma<DT_BF16, 32> {
+  typedef u32x4 Frag;
+  typedef f32x16 Acc;
+  static constexpr int FB = 16, NACC = 16;
+  static __device__ __forceinline__ Acc run(Frag a, Frag b, Acc c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  }
+};
+template <> struct Mma<DT_BF16, 16> {
+  typedef u32x4 Frag;
+  typedef f32x4 Acc;
+  static constexpr int FB = 16, NACC = 4;
+  static __device__ __forceinline__ Acc run(Frag a, Frag b, Acc c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  }
+};
+template <> struct Mma<DT_F16, 32> {
+  typedef u32x4 Frag;
+  typedef f32x16 Acc;
+  static constexpr int FB = 16, NACC = 16;
+  static __device__ __forceinline__ Acc run(Frag a, Frag b, Acc c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
+                                                  __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  }
+};
+template <> struct Mma<DT_F16, 16> {
+  typedef u32x4 Frag;
+  typedef f32x4 Acc;
+  static constexpr int FB = 16, NACC = 4;
+  static __device__ __forceinline__ Acc run(Frag a, Frag b, Acc c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                  __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  }
+};
+// fp8: the f8f6f4 MFMAs with format 0 (OCP E4M3) for both operands and unit
+// block scales (E8M0 exponent 127 = 2^0).  32 bytes of K per lane.
+template <> struct Mma<DT_FP8, 32> {
+  typedef i32x8 Frag;
+  typedef f32x16 Acc;
+  static constexpr int FB = 32, NACC = 16;
+  static __device__ __forceinline__ Acc run(Frag a, Frag b, Acc c) {
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
+  }
+};
+template <> struct Mma<DT_FP8, 16> {
+  typedef i32x8 Frag;
+  typedef f32x4 Acc;
+  static constexpr int FB = 32, NACC = 4;
+  static __device__ __forceinline__ Acc run(Frag a, Frag b, Acc c) {
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
+  }
+};
+
+template <class Frag> struct FragLoad;
+template <> struct FragLoad<u32x4> {
+  static __device__ __forceinline__ u32x4 run(const uint8_t* p) {
+    return *reinterpret_cast<const u32x4*>(p);
+  }
+};
+template <> struct FragLoad<i32x8> {
+  static __device__ __forceinline__ i32x8 run(const uint8_t* p) {
+    u32x4 lo = *reinterpret_cast<const u32x4*>(p);
+    u32x4 hi = *reinterpret_cast<const u32x4*>(p + 16);
+    i32x8 r;
+    r[0] = lo[0]; r[1] = lo[1]; r[2] = lo[2]; r[3] = lo[3];
+    r[4] = hi[0]; r[5] = hi[1]; r[6] = hi[2]; r[7] = hi[3];
+    return r;
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Global -> register -> LDS staging of one operand tile of ROWS x BK.
+//
+// Global reads go through raw buffer resources whose size is the operand's
+// exact extent in bytes, with 32-bit byte offsets: a read past the extent
+// returns zero and never touches memory.  Rows past the matrix edge start
+// past the extent, so they read as zero; elements past the K edge inside a
+// row are zeroed explicitly (they would otherwise mix into valid outputs).
+// ---------------------------------------------------------------------------
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr int kRsrcWord3 = 0x00020000;  // raw 32-bit data format, gfx9 family
+
+__device__ __forceinline__ Rsrc make_rsrc(const void* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kRsrcWord3);
+}
+
+template <int ES>
+__device__ __forceinline__ unsigned load_elem(Rsrc r, int off) {
+  if (ES == 2) return (unsigned)__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+  return (unsigned)__builtin_amdgcn_raw_buffer_load_b8(r, off, 0, 0);
+}
+
+// Operand that is K-contiguous in global memory: row r, k at byte
+// r*ld_bytes + k*ES.  Each 128-byte LDS row is 8 chunks of 16 bytes; thread
+// t moves chunks t, t+NT, ... (chunk c -> row c/8, piece c%8).
+template <int ES, int ROWS, int NT>
+struct StageK {
+  static constexpr int KPACK = 16 / ES;  // elements per chunk
+  static constexpr int CHUNKS = ROWS * 8;
+  static constexpr int NCH = (CHUNKS + NT - 1) / NT;
+  u32x4 r[NCH];
+
+  __device__ __forceinline__ void load(Rsrc src, int ld_bytes, int row0, int k0, int K, bool vec,
+                                       int tid) {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int c = tid + i * NT;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if ((CHUNKS % NT == 0) || c < CHUNKS) {
+        const int gk = k0 + (c & 7) * KPACK;
+        const int off = (row0 + (c >> 3)) * ld_bytes + gk * ES;
+        if (vec) {
+          v = __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0);
+        } else {
+#pragma unroll
+          for (int e = 0; e < KPACK; ++e) {
+            const int bit = e * ES * 8;
+            v[bit >> 5] |= load_elem<ES>(src, off + e * ES) << (bit & 31);
+          }
+        }
+        if (gk + KPACK > K) {  // K edge inside this chunk
+#pragma unroll
+          for (int e = 0; e < KPACK; ++e) {
+            const int bit = e * ES * 8;
+            const unsigned keep = (gk + e < K) ? 0xffffffffu : 0u;
+            const unsigned field = (ES == 2 ? 0xffffu : 0xffu) << (bit & 31);
+            v[bit >> 5] &= ~field | keep;
+          }
+        }
+      }
+      r[i] = v;
+    }
+  }
+
+  __device__ __forceinline__ void store(uint8_t* lds, int tid) const {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int c = tid + i * NT;
+      if ((CHUNKS % NT == 0) || c < CHUNKS)
+        *reinterpret_cast<u32x4*>(lds + (c >> 3) * kStride + (c & 7) * 16) = r[i];
+    }
+  }
+};
+
+// Operand stored k-major in global memory: row r, k at byte
+// k*ld_bytes + r*ES.  A block is KPACK consecutive k by 8 consecutive rows;
+// it is loaded as KPACK row-vectors of 8 elements and transposed in
+// registers into 8 K-vectors of 16 bytes.  Block b: k-block b%8, row-block
+// b/8, so the 8 lanes sharing a row-block fill one 128-byte LDS row.
+// k-rows past the K edge start past the extent and read as zero; elements
+// past the row edge only feed outputs that are never stored.
+template <int ES, int ROWS, int NT>
+struct StageT {
+  static constexpr int KPACK = 16 / ES;  // k per block (8 or 16)
+  static constexpr int W = 8 * ES / 4;   // 32-bit words per 8-element row-vector
+  static constexpr int BLOCKS = ROWS;    // (BK/KPACK = 8) x (ROWS/8)
+  static constexpr int NB = (BLOCKS + NT - 1) / NT;
+  unsigned in[NB][KPACK][W];
+
+  __device__ __forceinline__ void load(Rsrc src, int ld_bytes, int row0, int k0, int /*K*/,
+                                       bool vec, int tid) {
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int b = tid + i * NT;
+      const bool live = (BLOCKS % NT == 0) || b < BLOCKS;
+      const int base = (k0 + (b & 7) * KPACK) * ld_bytes + (row0 + (b >> 3) * 8) * ES;
+#pragma unroll
+      for (int r = 0; r < KPACK; ++r) {
+#pragma unroll
+        for (int w = 0; w < W; ++w) in[i][r][w] = 0u;
+        if (!live) continue;
+        const int off = base + r * ld_bytes;
+        if (vec) {
+          if (W == 4) {
+            u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0);
+#pragma unroll
+            for (int w = 0; w < W; ++w) in[i][r][w] = v[w];
+          } else {
+            u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(src, off, 0, 0);
+#pragma unroll
+            for (int w = 0; w < W; ++w) in[i][r][w] = v[w];
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int bit = e * ES * 8;
+            in[i][r][bit >> 5] |= load_elem<ES>(src, off + e * ES) << (bit & 31);
+          }
+        }
+      }
+    }
+  }
+
+  __device__ __forceinline__ void store(uint8_t* lds, int tid) const {
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int b = tid + i * NT;
+      if (!((BLOCKS % NT == 0) || b < BLOCKS)) continue;
+      uint8_t* dst = lds + (b >> 3) * 8 * kStride + (b & 7) * 16;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {  // row (m or n) within the block
+        u32x4 o;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (ES == 2) {
+            // k pairs (2j, 2j+1) of row c
+            const unsigned lo = (in[i][2 * j][c >> 1] >> ((c & 1) * 16)) & 0xffffu;
+            const unsigned hi = (in[i][2 * j + 1][c >> 1] >> ((c & 1) * 16)) & 0xffffu;
+            o[j] = lo | (hi << 16);
+          } else {
+            // k quads (4j .. 4j+3) of row c
+            const int sh = (c & 3) * 8;
+            const unsigned b0 = (in[i][4 * j + 0][c >> 2] >> sh) & 0xffu;
+            const unsigned b1 = (in[i][4 * j + 1][c >> 2] >> sh) & 0xffu;
+            const unsigned b2 = (in[i][4 * j + 2][c >> 2] >> sh) & 0xffu;
+            const unsigned b3 = (in[i][4 * j + 3][c >> 2] >> sh) & 0xffu;
+            o[j] = b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
+          }
+        }
+        *reinterpret_cast<u32x4*>(dst + c * kStride) = o;
+      }
+    }
+  }
+};
+
+template <bool KCONT, int ES, int ROWS, int NT> struct StageSel;
+template <int ES, int ROWS, int NT> struct StageSel<true, ES, ROWS, NT> { typedef StageK<ES, ROWS, NT> T; };
+template <int ES, int ROWS, int NT> struct StageSel<false, ES, ROWS, NT> { typedef StageT<ES, ROWS, NT> T; };
+
+// fp32 -> output element, round to nearest even.
+template <int DT> __device__ __forceinline__ uint16_t to_out(float x);
+template <> __device__ __forceinline__ uint16_t to_out<DT_F16>(float x) {
+  return __builtin_bit_cast(uint16_t, (_Float16)x);
+}
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
+  unsigned u = __builtin_bit_cast(unsigned, x);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);  // quiet NaN
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+template <> __device__ __forceinline__ uint16_t to_out<DT_BF16>(float x) { return f32_to_bf16_rne(x); }
+template <> __device__ __forceinline__ uint16_t to_out<DT_FP8>(float x) { return f32_to_bf16_rne(x); }
+
+// ---------------------------------------------------------------------------
+// Tile order: logical tile ids are laid out so that the first
+// floor(T/8)*8 ids dealt round-robin to the 8 XCDs land on one XCD in
+// consecutive runs, then grouped by GROUP_M tile rows so neighbours share
+// A rows and B columns in that XCD's L2.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void tile_coords(int t, const KArgs& p, int& tm, int& tn) {
+  const int T = p.tiles_m * p.tiles_n;
+  int logical = t;
+  if (p.xcd_remap) {
+    const int per = T >> 3;
+    if (t < per * 8) logical = (t & 7) * per + (t >> 3);
+  }
+  const int gm = p.group_m;
+  const int group_size = gm * p.tiles_n;
+  const int group = logical / group_size;
+  const int first_m = group * gm;
+  const int rows_here = min(p.tiles_m - first_m, gm);
+  const int in_group = logical - group * group_size;
+  tm = first_m + in_group % rows_here;
+  tn = in_group / rows_here;
+}
+
+template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int MM>
+struct GoCfg {
+  static constexpr int ES = ElemSize<DT>::v;
+  static constexpr int BK = kRowBytes / ES;
+  static constexpr int NT = WM * WN * 64;
+  static constexpr int WTM = BM / WM, WTN = BN / WN;
+  static constexpr int FM = WTM / MM, FN = WTN / MM;
+  typedef Mma<DT, MM> M;
+  static constexpr int G = 64 / MM;
+  static constexpr int KSTEP_BYTES = G * M::FB;
+  static constexpr int NKSTEP = kRowBytes / KSTEP_BYTES;
+  static constexpr int A_BYTES = BM * kStride;
+  static constexpr int B_BYTES = BN * kStride;
+  static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+  static constexpr int LDS = 2 * STAGE_BYTES;
+  static_assert(WTM % MM == 0 && WTN % MM == 0, "wave tile must hold whole MFMA blocks");
+  static_assert(kRowBytes % KSTEP_BYTES == 0, "K step must divide the LDS row");
+  static_assert(BM % 8 == 0 && BN % 8 == 0, "tiles are whole 8-row blocks");
+  static_assert(LDS <= 160 * 1024, "LDS budget");
+};
+
+template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int MM>
+__global__ void __launch_bounds__(WM * WN * 64)
+go_gemm(KArgs p) {
+  typedef GoCfg<DT, TA, TB, BM, BN, WM, WN, MM> C;
+  typedef typename C::M M;
+  typedef typename M::Frag Frag;
+  typedef typename M::Acc Acc;
+  typedef typename StageSel<TA == 0, C::ES, BM, C::NT>::T StA;
+  typedef typename StageSel<TB == 1, C::ES, BN, C::NT>::T StB;
+
+  __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave / WN;
+  const int wn = wave % WN;
+  const int ntiles = p.tiles_m * p.tiles_n;
+  const int K = (int)p.k;
+  const int nk = (K + C::BK - 1) / C::BK;
+  const Rsrc ra = make_rsrc(p.a, p.a_bytes);
+  const Rsrc rb = make_rsrc(p.b, p.b_bytes);
+  const Rsrc rc = make_rsrc(p.c, p.c_bytes);
+  const int lda_b = (int)p.lda * C::ES;
+  const int ldb_b = (int)p.ldb * C::ES;
+  const int ldc_b = (int)p.ldc * 2;
+  const int Mrows = (int)p.m, Ncols = (int)p.n;
+
+  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    int tm, tn;
+    tile_coords(t, p, tm, tn);
+    const int m0 = tm * BM;
+    const int n0 = tn * BN;
+
+    Acc acc[C::FM][C::FN];
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+        for (int r = 0; r < M::NACC; ++r) acc[i][j][r] = 0.f;
+
+    if (nk > 0) {
+      StA sa;
+      StB sb;
+      sa.load(ra, lda_b, m0, 0, K, p.a_vec, tid);
+      sb.load(rb, ldb_b, n0, 0, K, p.b_vec, tid);
+      sa.store(smem, tid);
+      sb.store(smem + C::A_BYTES, tid);
+      __syncthreads();
+
+      for (int kt = 0; kt < nk; ++kt) {
+        const bool more = kt + 1 < nk;
+        if (more) {
+          sa.load(ra, lda_b, m0, (kt + 1) * C::BK, K, p.a_vec, tid);
+          sb.load(rb, ldb_b, n0, (kt + 1) * C::BK, K, p.b_vec, tid);
+        }
+        const uint8_t* As = smem + (kt & 1) * C::STAGE_BYTES;
+        const uint8_t* Bs = As + C::A_BYTES;
+        const int frow = lane % MM;
+        const int fk = (lane / MM) * M::FB;
+#pragma unroll
+        for (int ks = 0; ks < C::NKSTEP; ++ks) {
+          Frag af[C::FM], bf[C::FN];
+#pragma unroll
+          for (int i = 0; i < C::FM; ++i)
+            af[i] = FragLoad<Frag>::run(As + (wm * C::WTM + i * MM + frow) * kStride +
+                                        ks * C::KSTEP_BYTES + fk);
+#pragma unroll
+          for (int j = 0; j < C::FN; ++j)
+            bf[j] = FragLoad<Frag>::run(Bs + (wn * C::WTN + j * MM + frow) * kStride +
+                                        ks * C::KSTEP_BYTES + fk);
+#pragma unroll
+          for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::FN; ++j) acc[i][j] = M::run(af[i], bf[j], acc[i][j]);
+        }
+        if (more) {
+          uint8_t* dst = smem + ((kt + 1) & 1) * C::STAGE_BYTES;
+          sa.store(dst, tid);
+          sb.store(dst + C::A_BYTES, tid);
+        }
+        __syncthreads();
+      }
+    }
+
+    // epilogue: scale, round, bounds-checked 16-bit stores
+    const float s = p.scale;
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) {
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j) {
+        const int col = n0 + wn * C::WTN + j * MM + (lane % MM);
+#pragma unroll
+        for (int r = 0; r < M::NACC; ++r) {
+          int rr;
+          if (MM == 32)
+            rr = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          else
+            rr = 4 * (lane >> 4) + r;
+          const int row = m0 + wm * C::WTM + i * MM + rr;
+          if (row < Mrows && col < Ncols)
+            __builtin_amdgcn_raw_buffer_store_b16(to_out<DT>(acc[i][j][r] * s), rc,
+                                                  row * ldc_b + col * 2, 0, 0);
+        }
+      }
+    }
+  }
+}
+
+}  // namespace gdy
+
+// Catalogue entry for one instantiation.
+#define GDY_KERNEL(DT, DTNAME, TA, TB, LAYOUT, BM, BN, WM, WN, MM)                                   \
+  {DTNAME "_" LAYOUT "_" #BM "x" #BN "_w" #WM "x" #WN "_m" #MM,                                       \
+   DT, TA, TB, BM, BN, ::gdy::GoCfg<DT, TA, TB, BM, BN, WM, WN, MM>::BK, WM * WN,                      \
+   MM, ::gdy::GoCfg<DT, TA, TB, BM, BN, WM, WN, MM>::LDS,                                             \
+   reinterpret_cast<const void*>(&::gdy::go_gemm<DT, TA, TB, BM, BN, WM, WN, MM>)}

@@ -2,6 +2,10 @@
 import os
 import sys
 
+# concurrency degrees up to 16 need as many HIP hardware queues; must be set
+# before anything in the test process initialises HIP
+os.environ.setdefault("GPU_MAX_HW_QUEUES", "16")
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)

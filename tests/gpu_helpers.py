@@ -1,0 +1,63 @@
+"""Helpers for GPU parity tests: run GEMMs through the C-ABI and compare
+them with the CPU oracle (the error bound of the spec contract:
+|c - ref| <= tau * sum_k |a b| + 1e-6, tau = 2^-7 for 16-bit inputs and
+2^-3 for fp8)."""
+import numpy as np
+import torch
+
+import oracle
+from paper_2409_02227_amd import inputs
+
+TAU = {"bf16": 2.0 ** -7, "f16": 2.0 ** -7, "fp8": 2.0 ** -3}
+ORC = {"bf16": "bf16", "f16": "f16", "fp8": "e4m3fn"}
+FULL_LIMIT = 3e8  # multiply-adds the oracle does in full; above: sampled
+
+
+def out_codes(mat) -> np.ndarray:
+    """Output codes (M x N, uint16) copied to the host."""
+    return mat.c.cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def decode_out(mat) -> np.ndarray:
+    return oracle.decode(out_codes(mat), "f16" if mat.spec.dtype == "f16" else "bf16")
+
+
+def check(mat, rng=None, samples=8, label=""):
+    """Compare one materialised GEMM with the oracle; returns worst ratio."""
+    s = mat.spec
+    dt = ORC[s.dtype]
+    got = decode_out(mat)
+    if s.m * s.n * s.k <= FULL_LIMIT:
+        ref, bound = oracle.gemm(s.m, s.n, s.k, mat.host["a"], dt, s.ld("a"), mat.host["b"], dt,
+                                 s.ld("b"), s.trans_a, s.trans_b, mat.scale_a, mat.scale_b)
+        ok, worst = oracle.accept(got, ref, bound, TAU[s.dtype])
+    else:
+        rng = rng or np.random.default_rng(s.seed)
+        rows = rng.choice(s.m, size=min(samples, s.m), replace=False)
+        cols = rng.choice(s.n, size=min(samples, s.n), replace=False)
+        if s.m <= 32:
+            rows = np.arange(s.m)
+        ii = np.concatenate([np.repeat(rows, s.n), np.tile(np.arange(s.m), len(cols))])
+        jj = np.concatenate([np.tile(np.arange(s.n), len(rows)), np.repeat(cols, s.m)])
+        ref, bound = oracle.gemm_entries(s.m, s.n, s.k, mat.host["a"], dt, s.ld("a"),
+                                         mat.host["b"], dt, s.ld("b"), ii, jj, s.trans_a,
+                                         s.trans_b, mat.scale_a, mat.scale_b)
+        ok, worst = oracle.accept(got[ii, jj], ref, bound, TAU[s.dtype])
+    assert ok, f"{label} {s.name} ({s.m},{s.n},{s.k},{s.dtype},t{s.trans_a}{s.trans_b}): " \
+               f"outside bound, worst ratio {worst:.3g}"
+    # columns between n and ldc must be untouched (they were NaN)
+    if s.pad_c:
+        pad = mat.c_full[:, s.n:].float()
+        assert torch.isnan(pad).all().item(), f"{label} {s.name}: wrote into C padding"
+    return worst
+
+
+def gemm_of(mat, variant=-1):
+    from paper_2409_02227_amd import gdy
+    return gdy.Gemm(mat.a, mat.b, mat.c, mat.spec.trans_a, mat.spec.trans_b,
+                    mat.scale_a, mat.scale_b, mat.spec.tenant, variant)
+
+
+def reset_outputs(mats):
+    for m in mats:
+        m.c_full.fill_(float("nan"))

@@ -1,0 +1,49 @@
+"""CPU checks of the C-ABI boundary: the built library loads and exports
+every function include/gdy.h declares, and the binding's structures match
+the header's field order and sizes."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2409_02227_amd import gdy
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gdy.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gdy_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_exports():
+    assert declared_functions() == sorted(gdy.EXPORTS)
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    if not os.path.exists(gdy.LIB_PATH):
+        pytest.fail("libgdy.so not built: run __graft_entry__.build()")
+    lib = ctypes.CDLL(gdy.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), f"{name} declared in gdy.h but not exported"
+
+
+def test_struct_layouts_match_header():
+    # gdy_gemm: 3 int64, 5 int32, then (ptr, int64) x 3, 2 floats, 2 int32
+    assert ctypes.sizeof(gdy.GemmDesc) == 3 * 8 + 5 * 4 + 4 + 6 * 8 + 2 * 4 + 2 * 4
+    assert gdy.GemmDesc.a.offset == 48
+    assert ctypes.sizeof(gdy.Plan) == 4 * 4 + 6 * 4 * gdy.MAX_GEMMS
+    assert ctypes.sizeof(gdy.VariantDesc) == 64 + 12 * 4
+    text = open(HEADER).read()
+    assert "#define GDY_MAX_GEMMS 256" in text and "#define GDY_N_FEATURES 18" in text
+
+
+def test_status_strings_without_device():
+    lib = gdy.load_library()
+    assert lib.gdy_status_string(0) == b"ok"
+    assert lib.gdy_status_string(3).startswith(b"output aliases")
+    assert lib.gdy_last_error(None) == b"null context"
+    assert lib.gdy_variant_count(None) == 0

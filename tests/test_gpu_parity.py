@@ -1,0 +1,222 @@
+"""GPU parity: every GO-Kernel and every execution mode against the CPU
+oracle, through the C-ABI (libgdy.so via the ctypes binding).
+
+Bar (spec contract): |gpu - ref| <= tau * sum_k |a(i,k) b(k,j)| + 1e-6
+with tau = 2^-7 for bf16/fp16 inputs and 2^-3 for fp8; results of one
+variant are bit-identical between isolated and concurrent execution.
+"""
+import itertools
+import os
+
+import numpy as np
+import pytest
+
+import paper_2409_02227_amd  # noqa: F401  (sets GPU_MAX_HW_QUEUES before HIP starts)
+
+torch = pytest.importorskip("torch")
+
+from paper_2409_02227_amd import gdy, inputs  # noqa: E402
+from paper_2409_02227_amd.inputs import GemmSpec  # noqa: E402
+from tests.gpu_helpers import check, gemm_of, out_codes, reset_outputs  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+DT_NAME = {1: "f16", 2: "bf16", 3: "fp8"}
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    c = gdy.Context(0, max_streams=16)
+    yield c
+    c.close()
+
+
+def _run(ctx, mats, mode, forced_cd=0, variants=None):
+    reset_outputs(mats)
+    gemms = [gemm_of(m, -1 if variants is None else variants[i]) for i, m in enumerate(mats)]
+    plan = ctx.execute(gemms, mode=mode, forced_cd=forced_cd, want_plan=True)
+    torch.cuda.synchronize()
+    return plan
+
+
+def _kernels(ctx):
+    """Uncapped variant of every kernel in the catalogue."""
+    return [(i, v) for i, v in enumerate(ctx.variants()) if v["grid_cap_cus"] == 0]
+
+
+def test_every_kernel_ragged_tiles(ctx):
+    """Each kernel on a shape spanning several tiles with ragged M, N and K
+    tails (K tail inside a 16-byte chunk too)."""
+    for vid, v in _kernels(ctx):
+        bm, bn, bk = v["bm"], v["bn"], v["bk"]
+        dt = DT_NAME[v["dtype"]]
+        spec = GemmSpec(2 * bm - 5, bn + 3, 2 * bk + 37 if dt != "fp8" else bk + 53, dt,
+                        v["trans_a"], v["trans_b"], seed=vid, name=v["name"])
+        mat = inputs.materialize(spec)
+        _run(ctx, [mat], "forced", 1, [vid])
+        check(mat, label=v["name"])
+
+
+def test_every_kernel_aligned_multi_tile(ctx):
+    """Each kernel on exact multiples of its tile (vector-load fast path)."""
+    for vid, v in _kernels(ctx):
+        dt = DT_NAME[v["dtype"]]
+        spec = GemmSpec(v["bm"] * 2, v["bn"] * 2, v["bk"] * 3, dt, v["trans_a"], v["trans_b"],
+                        seed=1000 + vid, name=v["name"])
+        mat = inputs.materialize(spec)
+        _run(ctx, [mat], "forced", 1, [vid])
+        check(mat, label=v["name"])
+
+
+@pytest.mark.parametrize("dt,ta,tb", [(d, a, b) for d in ("bf16", "f16", "fp8")
+                                      for a, b in itertools.product([0, 1], [0, 1])])
+def test_odd_leading_dims_and_tiny_shapes(ctx, dt, ta, tb):
+    """ld > minimal and unaligned (element-wise load path), M = 1, K = 1,
+    K below one K tile, and C padding that must stay untouched."""
+    shapes = [(1, 1, 1), (1, 77, 300), (5, 3, 1), (33, 65, 17), (130, 70, 200)]
+    for i, (m, n, k) in enumerate(shapes):
+        spec = GemmSpec(m, n, k, dt, ta, tb, seed=50 + i, pad_a=3, pad_b=5, pad_c=7,
+                        name=f"odd{i}")
+        mat = inputs.materialize(spec)
+        _run(ctx, [mat], "sequential")
+        check(mat, label=f"{dt} t{ta}{tb}")
+
+
+def test_k_zero_writes_zeros_and_empty_is_noop(ctx):
+    spec = GemmSpec(40, 50, 0, "bf16", seed=1, name="k0")
+    mat = inputs.materialize(spec)
+    empty = inputs.materialize(GemmSpec(0, 50, 64, "bf16", seed=2, name="m0"))
+    _run(ctx, [mat, empty], "default")
+    assert (mat.c.float() == 0).all().item()
+
+
+def test_grid_caps_are_bit_identical(ctx):
+    """A grid cap changes which workgroup runs a tile, never the tile's sum."""
+    spec = GemmSpec(700, 900, 650, "bf16", seed=77, name="caps")
+    mat = inputs.materialize(spec)
+    by_kernel = {}
+    for vid, v in enumerate(ctx.variants()):
+        if v["dtype"] == 2 and v["trans_a"] == 0 and v["trans_b"] == 0:
+            by_kernel.setdefault(v["name"].rsplit("_c", 1)[0], []).append(vid)
+    for name, vids in by_kernel.items():
+        ref = None
+        for vid in vids:
+            _run(ctx, [mat], "forced", 1, [vid])
+            got = out_codes(mat).copy()
+            if ref is None:
+                check(mat, label=name)
+                ref = got
+            assert np.array_equal(got, ref), f"{name}: cap variant {vid} differs"
+
+
+def test_concurrent_equals_isolated_bitwise(ctx):
+    """Same variant: isolated, then 8 concurrent on 8 streams, same bits."""
+    specs = [GemmSpec(300, 1000, 700, "bf16", seed=200 + i, name=f"c{i}") for i in range(8)]
+    mats = [inputs.materialize(s) for s in specs]
+    vid = ctx.find("bf16_nn_128x128_w2x2_m32_c0")
+    assert vid >= 0
+    iso = []
+    for m in mats:
+        _run(ctx, [m], "forced", 1, [vid])
+        iso.append(out_codes(m).copy())
+    for rep in range(3):
+        _run(ctx, mats, "forced", 8, [vid] * 8)
+        for m, ref in zip(mats, iso):
+            assert np.array_equal(out_codes(m), ref), f"rep {rep} {m.spec.name} differs"
+    check(mats[0])
+
+
+@pytest.mark.parametrize("mode", ["sequential", "default", "go", "selector"])
+def test_config1_and_config2_full(ctx, mode):
+    for specs in (inputs.config1(), inputs.config2()):
+        mats = [inputs.materialize(s) for s in specs]
+        plan = _run(ctx, mats, mode)
+        assert sorted(plan["order"]) == list(range(len(specs)))
+        for m in mats:
+            check(m, label=mode)
+
+
+def test_config3_sampled(ctx):
+    mats = [inputs.materialize(s) for s in inputs.config3()]
+    for mode in ("sequential", "selector"):
+        _run(ctx, mats, mode)
+        for m in mats:
+            check(m, samples=6, label=mode)
+
+
+def test_config5_fp8_sampled(ctx):
+    mats = [inputs.materialize(s) for s in inputs.config5()]
+    for mode in ("sequential", "default"):
+        _run(ctx, mats, mode)
+        for m in mats:
+            check(m, samples=4, label=mode)
+
+
+def test_config4_first_submissions_sampled(ctx):
+    subs = inputs.config4(count=3)
+    for sub in subs:
+        mats = [inputs.materialize(s) for s in sub]
+        _run(ctx, mats, "selector")
+        for m in mats:
+            check(m, samples=3, label="selector")
+
+
+def test_validation_errors(ctx):
+    a = torch.zeros(64, 64, dtype=torch.bfloat16, device="cuda")
+    b = torch.zeros(64, 64, dtype=torch.bfloat16, device="cuda")
+    c = torch.zeros(64, 64, dtype=torch.bfloat16, device="cuda")
+    ok = gdy.Gemm(a, b, c)
+    with pytest.raises(gdy.GdyError) as e:
+        ctx.execute([gdy.Gemm(a, b, a)])  # C aliases A
+    assert e.value.status == 3
+    with pytest.raises(gdy.GdyError) as e:
+        ctx.execute([ok, gdy.Gemm(a, b, c)])  # two GEMMs write the same C
+    assert e.value.status == 3
+    d = ok.desc()
+    d.lda = 10
+    with pytest.raises(gdy.GdyError) as e:
+        ctx.execute([d])
+    assert e.value.status == 1
+    d = ok.desc()
+    d.c_type = 1
+    with pytest.raises(gdy.GdyError) as e:
+        ctx.execute([d])
+    assert e.value.status == 2
+    d = ok.desc()
+    d.scale_a = 2.0
+    with pytest.raises(gdy.GdyError) as e:
+        ctx.execute([d])
+    assert e.value.status == 1
+    with pytest.raises(gdy.GdyError) as e:
+        ctx.execute([ok] * 257)
+    assert e.value.status == 4
+    d = ok.desc()
+    d.variant = 10 ** 6
+    with pytest.raises(gdy.GdyError) as e:
+        ctx.execute([d], mode="forced", forced_cd=1)
+    assert e.value.status == 1
+    # nothing was launched by the failed calls: C still zero
+    torch.cuda.synchronize()
+    assert (c.float() == 0).all().item()
+
+
+def test_concurrent_kernels_overlap(ctx):
+    """With CD > 1 the per-kernel intervals overlap (streams really run
+    concurrently; needs GPU_MAX_HW_QUEUES >= the CD)."""
+    specs = [GemmSpec(64, 4096, 4096, "bf16", seed=300 + i, name=f"ov{i}") for i in range(4)]
+    mats = [inputs.materialize(s) for s in specs]
+    ctx.set_timing(True)
+    try:
+        best = 0.0
+        for _ in range(5):
+            _run(ctx, mats, "default")
+            st, en = ctx.kernel_times(4)
+            iv = sorted(zip(st, en))
+            ov = max(0.0, min(e for _, e in iv) - max(s for s, _ in iv))
+            best = max(best, ov)
+        print("GPU_MAX_HW_QUEUES", os.environ.get("GPU_MAX_HW_QUEUES"), "overlap ms", best)
+        assert best > 0.0, f"kernels never overlapped: {iv}"
+    finally:
+        ctx.set_timing(False)
