@@ -131,6 +131,11 @@ typedef struct gdy_ctx gdy_ctx;
  * `use_cu_masks` != 0 also creates CU-masked pools for the resource
  * constraints GPU/2, GPU/4 and GPU/8 (used by the tuner).  On error *out is
  * NULL.
+ *
+ * device < 0 creates a host-only context that plans without a GPU: its CU
+ * count is GDY_HOST_CUS (default 256) or the loaded table's, kernel
+ * occupancy comes from LDS size and wave count alone, the table's device
+ * line is not checked, and gdy_execute returns GDY_ERR_UNSUPPORTED.
  */
 gdy_status gdy_create(gdy_ctx** out, int device, const char* table_path, int32_t max_streams,
                       int32_t use_cu_masks);

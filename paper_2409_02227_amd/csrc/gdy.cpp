@@ -89,6 +89,7 @@ struct gdy_ctx {
   std::vector<hipStream_t> pool;                   // whole GPU
   std::vector<std::vector<hipStream_t>> rc_pools;  // one per kRcBudgets entry
   int rc = 0;                                      // active CU budget, 0 = whole GPU
+  int host_slots = 0;                              // host-only context: planned stream slots
   std::vector<hipEvent_t> done;                    // one per stream slot
   hipEvent_t fork_ev = nullptr;
   bool timing = false;
@@ -367,6 +368,7 @@ void plan_reset(gdy_plan_t* p, int n) {
 bool active(const gdy_gemm& g) { return g.m > 0 && g.n > 0; }
 
 int pool_size(const gdy_ctx* ctx) {
+  if (ctx->device < 0) return ctx->host_slots;
   if (ctx->rc == 0) return (int)ctx->pool.size();
   for (size_t r = 0; r < ctx->rc_pools.size(); ++r)
     if (kRcBudgets[r] == ctx->rc) return (int)ctx->rc_pools[r].size();
@@ -483,6 +485,16 @@ bool vec_ok(const void* ptr, int64_t ld, int es, bool kcontiguous) {
   return a % 8 == 0 && (ld * es) % 8 == 0;  // fp8 k-major operand: 8-byte row vectors
 }
 
+// Buffer size for reads: the extent rounded up to the end of the dword that
+// holds its last byte.  The buffer unit drops a multi-dword read's dwords
+// that end past the size, so an exact size would zero a last element that
+// shares its dword with bytes past the extent; that dword is mapped memory.
+int32_t read_records(const void* base, int64_t bytes) {
+  if (bytes <= 0) return 0;
+  const uintptr_t p = (uintptr_t)base;
+  return (int32_t)(((p + (uintptr_t)bytes + 3) & ~(uintptr_t)3) - p);
+}
+
 KArgs make_args(const gdy_ctx* ctx, int vid, const gdy_gemm& g, Geometry* geo_out) {
   const Kernel& k = ctx->kernels[ctx->variants[vid].kernel];
   const Geometry geo = geometry(ctx, vid, g);
@@ -505,9 +517,9 @@ KArgs make_args(const gdy_ctx* ctx, int vid, const gdy_gemm& g, Geometry* geo_ou
     if (g.trans_b) stored_extent(g.n, g.k, g.ldb, es, &bb); else stored_extent(g.k, g.n, g.ldb, es, &bb);
   }
   stored_extent(g.m, g.n, g.ldc, 2, &cb);
-  a.a_bytes = (int32_t)ab;
-  a.b_bytes = (int32_t)bb;
-  a.c_bytes = (int32_t)cb;
+  a.a_bytes = read_records(g.a, ab);
+  a.b_bytes = read_records(g.b, bb);
+  a.c_bytes = (int32_t)cb;  // stores are element-wise: exact extent
   a.tiles_m = geo.tiles_m;
   a.tiles_n = geo.tiles_n;
   a.a_vec = g.k > 0 && vec_ok(g.a, g.lda, es, g.trans_a == 0);
@@ -609,7 +621,11 @@ gdy_status load_table(gdy_ctx* ctx, const char* path) {
       std::string arch, cus_tag;
       int cus = 0;
       in >> arch >> cus_tag >> cus;
-      if (arch != ctx->arch || cus != ctx->cus)
+      if (ctx->device < 0) {
+        // host-only planning adopts the tuned device's CU count
+        if (cus <= 0) return fail(ctx, GDY_ERR_TABLE, "bad CU count in GO table");
+        ctx->cus = cus;
+      } else if (arch != ctx->arch || cus != ctx->cus)
         return fail(ctx, GDY_ERR_TABLE, "GO table is for %s/%d CUs, device is %s/%d", arch.c_str(),
                     cus, ctx->arch.c_str(), ctx->cus);
     } else if (tag == "catalogue") {
@@ -698,15 +714,32 @@ static void destroy_streams(gdy_ctx* ctx) {
   ctx->fork_ev = ctx->sub_start = nullptr;
 }
 
+// Host-only contexts (device < 0) plan without a GPU: CU count from
+// GDY_HOST_CUS (default 256) and each kernel's occupancy from its LDS and
+// wave count alone (160 KiB LDS and 32 waves per CU); they cannot execute.
+static int host_occupancy(const KernelDesc* d) {
+  const int by_lds = d->lds_bytes > 0 ? (160 * 1024) / d->lds_bytes : 32;
+  const int by_waves = 32 / d->waves;
+  return std::max(1, std::min(by_lds, by_waves));
+}
+
 static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, int32_t max_streams,
                               int32_t use_cu_masks) {
-  HIP_TRY(ctx, hipSetDevice(device));
-  hipDeviceProp_t prop;
-  HIP_TRY(ctx, hipGetDeviceProperties(&prop, device));
+  const bool host_only = device < 0;
   ctx->device = device;
-  ctx->cus = prop.multiProcessorCount;
-  ctx->arch = prop.gcnArchName;
-  ctx->arch = ctx->arch.substr(0, ctx->arch.find(':'));
+  if (host_only) {
+    const char* env = std::getenv("GDY_HOST_CUS");
+    ctx->cus = env ? std::atoi(env) : 256;
+    if (ctx->cus <= 0) return fail(ctx, GDY_ERR_INVALID_ARG, "GDY_HOST_CUS must be positive");
+    ctx->arch = "host";
+  } else {
+    HIP_TRY(ctx, hipSetDevice(device));
+    hipDeviceProp_t prop;
+    HIP_TRY(ctx, hipGetDeviceProperties(&prop, device));
+    ctx->cus = prop.multiProcessorCount;
+    ctx->arch = prop.gcnArchName;
+    ctx->arch = ctx->arch.substr(0, ctx->arch.find(':'));
+  }
 
   const KernelDesc* tabs[3];
   int counts[3];
@@ -718,12 +751,17 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
     for (int i = 0; i < counts[t]; ++i) {
       Kernel k;
       k.d = &tabs[t][i];
-      int occ = 0;
-      HIP_TRY(ctx, hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, k.d->func, k.d->waves * 64, 0));
-      hipFuncAttributes attr;
-      HIP_TRY(ctx, hipFuncGetAttributes(&attr, k.d->func));
-      k.occupancy = occ;
-      k.vgprs = attr.numRegs;
+      if (host_only) {
+        k.occupancy = host_occupancy(k.d);
+        k.vgprs = 0;
+      } else {
+        int occ = 0;
+        HIP_TRY(ctx, hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, k.d->func, k.d->waves * 64, 0));
+        hipFuncAttributes attr;
+        HIP_TRY(ctx, hipFuncGetAttributes(&attr, k.d->func));
+        k.occupancy = occ;
+        k.vgprs = attr.numRegs;
+      }
       const int kid = (int)ctx->kernels.size();
       ctx->kernels.push_back(k);
       for (int c = 0; c < kNumCaps; ++c) {
@@ -741,6 +779,11 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
 
   int S = max_streams <= 0 ? 16 : max_streams;
   if (S > 64) return fail(ctx, GDY_ERR_INVALID_ARG, "max_streams %d > 64", S);
+  if (host_only) {
+    ctx->host_slots = S;
+    if (table_path && table_path[0]) return load_table(ctx, table_path);
+    return GDY_OK;
+  }
   for (int s = 0; s < S; ++s) {
     hipStream_t st;
     HIP_TRY(ctx, hipStreamCreateWithFlags(&st, hipStreamNonBlocking));
@@ -803,6 +846,10 @@ gdy_status gdy_create(gdy_ctx** out, int device, const char* table_path, int32_t
 
 void gdy_destroy(gdy_ctx* ctx) {
   if (!ctx) return;
+  if (ctx->device < 0) {
+    delete ctx;
+    return;
+  }
   for (hipStream_t s : ctx->pool) (void)hipStreamSynchronize(s);
   for (auto& pl : ctx->rc_pools)
     for (hipStream_t s : pl) (void)hipStreamSynchronize(s);
@@ -848,6 +895,7 @@ gdy_status gdy_execute(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t m
   gdy_plan_t* p = out ? out : &local;
   gdy_status s = gdy_plan(ctx, gemms, n, mode, forced_cd, p);
   if (s != GDY_OK) return s;
+  if (ctx->device < 0) return fail(ctx, GDY_ERR_UNSUPPORTED, "host-only context cannot execute");
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess || cur != ctx->device) HIP_TRY(ctx, hipSetDevice(ctx->device));
   try {

@@ -136,11 +136,13 @@ template <> struct FragLoad<i32x8> {
 // ---------------------------------------------------------------------------
 // Global -> register -> LDS staging of one operand tile of ROWS x BK.
 //
-// Global reads go through raw buffer resources whose size is the operand's
-// exact extent in bytes, with 32-bit byte offsets: a read past the extent
-// returns zero and never touches memory.  Rows past the matrix edge start
-// past the extent, so they read as zero; elements past the K edge inside a
-// row are zeroed explicitly (they would otherwise mix into valid outputs).
+// Global reads go through raw buffer resources with 32-bit byte offsets.
+// The buffer size is the operand's extent rounded up to the end of the
+// dword holding its last byte (the unit range-checks whole dwords, and that
+// dword is always mapped): a read beyond it returns zero and never touches
+// memory.  Elements past the K edge are zeroed explicitly, since they would
+// otherwise mix into valid outputs; rows past the M/N edge only feed
+// outputs that are never stored.
 // ---------------------------------------------------------------------------
 typedef __amdgpu_buffer_rsrc_t Rsrc;
 constexpr int kRsrcWord3 = 0x00020000;  // raw 32-bit data format, gfx9 family
@@ -212,8 +214,8 @@ struct StageK {
 // it is loaded as KPACK row-vectors of 8 elements and transposed in
 // registers into 8 K-vectors of 16 bytes.  Block b: k-block b%8, row-block
 // b/8, so the 8 lanes sharing a row-block fill one 128-byte LDS row.
-// k-rows past the K edge start past the extent and read as zero; elements
-// past the row edge only feed outputs that are never stored.
+// k-rows past the K edge are never loaded (zeros); elements past the row
+// edge only feed outputs that are never stored.
 template <int ES, int ROWS, int NT>
 struct StageT {
   static constexpr int KPACK = 16 / ES;  // k per block (8 or 16)
@@ -222,18 +224,19 @@ struct StageT {
   static constexpr int NB = (BLOCKS + NT - 1) / NT;
   unsigned in[NB][KPACK][W];
 
-  __device__ __forceinline__ void load(Rsrc src, int ld_bytes, int row0, int k0, int /*K*/,
-                                       bool vec, int tid) {
+  __device__ __forceinline__ void load(Rsrc src, int ld_bytes, int row0, int k0, int K, bool vec,
+                                       int tid) {
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int b = tid + i * NT;
       const bool live = (BLOCKS % NT == 0) || b < BLOCKS;
-      const int base = (k0 + (b & 7) * KPACK) * ld_bytes + (row0 + (b >> 3) * 8) * ES;
+      const int gk0 = k0 + (b & 7) * KPACK;
+      const int base = gk0 * ld_bytes + (row0 + (b >> 3) * 8) * ES;
 #pragma unroll
       for (int r = 0; r < KPACK; ++r) {
 #pragma unroll
         for (int w = 0; w < W; ++w) in[i][r][w] = 0u;
-        if (!live) continue;
+        if (!live || gk0 + r >= K) continue;  // k-rows past the K edge stay zero
         const int off = base + r * ld_bytes;
         if (vec) {
           if (W == 4) {
