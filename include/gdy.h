@@ -180,6 +180,10 @@ gdy_status gdy_execute(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t m
  */
 gdy_status gdy_set_timing(gdy_ctx* ctx, int32_t enable);
 gdy_status gdy_last_kernel_times(gdy_ctx* ctx, float* start_ms, float* end_ms, int32_t n);
+/* Same for an earlier timed submission: back = 0 is the last one, up to 63
+ * (the context keeps the events of the last 64 timed submissions). */
+gdy_status gdy_kernel_times(gdy_ctx* ctx, int32_t back, float* start_ms, float* end_ms,
+                            int32_t n);
 
 /* Features of one GEMM (Sec. 4.3): M, N, K, then for each CD class
  * 1, 2, 4, 8, 16 the bound variant's #WGs, occupancy and #waves. */

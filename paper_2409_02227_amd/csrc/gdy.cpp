@@ -79,6 +79,15 @@ uint64_t fnv1a(const std::string& s, uint64_t h) {
 
 }  // namespace
 
+// Per-kernel timing events of one submission (created on first use).
+struct TimingSlot {
+  hipEvent_t sub_start = nullptr;
+  std::vector<hipEvent_t> start, stop;
+  std::vector<char> launched;
+  int n = 0;
+};
+const int kTimingRing = 64;
+
 struct gdy_ctx {
   int device = 0;
   int cus = 0;
@@ -93,10 +102,8 @@ struct gdy_ctx {
   std::vector<hipEvent_t> done;                    // one per stream slot
   hipEvent_t fork_ev = nullptr;
   bool timing = false;
-  hipEvent_t sub_start = nullptr;
-  std::vector<hipEvent_t> t_start, t_stop;
-  int last_n = 0;
-  std::vector<char> last_launched;
+  TimingSlot ring[kTimingRing];                    // per-kernel events of recent submissions
+  int64_t submissions = 0;                         // timed submissions so far
   Table table;
   std::string err;
 };
@@ -541,9 +548,22 @@ hipStream_t slot_stream(const gdy_ctx* ctx, int slot) {
 gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, hipStream_t origin) {
   gdy_status st = GDY_OK;
   const int n = p.n;
-  ctx->last_n = n;
-  ctx->last_launched.assign(n, 0);
-  if (ctx->timing) HIP_TRY(ctx, hipEventRecord(ctx->sub_start, origin));
+  TimingSlot* ts = nullptr;
+  if (ctx->timing) {
+    ts = &ctx->ring[ctx->submissions % kTimingRing];
+    if (!ts->sub_start) HIP_TRY(ctx, hipEventCreate(&ts->sub_start));
+    while ((int)ts->start.size() < n) {
+      hipEvent_t a, b;
+      HIP_TRY(ctx, hipEventCreate(&a));
+      HIP_TRY(ctx, hipEventCreate(&b));
+      ts->start.push_back(a);
+      ts->stop.push_back(b);
+    }
+    ts->n = n;
+    ts->launched.assign(n, 0);
+    ++ctx->submissions;
+    HIP_TRY(ctx, hipEventRecord(ts->sub_start, origin));
+  }
 
   // launch order is p.order; groups are contiguous in it
   std::vector<int> prev_slots;  // slots used by the previous group
@@ -583,14 +603,14 @@ gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, hip
       void* argv[] = {&args};
       hipStream_t hs = p.stream_of[i] >= 0 ? slot_stream(ctx, p.stream_of[i]) : origin;
       hipError_t e = hipExtLaunchKernel(k.d->func, dim3(std::max(geo.grid, 1)), dim3(k.d->waves * 64),
-                                        argv, 0, hs, ctx->timing ? ctx->t_start[i] : nullptr,
-                                        ctx->timing ? ctx->t_stop[i] : nullptr, 0);
+                                        argv, 0, hs, ts ? ts->start[i] : nullptr,
+                                        ts ? ts->stop[i] : nullptr, 0);
       if (e != hipSuccess) {
         st = fail(ctx, GDY_ERR_HIP, "launch of %s for gemm %d failed: %s",
                   ctx->variants[vid].name.c_str(), i, hipGetErrorString(e));
         break;
       }
-      ctx->last_launched[i] = 1;
+      if (ts) ts->launched[i] = 1;
     }
     for (int s : slots) HIP_TRY(ctx, hipEventRecord(ctx->done[s], slot_stream(ctx, s)));
     if (!slots.empty()) prev_slots = slots;
@@ -702,16 +722,17 @@ static void destroy_streams(gdy_ctx* ctx) {
   for (auto& pl : ctx->rc_pools)
     for (hipStream_t s : pl) (void)hipStreamDestroy(s);
   for (hipEvent_t e : ctx->done) (void)hipEventDestroy(e);
-  for (hipEvent_t e : ctx->t_start) (void)hipEventDestroy(e);
-  for (hipEvent_t e : ctx->t_stop) (void)hipEventDestroy(e);
+  for (TimingSlot& t : ctx->ring) {
+    for (hipEvent_t e : t.start) (void)hipEventDestroy(e);
+    for (hipEvent_t e : t.stop) (void)hipEventDestroy(e);
+    if (t.sub_start) (void)hipEventDestroy(t.sub_start);
+    t = TimingSlot();
+  }
   if (ctx->fork_ev) (void)hipEventDestroy(ctx->fork_ev);
-  if (ctx->sub_start) (void)hipEventDestroy(ctx->sub_start);
   ctx->pool.clear();
   ctx->rc_pools.clear();
   ctx->done.clear();
-  ctx->t_start.clear();
-  ctx->t_stop.clear();
-  ctx->fork_ev = ctx->sub_start = nullptr;
+  ctx->fork_ev = nullptr;
 }
 
 // Host-only contexts (device < 0) plan without a GPU: CU count from
@@ -807,14 +828,6 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
     }
   }
   HIP_TRY(ctx, hipEventCreateWithFlags(&ctx->fork_ev, hipEventDisableTiming));
-  HIP_TRY(ctx, hipEventCreate(&ctx->sub_start));
-  for (int i = 0; i < GDY_MAX_GEMMS; ++i) {
-    hipEvent_t a, b;
-    HIP_TRY(ctx, hipEventCreate(&a));
-    HIP_TRY(ctx, hipEventCreate(&b));
-    ctx->t_start.push_back(a);
-    ctx->t_stop.push_back(b);
-  }
   if (table_path && table_path[0]) {
     gdy_status s = load_table(ctx, table_path);
     if (s != GDY_OK) return s;
@@ -911,16 +924,23 @@ gdy_status gdy_set_timing(gdy_ctx* ctx, int32_t enable) {
   return GDY_OK;
 }
 
-gdy_status gdy_last_kernel_times(gdy_ctx* ctx, float* start_ms, float* end_ms, int32_t n) {
+gdy_status gdy_kernel_times(gdy_ctx* ctx, int32_t back, float* start_ms, float* end_ms,
+                            int32_t n) {
   if (!ctx || n < 0 || (n > 0 && (!start_ms || !end_ms))) return GDY_ERR_INVALID_ARG;
-  if (!ctx->timing) return fail(ctx, GDY_ERR_INVALID_ARG, "timing is off");
+  if (back < 0 || back >= kTimingRing || back >= ctx->submissions)
+    return fail(ctx, GDY_ERR_INVALID_ARG, "no timed submission %d back", back);
+  const TimingSlot& ts = ctx->ring[(ctx->submissions - 1 - back) % kTimingRing];
   for (int i = 0; i < n; ++i) {
     start_ms[i] = end_ms[i] = -1.f;
-    if (i >= ctx->last_n || !ctx->last_launched[i]) continue;
-    HIP_TRY(ctx, hipEventElapsedTime(&start_ms[i], ctx->sub_start, ctx->t_start[i]));
-    HIP_TRY(ctx, hipEventElapsedTime(&end_ms[i], ctx->sub_start, ctx->t_stop[i]));
+    if (i >= ts.n || !ts.launched[i]) continue;
+    HIP_TRY(ctx, hipEventElapsedTime(&start_ms[i], ts.sub_start, ts.start[i]));
+    HIP_TRY(ctx, hipEventElapsedTime(&end_ms[i], ts.sub_start, ts.stop[i]));
   }
   return GDY_OK;
+}
+
+gdy_status gdy_last_kernel_times(gdy_ctx* ctx, float* start_ms, float* end_ms, int32_t n) {
+  return gdy_kernel_times(ctx, 0, start_ms, end_ms, n);
 }
 
 gdy_status gdy_features(gdy_ctx* ctx, const gdy_gemm* gemm, double* out_features) {

@@ -30,7 +30,8 @@ STATUS = {0: "GDY_OK", 1: "GDY_ERR_INVALID_ARG", 2: "GDY_ERR_UNSUPPORTED", 3: "G
           4: "GDY_ERR_TOO_MANY", 5: "GDY_ERR_TABLE", 6: "GDY_ERR_HIP", 7: "GDY_ERR_NOMEM"}
 
 EXPORTS = ("gdy_create", "gdy_destroy", "gdy_set_rc", "gdy_plan", "gdy_execute",
-           "gdy_set_timing", "gdy_last_kernel_times", "gdy_features", "gdy_variant_count",
+           "gdy_set_timing", "gdy_last_kernel_times", "gdy_kernel_times", "gdy_features",
+           "gdy_variant_count",
            "gdy_variant_info", "gdy_variant_find", "gdy_isolated_variant",
            "gdy_catalogue_hash", "gdy_device_cus", "gdy_status_string", "gdy_last_error")
 
@@ -102,6 +103,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "gdy_set_timing": (i32, [P, i32]),
         "gdy_last_kernel_times": (i32, [P, ctypes.POINTER(ctypes.c_float),
                                         ctypes.POINTER(ctypes.c_float), i32]),
+        "gdy_kernel_times": (i32, [P, i32, ctypes.POINTER(ctypes.c_float),
+                                   ctypes.POINTER(ctypes.c_float), i32]),
         "gdy_features": (i32, [P, ctypes.POINTER(GemmDesc), ctypes.POINTER(ctypes.c_double)]),
         "gdy_variant_count": (i32, [P]),
         "gdy_variant_info": (i32, [P, i32, ctypes.POINTER(VariantDesc)]),
@@ -168,7 +171,8 @@ class Gemm:
         return d
 
 
-def _descs(gemms) -> ctypes.Array:
+def descs(gemms) -> ctypes.Array:
+    """Marshal Gemm objects (or GemmDesc) into a C array once."""
     arr = (GemmDesc * max(len(gemms), 1))()
     for i, g in enumerate(gemms):
         arr[i] = g if isinstance(g, GemmDesc) else g.desc()
@@ -204,7 +208,7 @@ class Context:
             raise GdyError(st, self.lib.gdy_last_error(self.h).decode())
 
     def plan(self, gemms, mode="selector", forced_cd: int = 0) -> dict:
-        arr = _descs(gemms)
+        arr = descs(gemms)
         p = Plan()
         self._check(self.lib.gdy_plan(self.h, arr, len(gemms), _mode(mode), forced_cd, ctypes.byref(p)))
         return p.as_dict()
@@ -212,7 +216,7 @@ class Context:
     def execute(self, gemms, mode="selector", forced_cd: int = 0, stream=None, want_plan=False):
         """Launch a submission on `stream` (torch stream, raw handle or None for
         torch's current stream).  Returns the plan dict when want_plan."""
-        arr = _descs(gemms)
+        arr = descs(gemms)
         handle = _stream_handle(stream)
         p = Plan()
         self._check(self.lib.gdy_execute(self.h, arr, len(gemms), _mode(mode), forced_cd,
@@ -229,10 +233,12 @@ class Context:
     def set_timing(self, on: bool):
         self._check(self.lib.gdy_set_timing(self.h, int(on)))
 
-    def kernel_times(self, n: int):
+    def kernel_times(self, n: int, back: int = 0):
+        """(start_ms, end_ms) lists for the GEMMs of a timed submission
+        (back = 0: the last one), relative to that submission's start."""
         s = (ctypes.c_float * max(n, 1))()
         e = (ctypes.c_float * max(n, 1))()
-        self._check(self.lib.gdy_last_kernel_times(self.h, s, e, n))
+        self._check(self.lib.gdy_kernel_times(self.h, back, s, e, n))
         return list(s[:n]), list(e[:n])
 
     def features(self, gemm) -> list:

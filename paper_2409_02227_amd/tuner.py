@@ -1,0 +1,333 @@
+"""Offline GO-Kernel tuning and predictor training (not on the timed path).
+
+GOLDYLOC Sec. 4.2.1 tunes each GEMM shape twice over:
+  step 1 -- benchmark the kernel list in isolation on the whole GPU and
+            under resource constraints (RC: GPU/2, GPU/4; here also GPU/8),
+            keeping the fastest kernel per RC;
+  step 2 -- for each concurrency degree (CD) 2, 4, 8, 16, co-run CD copies
+            of the GEMM with each RC's best kernel; the fastest becomes the
+            GO-Kernel for that CD (the isolated kernel may win).
+Sec. 4.3 then labels each shape with the CD giving the most speedup over
+running the same copies one after another (1 when no CD helps; the 5%
+threshold is the paper's best-CD rule in Sec. 5.5), builds the feature
+vector (M, N, K and per-CD #WGs, occupancy, #waves) and fits a multi-class
+logistic regression (Eq. 1) on min-max normalised features with a 90/10
+split.
+
+On MI355X the RCs are CU-masked stream pools of 128, 64 and 32 CUs; the
+kernel list is the library's catalogue (tiles x grid caps).  Timings follow
+Sec. 5.3: copies run back-to-back on each stream, several rounds.
+
+Usage (on the GPU):  python -m paper_2409_02227_amd.tuner --out TABLE
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+if os.path.dirname(HERE) not in sys.path:
+    sys.path.insert(0, os.path.dirname(HERE))
+
+import paper_2409_02227_amd  # noqa: F401,E402  (GPU_MAX_HW_QUEUES before HIP starts)
+
+CDS = (1, 2, 4, 8, 16)
+RCS = (0, 128, 64, 32)  # whole GPU, then CU-masked budgets
+DT_CODE = {"f16": 1, "bf16": 2, "fp8": 3}
+BEST_CD_GAIN = 1.05     # Sec. 5.5: sequential unless a CD gives >= 5%
+
+
+# ---------------------------------------------------------------------------
+# tuning shape sets
+# ---------------------------------------------------------------------------
+
+def shape_set(kind: str) -> list:
+    """(dtype, trans_a, trans_b, M, N, K) tuples to tune."""
+    shapes = []
+    if kind in ("small", "full"):
+        # the workloads' own buckets
+        shapes += [("f16", 0, 0, 256, 256, 256), ("bf16", 0, 0, 64, 4096, 1024)]
+        shapes += [("bf16", 0, 0, 512, n, k) for n, k in
+                   ((4608, 12288), (12288, 1536), (6144, 12288), (12288, 6144))]
+        shapes += [("fp8", 0, 0, m, nk, nk) for m in (1, 32, 256, 2048) for nk in (4096, 8192)]
+    if kind == "small":
+        ms = (16, 128, 1024, 4096)
+        nks = (1024, 4096, 8192)
+    else:
+        ms = (16, 32, 64, 128, 256, 512, 1024, 2048, 4096)
+        nks = (1024, 2048, 4096, 8192)
+    shapes += [("bf16", 0, 0, m, n, k) for m in ms for n in nks for k in nks]
+    seen, out = set(), []
+    for s in shapes:
+        if s not in seen:
+            seen.add(s)
+            out.append(s)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# measurement helpers
+# ---------------------------------------------------------------------------
+
+class Bench:
+    """GPU-side time of one submission.  A spin kernel on the origin stream
+    holds the GPU while the host enqueues every launch, so the events bracket
+    kernel execution only, not host launch cost (Sec. 5.3 measures kernel
+    runtimes with a profiler for the same reason)."""
+
+    def __init__(self, ctx, torch):
+        self.ctx = ctx
+        self.torch = torch
+        self.s = torch.cuda.Event(enable_timing=True)
+        self.e = torch.cuda.Event(enable_timing=True)
+        self.handle = gdy_stream_handle(torch)
+
+    def time(self, gemms, mode, cd, reps=3, warm=1) -> float:
+        """Median ms of one gdy_execute of `gemms`."""
+        from paper_2409_02227_amd import gdy
+        arr = gdy.descs(gemms)
+        n = len(gemms)
+        m = gdy.MODES[mode]
+        for _ in range(warm):
+            self.ctx.execute_descs(arr, n, m, cd, self.handle)
+        out = []
+        for _ in range(reps):
+            self.torch.cuda._sleep(2_000_000 + 100_000 * n)
+            self.s.record()
+            self.ctx.execute_descs(arr, n, m, cd, self.handle)
+            self.e.record()
+            self.e.synchronize()
+            out.append(self.s.elapsed_time(self.e))
+        return float(np.median(out))
+
+
+def gdy_stream_handle(torch):
+    import ctypes
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def operands(torch, dtype, ta, tb, m, n, k, copies, outputs_per_copy):
+    """`copies` independent operand sets with random values (timing only);
+    each copy gets `outputs_per_copy` distinct C buffers so that repeated
+    runs of one copy are separate GEMMs of the submission."""
+    tdt = {"bf16": torch.bfloat16, "f16": torch.float16, "fp8": torch.float8_e4m3fn}[dtype]
+    odt = torch.float16 if dtype == "f16" else torch.bfloat16
+    out = []
+    for _ in range(copies):
+        a = torch.randn((k, m) if ta else (m, k), device="cuda").to(tdt)
+        b = (torch.randn((n, k) if tb else (k, n), device="cuda") * 0.02).to(tdt)
+        cs = [torch.empty((m, n), device="cuda", dtype=odt) for _ in range(outputs_per_copy)]
+        out.append((a, b, cs))
+    return out
+
+
+def submission(ops, cd, rounds, vid, ta, tb):
+    """cd copies, each run `rounds` times; entry i belongs to copy i % cd so
+    FORCED mode's round-robin puts a copy's runs back-to-back on one stream."""
+    from paper_2409_02227_amd import gdy
+    out = []
+    for r in range(rounds):
+        for j in range(cd):
+            a, b, cs = ops[j]
+            out.append(gdy.Gemm(a, b, cs[r], ta, tb, 1.0, 1.0, 0, vid))
+    return out
+
+
+def candidates(variants, code, ta, tb, m):
+    """Catalogue variants for this dtype/layout, without tiles more than 4x
+    taller than M (they only burn MFMA work on padding)."""
+    mp2 = 1 << max(0, math.ceil(math.log2(max(m, 1))))
+    out = [i for i, v in enumerate(variants)
+           if v["dtype"] == code and v["trans_a"] == ta and v["trans_b"] == tb and v["bm"] <= 4 * mp2]
+    if not out:
+        out = [i for i, v in enumerate(variants)
+               if v["dtype"] == code and v["trans_a"] == ta and v["trans_b"] == tb]
+    return out
+
+
+def tune_shape(ctx, bench, torch, variants, shape, rounds=3):
+    """Steps 1 and 2 for one shape; returns a JSON-able record."""
+    dtype, ta, tb, m, n, k = shape
+    code = DT_CODE[dtype]
+    cands = candidates(variants, code, ta, tb, m)
+    uncapped = [v for v in cands if variants[v]["grid_cap_cus"] == 0]
+    by_name = {v["name"]: i for i, v in enumerate(variants)}
+    ops = operands(torch, dtype, ta, tb, m, n, k, 16, rounds)
+    rec = {"shape": list(shape), "iso": {}, "rc_best": {}, "conc": {}, "seq": {}, "pool": []}
+    # step 1: isolated timings on the whole GPU (every variant, grid caps
+    # included) and on each CU-masked pool (uncapped tiles)
+    best_tile = {}
+    for rc in RCS:
+        ctx.set_rc(rc)
+        times = {}
+        for vid in (cands if rc == 0 else uncapped):
+            # `rounds` distinct operand copies back-to-back on one stream
+            times[vid] = bench.time(submission(ops, rounds, 1, vid, ta, tb), "forced", 1) / rounds
+        ctx.set_rc(0)
+        order = sorted(times, key=times.get)
+        rec["rc_best"][str(rc)] = [variants[v]["name"] for v in order[:2]]
+        best_tile[rc] = order[0]
+        if rc == 0:
+            rec["iso"] = {variants[v]["name"]: times[v] for v in order[:8]}
+    best_iso = best_tile[0]
+    # GO candidates: the isolated best, and each RC's best tile both as is
+    # and with its grid capped to that RC's CU count
+    pool = [best_iso]
+    for rc in RCS[1:]:
+        tile = variants[best_tile[rc]]["name"].rsplit("_c", 1)[0]
+        for cap in (0, rc):
+            vid = by_name.get(f"{tile}_c{cap}")
+            if vid is not None and vid not in pool:
+                pool.append(vid)
+    rec["pool"] = [variants[v]["name"] for v in pool]
+    rec["go"] = {"1": variants[best_iso]["name"]}
+    # step 2: each CD co-runs cd copies, `rounds` runs back-to-back per stream
+    for cd in CDS[1:]:
+        n_g = cd * rounds
+        t_seq = bench.time(submission(ops, cd, rounds, best_iso, ta, tb), "forced", 1) / n_g
+        best, best_t = None, None
+        for vid in pool:
+            t = bench.time(submission(ops, cd, rounds, vid, ta, tb), "forced", cd) / n_g
+            if best_t is None or t < best_t:
+                best, best_t = vid, t
+        rec["seq"][str(cd)] = t_seq
+        rec["conc"][str(cd)] = best_t
+        rec["go"][str(cd)] = variants[best]["name"]
+    # label (Sec. 4.3 with the Sec. 5.5 threshold)
+    sp = {cd: rec["seq"][str(cd)] / rec["conc"][str(cd)] for cd in CDS[1:]}
+    best_cd = max(sp, key=lambda c: (sp[c], -c))
+    rec["speedup"] = {str(c): sp[c] for c in sp}
+    rec["label"] = best_cd if sp[best_cd] >= BEST_CD_GAIN else 1
+    del ops
+    return rec
+
+
+# ---------------------------------------------------------------------------
+# table writing and predictor training
+# ---------------------------------------------------------------------------
+
+def write_table(path, ctx, records, lr=None):
+    import socket  # noqa: F401  (hostnames are not recorded)
+    lines = ["gdy-go-table 1",
+             f"# written by paper_2409_02227_amd.tuner on {time.strftime('%Y-%m-%d %H:%M:%S')}",
+             f"device gfx950 cus {ctx.cus()}",
+             f"catalogue {ctx.catalogue_hash():016x}"]
+    if lr is not None:
+        lines.append("lr_min " + " ".join(repr(float(x)) for x in lr["xmin"]))
+        lines.append("lr_max " + " ".join(repr(float(x)) for x in lr["xmax"]))
+        lines.append("lr_w " + " ".join(repr(float(x)) for x in np.asarray(lr["w"]).ravel()))
+        lines.append("lr_b " + " ".join(repr(float(x)) for x in lr["b"]))
+    for r in records:
+        dtype, ta, tb, m, n, k = r["shape"]
+        mlog = max(0, math.ceil(math.log2(max(m, 1))))
+        names = [r["go"][str(cd)] for cd in CDS]
+        lines.append(f"entry {DT_CODE[dtype]} {ta} {tb} {mlog} {n} {k} " + " ".join(names))
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def feature_rows(ctx, records):
+    """Features of each tuned shape under the table just written (the per-CD
+    kernels are the GO-Kernels), via the library's own feature code."""
+    from paper_2409_02227_amd import gdy
+    X, y = [], []
+    for r in records:
+        dtype, ta, tb, m, n, k = r["shape"]
+        d = gdy.GemmDesc()
+        d.m, d.n, d.k = m, n, k
+        d.a_type = d.b_type = DT_CODE[dtype]
+        d.c_type = 1 if dtype == "f16" else 2
+        d.trans_a, d.trans_b = ta, tb
+        d.a, d.b, d.c = 1 << 20, 1 << 32, 1 << 40  # never dereferenced
+        d.lda = m if ta else k
+        d.ldb = k if tb else n
+        d.ldc = n
+        d.scale_a = d.scale_b = 1.0
+        X.append(ctx.features(d))
+        y.append(r["label"])
+    return np.array(X, dtype=np.float64), np.array(y)
+
+
+def train_lr(X, y, seed=0):
+    """Multinomial logistic regression (Eq. 1) on min-max features, 90/10."""
+    from sklearn.linear_model import LogisticRegression
+    xmin, xmax = X.min(axis=0), X.max(axis=0)
+    span = np.where(xmax > xmin, xmax - xmin, 1.0)
+    Xn = np.where(xmax > xmin, (X - xmin) / span, 0.0)
+    rng = np.random.default_rng(seed)
+    idx = rng.permutation(len(y))
+    n_test = max(1, len(y) // 10)
+    test, train = idx[:n_test], idx[n_test:]
+    w = np.zeros((X.shape[1], len(CDS)))
+    b = np.full(len(CDS), -1e3)  # classes never seen in training are never predicted
+    present = sorted(set(int(c) for c in y[train]))
+    if len(present) == 1:
+        b[CDS.index(present[0])] = 0.0
+        acc_train = acc_test = float(np.mean(y[test] == present[0]))
+        return {"xmin": xmin, "xmax": xmax, "w": w, "b": b, "acc_train": acc_train,
+                "acc_test": acc_test, "n_train": len(train), "n_test": len(test)}
+    clf = LogisticRegression(max_iter=5000, C=10.0)
+    clf.fit(Xn[train], y[train])
+    for j, cls in enumerate(clf.classes_):
+        ci = CDS.index(int(cls))
+        w[:, ci] = clf.coef_[j] if len(clf.classes_) > 2 else (clf.coef_[0] if j == 1 else 0.0)
+        b[ci] = clf.intercept_[j] if len(clf.classes_) > 2 else (clf.intercept_[0] if j == 1 else 0.0)
+    return {"xmin": xmin, "xmax": xmax, "w": w, "b": b,
+            "acc_train": float(clf.score(Xn[train], y[train])),
+            "acc_test": float(clf.score(Xn[test], y[test])),
+            "n_train": len(train), "n_test": len(test)}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--out", required=True, help="GO table to write")
+    ap.add_argument("--records", default=None, help="JSONL of per-shape results (appended, resumable)")
+    ap.add_argument("--shapes", default="small", choices=("small", "full"))
+    ap.add_argument("--limit", type=int, default=0)
+    args = ap.parse_args(argv)
+
+    import torch
+    from paper_2409_02227_amd import gdy
+    ctx = gdy.Context(0, max_streams=16, use_cu_masks=True)
+    variants = ctx.variants()
+    bench = Bench(ctx, torch)
+    records, done = [], set()
+    if args.records and os.path.exists(args.records):
+        for line in open(args.records):
+            r = json.loads(line)
+            records.append(r)
+            done.add(tuple(r["shape"]))
+    shapes = shape_set(args.shapes)
+    if args.limit:
+        shapes = shapes[:args.limit]
+    t0 = time.time()
+    for i, s in enumerate(shapes):
+        if tuple(s) in done:
+            continue
+        r = tune_shape(ctx, bench, torch, variants, s)
+        records.append(r)
+        if args.records:
+            with open(args.records, "a") as f:
+                f.write(json.dumps(r) + "\n")
+        print(f"[{i + 1}/{len(shapes)} {time.time() - t0:.0f}s] {s} label={r['label']} "
+              f"go={[r['go'][str(c)].replace('_w', ' w') for c in CDS[:1]]} "
+              f"sp={ {c: round(v, 2) for c, v in r['speedup'].items()} }", flush=True)
+        torch.cuda.empty_cache()
+    records = [r for r in records if tuple(r["shape"]) in set(map(tuple, shapes))]
+    write_table(args.out, ctx, records)           # GO mapping first: features depend on it
+    ctx2 = gdy.Context(0, table=args.out, max_streams=16)
+    X, y = feature_rows(ctx2, records)
+    lr = train_lr(X, y)
+    write_table(args.out, ctx, records, lr)
+    print(json.dumps({"shapes": len(records), "labels": {int(c): int((y == c).sum()) for c in CDS},
+                      "acc_train": lr["acc_train"], "acc_test": lr["acc_test"]}), flush=True)
+
+
+if __name__ == "__main__":
+    main()
