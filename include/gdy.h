@@ -117,6 +117,9 @@ typedef struct {
   int32_t vgprs;            /* registers per lane reported by the runtime              */
   int32_t occupancy;        /* workgroups resident per CU (runtime occupancy query)    */
   int32_t grid_cap_cus;     /* 0: one workgroup per tile; else grid = cap * occupancy  */
+  int32_t direct;           /* 1: global->LDS copies; needs K % bk == 0 and 16-byte
+                               aligned A/B bases and row pitches, else the staged
+                               variant of the same tile and cap runs instead     */
 } gdy_variant_desc;
 
 typedef struct gdy_ctx gdy_ctx;

@@ -44,6 +44,7 @@ struct Variant {
   int kernel;
   int cap;  // grid cap in CUs, 0 = none
   std::string name;
+  int staged = -1;  // direct kernels: the staged variant with the same tile and cap
 };
 
 struct TableEntry {
@@ -154,21 +155,39 @@ bool variant_fits(const gdy_ctx* ctx, int vid, const gdy_gemm& g) {
   return d->dtype == g.a_type && d->ta == g.trans_a && d->tb == g.trans_b;
 }
 
+// Direct kernels copy whole 16-byte chunks of whole K tiles: they need K to
+// be a multiple of the K tile and 16-byte aligned bases and row pitches.
+bool direct_ok(const gdy_ctx* ctx, int vid, const gdy_gemm& g) {
+  const KernelDesc* d = ctx->kernels[ctx->variants[vid].kernel].d;
+  if (!d->direct) return true;
+  const int es = g.a_type == GDY_FP8_E4M3 ? 1 : 2;
+  return g.k % d->bk == 0 && (uintptr_t)g.a % 16 == 0 && (uintptr_t)g.b % 16 == 0 &&
+         (g.lda * es) % 16 == 0 && (g.ldb * es) % 16 == 0;
+}
+
+// The variant that actually runs for g: a direct variant whose requirements
+// g does not meet is replaced by the staged kernel of the same tile and cap.
+int runnable(const gdy_ctx* ctx, int vid, const gdy_gemm& g) {
+  if (vid < 0) return vid;
+  if (direct_ok(ctx, vid, g)) return vid;
+  return ctx->variants[vid].staged;
+}
+
 // Isolated heuristic used when no GO table is loaded: estimate each
 // uncapped tile's time as max(tile area / 128, tile perimeter) per wave of
-// workgroups and take the cheapest.
+// workgroups (direct kernels counted 1.5x faster) and take the cheapest.
 int heuristic_variant(const gdy_ctx* ctx, const gdy_gemm& g) {
   int best = -1;
   double best_t = 0;
   for (int vid = 0; vid < (int)ctx->variants.size(); ++vid) {
     const Variant& v = ctx->variants[vid];
-    if (v.cap != 0 || !variant_fits(ctx, vid, g)) continue;
+    if (v.cap != 0 || !variant_fits(ctx, vid, g) || !direct_ok(ctx, vid, g)) continue;
     const Kernel& k = ctx->kernels[v.kernel];
     const Geometry geo = geometry(ctx, vid, g);
     const double slots = (double)ctx->cus * std::max(k.occupancy, 1);
     const double waves = std::ceil(std::max(geo.tiles, 1) / slots);
     const double per = std::max(k.d->bm * (double)k.d->bn / 128.0, (double)(k.d->bm + k.d->bn));
-    const double t = waves * per;
+    const double t = waves * per / (k.d->direct ? 1.5 : 1.0);
     if (best < 0 || t < best_t) {
       best = vid;
       best_t = t;
@@ -204,7 +223,7 @@ int table_variant(const gdy_ctx* ctx, const gdy_gemm& g, int ci) {
 int bind_variant(const gdy_ctx* ctx, const gdy_gemm& g, int ci, bool* fallback) {
   if (ctx->table.loaded) {
     const int v = table_variant(ctx, g, ci);
-    if (v >= 0) return v;
+    if (v >= 0) return runnable(ctx, v, g);
   }
   if (fallback) *fallback = true;
   return heuristic_variant(ctx, g);
@@ -423,7 +442,7 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
       else if (mode == GDY_GO)
         p->variant_of[i] = bind_variant(ctx, g[i], ci, &fb);
       else
-        p->variant_of[i] = g[i].variant;
+        p->variant_of[i] = runnable(ctx, g[i].variant, g[i]);
     }
     p->n_groups = L > 0 ? 1 : 0;
     p->group_size[0] = L;
@@ -531,6 +550,7 @@ KArgs make_args(const gdy_ctx* ctx, int vid, const gdy_gemm& g, Geometry* geo_ou
   a.tiles_n = geo.tiles_n;
   a.a_vec = g.k > 0 && vec_ok(g.a, g.lda, es, g.trans_a == 0);
   a.b_vec = g.k > 0 && vec_ok(g.b, g.ldb, es, g.trans_b == 1);
+  a.c_vec = (uintptr_t)g.c % 8 == 0 && (g.ldc * 2) % 8 == 0;
   a.group_m = 8;
   a.xcd_remap = 1;
   (void)k;
@@ -762,13 +782,16 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
     ctx->arch = ctx->arch.substr(0, ctx->arch.find(':'));
   }
 
-  const KernelDesc* tabs[3];
-  int counts[3];
+  const KernelDesc* tabs[6];
+  int counts[6];
   counts[0] = kernels_bf16(&tabs[0]);
   counts[1] = kernels_f16(&tabs[1]);
   counts[2] = kernels_fp8(&tabs[2]);
+  counts[3] = kernels_d_bf16(&tabs[3]);
+  counts[4] = kernels_d_f16(&tabs[4]);
+  counts[5] = kernels_d_fp8(&tabs[5]);
   uint64_t h = 1469598103934665603ull;
-  for (int t = 0; t < 3; ++t) {
+  for (int t = 0; t < 6; ++t) {
     for (int i = 0; i < counts[t]; ++i) {
       Kernel k;
       k.d = &tabs[t][i];
@@ -797,6 +820,20 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
     }
   }
   ctx->cat_hash = h;
+  // each direct variant falls back to the staged variant of the same tile and cap
+  for (Variant& v : ctx->variants) {
+    const KernelDesc* d = ctx->kernels[v.kernel].d;
+    if (!d->direct) continue;
+    for (size_t w = 0; w < ctx->variants.size(); ++w) {
+      const KernelDesc* e = ctx->kernels[ctx->variants[w].kernel].d;
+      if (!e->direct && e->dtype == d->dtype && e->ta == d->ta && e->tb == d->tb && e->bm == d->bm &&
+          e->bn == d->bn && ctx->variants[w].cap == v.cap) {
+        v.staged = (int)w;
+        break;
+      }
+    }
+    if (v.staged < 0) return fail(ctx, GDY_ERR_UNSUPPORTED, "no staged kernel for %s", v.name.c_str());
+  }
 
   int S = max_streams <= 0 ? 16 : max_streams;
   if (S > 64) return fail(ctx, GDY_ERR_INVALID_ARG, "max_streams %d > 64", S);
@@ -971,6 +1008,7 @@ gdy_status gdy_variant_info(gdy_ctx* ctx, int32_t id, gdy_variant_desc* out) {
   out->vgprs = k.vgprs;
   out->occupancy = k.occupancy;
   out->grid_cap_cus = v.cap;
+  out->direct = k.d->direct;
   return GDY_OK;
 }
 

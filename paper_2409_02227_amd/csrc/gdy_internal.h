@@ -26,6 +26,7 @@ struct KArgs {
   int32_t tiles_n;    // ceil(n / BN)
   int32_t a_vec;      // 1: A base and rows are aligned for vector loads
   int32_t b_vec;      // 1: same for B
+  int32_t c_vec;      // 1: C base and rows allow 8-byte stores
   int32_t group_m;    // tile-order swizzle: tile rows per group
   int32_t xcd_remap;  // 1: keep consecutive tiles on one XCD
 };
@@ -40,11 +41,15 @@ struct KernelDesc {
   int mfma;           // 32 -> 32x32 MFMA blocks, 16 -> 16x16 blocks
   int lds_bytes;      // static LDS per workgroup
   const void* func;   // __global__ entry, launched with hipExtLaunchKernel
+  int direct;         // 1: global->LDS copies; needs K % bk == 0 and 16-byte alignment
 };
 
 // Each instantiation unit exports its table.
 int kernels_bf16(const KernelDesc** out);
 int kernels_f16(const KernelDesc** out);
 int kernels_fp8(const KernelDesc** out);
+int kernels_d_bf16(const KernelDesc** out);
+int kernels_d_f16(const KernelDesc** out);
+int kernels_d_fp8(const KernelDesc** out);
 
 }  // namespace gdy

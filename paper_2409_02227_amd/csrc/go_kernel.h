@@ -470,4 +470,4 @@ go_gemm(KArgs p) {
   {DTNAME "_" LAYOUT "_" #BM "x" #BN "_w" #WM "x" #WN "_m" #MM,                                       \
    DT, TA, TB, BM, BN, ::gdy::GoCfg<DT, TA, TB, BM, BN, WM, WN, MM>::BK, WM * WN,                      \
    MM, ::gdy::GoCfg<DT, TA, TB, BM, BN, WM, WN, MM>::LDS,                                             \
-   reinterpret_cast<const void*>(&::gdy::go_gemm<DT, TA, TB, BM, BN, WM, WN, MM>)}
+   reinterpret_cast<const void*>(&::gdy::go_gemm<DT, TA, TB, BM, BN, WM, WN, MM>), 0}

@@ -1,0 +1,391 @@
+// go_kernel_d.h -- "direct" GO-Kernels: global -> LDS copies by the buffer
+// unit (no staging registers), a multi-stage LDS ring, LDS transpose reads
+// for k-major operands, 32x32 MFMA blocks.
+//
+// Same GEMM and same storage reading as go_kernel.h; this family covers
+// the large tiles, where the main loop decides throughput.  It requires
+// K to be a multiple of the K tile, 16-byte aligned operand bases and
+// leading dimensions whose byte size is a multiple of 16; the host binds the
+// register-staged kernel of the same tile otherwise.
+//
+// LDS layouts (one stage = one K tile of A and of B):
+//  * K-contiguous operand (A untransposed, B transposed): ROWS rows of 128
+//    bytes of K, no padding; the 16-byte chunk c of row r sits at position
+//    c ^ ((r >> 1) & 7), so the 16 rows of an MFMA fragment read hit 16
+//    distinct bank groups.
+//  * k-major operand (B untransposed, A transposed): BK rows (one per k) of
+//    ROWS elements, chunk c of row k at position c ^ h(k) with
+//    h(k) = 2*(k%4) + 8*((k/4)%2) (mod chunks per row); fragments are read
+//    with ds_read_b64_tr_b16 / ds_read_b64_tr_b8, which transpose within
+//    each group of 16 lanes: with 16-bit data, output lane i, element j
+//    comes from the address of lane i/4 + 4j, element i%4; with 8-bit data,
+//    from lane i/8 + 2j, byte i%8.  Pointing lane L at row kb + L/4 (kb +
+//    L/2) and columns 4*(L%4) (8*(L%2)) gives lane i consecutive k of
+//    column i -- the MFMA operand layout.
+// A direct copy writes 64 lanes x 16 bytes = 1 KiB of contiguous LDS per
+// wave instruction; each lane picks the global chunk that belongs at its
+// position.
+//
+// Pipeline: STAGES-1 K tiles are in flight while one is computed; one
+// barrier per K tile.  The MFMA computes C^T blocks (B fragment as the
+// first operand) so each lane holds 4 consecutive N outputs: 8-byte stores.
+#pragma once
+#include "go_kernel.h"
+
+namespace gdy {
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef int i32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 layout:
+// vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Buffer descriptor as four SGPRs (raw buffer, stride 0): the copies are
+// issued from inline assembly so that the compiler neither tracks them nor
+// adds its own waits (it would wait for every copy in flight before each
+// barrier and LDS read, collapsing the ring to one stage).  Completion is
+// tracked by hand with wait_vmcnt.
+typedef int sdesc __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ sdesc make_sdesc(const void* base, int bytes) {
+  const uint64_t a = (uint64_t)base;
+  sdesc d;
+  d[0] = (int)(uint32_t)a;
+  d[1] = (int)((a >> 32) & 0xffffu);  // stride 0
+  d[2] = bytes;
+  d[3] = kRsrcWord3;
+  return d;
+}
+
+// One 16-byte copy per lane: global byte `voffset` of `d` -> LDS address
+// lds_addr + 16 * lane (lds_addr is wave-uniform).
+__device__ __forceinline__ void copy16_to_lds(sdesc d, const lds_u8* lds_base, int voffset) {
+  const uint32_t lds_addr = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds_base);
+  asm volatile("buffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "{m0}"(lds_addr), "v"(voffset), "s"(d)
+               : "memory");
+}
+
+// Workgroup barrier the compiler does not decorate with memory waits; the
+// caller has already waited for its own copies.
+__device__ __forceinline__ void barrier_nowait() { asm volatile("s_barrier" ::: "memory"); }
+
+// ---- K-contiguous operand -------------------------------------------------
+template <int ES, int ROWS, int NW>
+struct DirectK {
+  static constexpr int INSTR = ROWS / (8 * NW);  // 1 KiB copies per wave per tile
+  static_assert(ROWS % (8 * NW) == 0, "tile rows must split into 8-row copies per wave");
+
+  // Issue this wave's copies of rows [row0, row0+ROWS) x K bytes
+  // [k0*ES, k0*ES+128) into the stage at `dst`.
+  static __device__ __forceinline__ void issue(sdesc src, int ld_bytes, int row0, int k0,
+                                               lds_u8* dst, int wave, int lane) {
+#pragma unroll
+    for (int j = 0; j < INSTR; ++j) {
+      const int blk = wave + NW * j;           // 8-row block
+      const int r = blk * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ ((r >> 1) & 7);
+      const int off = (row0 + r) * ld_bytes + k0 * ES + c * 16;
+      copy16_to_lds(src, dst + blk * 1024, off);
+    }
+  }
+  // byte address of logical chunk c of row r
+  static __device__ __forceinline__ int addr(int r, int c) { return r * 128 + ((c ^ ((r >> 1) & 7)) << 4); }
+};
+
+// ---- k-major operand --------------------------------------------------------
+template <int ES, int ROWS, int NW, int BK>
+struct DirectT {
+  static constexpr int RB = ROWS * ES;          // bytes per k-row
+  static constexpr int NCH = RB / 16;           // chunks per k-row
+  static constexpr int KPI = 1024 / RB;         // k-rows per 1 KiB copy
+  static constexpr int INSTR = BK / (KPI * NW);
+  static_assert(RB <= 1024 && 1024 % RB == 0, "k-row must tile a 1 KiB copy");
+  static_assert(BK % (KPI * NW) == 0, "K tile must split into copies per wave");
+  static_assert(NCH >= 4, "at least 4 chunks per k-row");
+
+  static __device__ __forceinline__ int h(int k) {
+    return (2 * (k & 3) + 8 * ((k >> 2) & 1)) & (NCH - 1);
+  }
+  static __device__ __forceinline__ void issue(sdesc src, int ld_bytes, int row0, int k0,
+                                               lds_u8* dst, int wave, int lane) {
+#pragma unroll
+    for (int j = 0; j < INSTR; ++j) {
+      const int blk = wave + NW * j;             // copy index within the tile
+      const int q = blk * 64 + lane;             // chunk index within the tile
+      const int k = q / NCH;
+      const int c = (q % NCH) ^ h(k);
+      const int off = (k0 + k) * ld_bytes + row0 * ES + c * 16;
+      copy16_to_lds(src, dst + blk * 1024, off);
+    }
+  }
+  // byte address of the 8 bytes at (k-row k, element col) (col*ES % 8 == 0)
+  static __device__ __forceinline__ int addr(int k, int col) {
+    const int byte = col * ES;
+    return k * RB + (((byte >> 4) ^ h(k)) << 4) + (byte & 15);
+  }
+};
+
+// ---- fragment loads ----------------------------------------------------------
+// A 32-row MFMA fragment: lane l covers row (l % 32) of the block and the
+// K bytes [ks*2*FB + (l/32)*FB, +FB) of the tile.
+template <int ES> struct FragT;  // fragment type by element size
+template <> struct FragT<2> { typedef u32x4 T; static constexpr int FB = 16; };
+template <> struct FragT<1> { typedef i32x8 T; static constexpr int FB = 32; };
+
+__device__ __forceinline__ u32x4 lds_read16(const lds_u8* p) {
+  return *(const __attribute__((address_space(3))) u32x4*)p;
+}
+
+// K-contiguous layout.  Rows of a 32-row block start at multiples of 32,
+// so the swizzle (r>>1)&7 depends on the lane only; the chunk of K step ks
+// is (chunk0 ^ f(ks)) with f(ks) = 2ks (16-bit) or 4ks (fp8), i.e. byte
+// offset xor 32*ks (64*ks).  kc_lane() is the per-lane offset at ks = 0.
+template <int ES>
+__device__ __forceinline__ int kc_lane(int lane, int e) {
+  const int r = lane & 31, g = lane >> 5;
+  const int sw = (r >> 1) & 7;
+  const int c = (ES == 2) ? g : 2 * g + e;  // chunk at ks = 0
+  return r * 128 + ((c ^ sw) << 4);
+}
+
+template <int ES>
+__device__ __forceinline__ typename FragT<ES>::T frag_k(const lds_u8* blk, int lane_off0,
+                                                        int lane_off1, int ks) {
+  if constexpr (ES == 2) {
+    return lds_read16(blk + (lane_off0 ^ (32 * ks)));
+  } else {
+    u32x4 lo = lds_read16(blk + (lane_off0 ^ (64 * ks)));
+    u32x4 hi = lds_read16(blk + (lane_off1 ^ (64 * ks)));
+    i32x8 r;
+    r[0] = lo[0]; r[1] = lo[1]; r[2] = lo[2]; r[3] = lo[3];
+    r[4] = hi[0]; r[5] = hi[1]; r[6] = hi[2]; r[7] = hi[3];
+    return r;
+  }
+}
+
+// k-major layout, transpose reads.  The lane's k-row within the K step,
+// (l/32)*FB/ES + sub-step + L/4 (L/2), leaves h(k) independent of ks
+// (K steps advance k by multiples of 8), so each (column block, sub-read)
+// pair has one per-lane offset, plus ks * (k per step) * row bytes.
+template <int ES, class LT>
+__device__ __forceinline__ int kt_lane(int lane, int col0, int hh) {
+  const int L = lane & 15;
+  const int cgrp = col0 + 16 * ((lane >> 4) & 1);
+  const int kb = (lane >> 5) * (FragT<ES>::FB / ES);
+  if constexpr (ES == 2) return LT::addr(kb + 4 * hh + (L >> 2), cgrp + 4 * (L & 3));
+  else return LT::addr(kb + 8 * hh + (L >> 1), cgrp + 8 * (L & 1));
+}
+
+template <int ES, class LT, int NCOL>
+__device__ __forceinline__ typename FragT<ES>::T frag_t(const lds_u8* tile, const int (&off)[NCOL],
+                                                        int ks) {
+  constexpr int KSTEP = 2 * FragT<ES>::FB / ES;  // k per MFMA step
+  const lds_u8* base = tile + ks * KSTEP * LT::RB;
+  if constexpr (ES == 2) {
+    u32x4 r;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) s16x4*)(base + off[hh]));
+      i32x2 w = __builtin_bit_cast(i32x2, v);
+      r[2 * hh] = w[0];
+      r[2 * hh + 1] = w[1];
+    }
+    return r;
+  } else {
+    i32x8 r;
+#pragma unroll
+    for (int hh = 0; hh < 4; ++hh) {
+      i32x2 v = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+          (__attribute__((address_space(3))) i32x2*)(base + off[hh]));
+      r[2 * hh] = v[0];
+      r[2 * hh + 1] = v[1];
+    }
+    return r;
+  }
+}
+
+template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int STAGES>
+struct DCfg {
+  static constexpr int ES = ElemSize<DT>::v;
+  static constexpr int BK = kRowBytes / ES;  // 64 (16-bit) or 128 (fp8) elements
+  static constexpr int NW = WM * WN;
+  static constexpr int NT = NW * 64;
+  static constexpr int WTM = BM / WM, WTN = BN / WN;
+  static constexpr int FM = WTM / 32, FN = WTN / 32;
+  static constexpr int FB = FragT<ES>::FB;
+  static constexpr int NKSTEP = kRowBytes / (2 * FB);  // K steps per tile
+  static constexpr int A_BYTES = BM * kRowBytes;
+  static constexpr int B_BYTES = BN * kRowBytes;
+  static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+  static constexpr int LDS = STAGES * STAGE_BYTES;
+  typedef Mma<DT, 32> M;
+  static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must hold whole 32x32 blocks");
+  static_assert(LDS <= 160 * 1024, "LDS budget");
+  static_assert(STAGES >= 2 && STAGES <= 4, "stages");
+};
+
+template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int STAGES>
+__global__ void __launch_bounds__(WM * WN * 64)
+go_gemm_d(KArgs p) {
+  typedef DCfg<DT, TA, TB, BM, BN, WM, WN, STAGES> C;
+  typedef typename C::M M;
+  typedef typename FragT<C::ES>::T Frag;
+  typedef typename M::Acc Acc;
+  typedef DirectK<C::ES, BM, C::NW> AK;
+  typedef DirectT<C::ES, BM, C::NW, C::BK> AT;
+  typedef DirectK<C::ES, BN, C::NW> BKc;
+  typedef DirectT<C::ES, BN, C::NW, C::BK> BT;
+  constexpr int A_INSTR = TA == 0 ? AK::INSTR : AT::INSTR;
+  constexpr int B_INSTR = TB == 1 ? BKc::INSTR : BT::INSTR;
+  constexpr int PER_TILE = A_INSTR + B_INSTR;  // copies per wave per K tile
+
+  __shared__ __attribute__((aligned(1024))) uint8_t smem_raw[C::LDS];
+  lds_u8* smem = (lds_u8*)smem_raw;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave / WN;
+  const int wn = wave % WN;
+  const int ntiles = p.tiles_m * p.tiles_n;
+  const int nk = (int)p.k / C::BK;  // host guarantees K % BK == 0
+  const sdesc ra = make_sdesc(p.a, p.a_bytes);
+  const sdesc rb = make_sdesc(p.b, p.b_bytes);
+  const Rsrc rc = make_rsrc(p.c, p.c_bytes);
+  const int lda_b = (int)p.lda * C::ES;
+  const int ldb_b = (int)p.ldb * C::ES;
+  const int ldc_b = (int)p.ldc * 2;
+  const int Mrows = (int)p.m, Ncols = (int)p.n;
+
+  // per-lane LDS offsets of the fragments (independent of tile and K step)
+  constexpr int NHH = C::ES == 2 ? 2 : 4;
+  const int ak0 = kc_lane<C::ES>(lane, 0), ak1 = kc_lane<C::ES>(lane, 1);
+  const int bk0 = ak0, bk1 = ak1;
+  int aoff[C::FM][NHH], boff[C::FN][NHH];
+  if constexpr (TA == 1) {
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+      for (int hh = 0; hh < NHH; ++hh) aoff[i][hh] = kt_lane<C::ES, AT>(lane, wm * C::WTM + i * 32, hh);
+  }
+  if constexpr (TB == 0) {
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+      for (int hh = 0; hh < NHH; ++hh) boff[j][hh] = kt_lane<C::ES, BT>(lane, wn * C::WTN + j * 32, hh);
+  }
+
+  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    int tm, tn;
+    tile_coords(t, p, tm, tn);
+    const int m0 = tm * BM;
+    const int n0 = tn * BN;
+
+    auto issue_tile = [&](int kt) {
+      lds_u8* st = smem + (kt % STAGES) * C::STAGE_BYTES;
+      if constexpr (TA == 0) AK::issue(ra, lda_b, m0, kt * C::BK, st, wave, lane);
+      else AT::issue(ra, lda_b, m0, kt * C::BK, st, wave, lane);
+      if constexpr (TB == 1) BKc::issue(rb, ldb_b, n0, kt * C::BK, st + C::A_BYTES, wave, lane);
+      else BT::issue(rb, ldb_b, n0, kt * C::BK, st + C::A_BYTES, wave, lane);
+    };
+
+    Acc acc[C::FN][C::FM];  // C^T blocks: [n block][m block]
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+      for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+        for (int r = 0; r < M::NACC; ++r) acc[j][i][r] = 0.f;
+
+    wait_vmcnt<0>();  // previous tile's stores and copies are done
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+      if (s < nk) issue_tile(s);
+
+    for (int kt = 0; kt < nk; ++kt) {
+      // tile kt has landed once at most (tiles issued after it) copies remain
+      if constexpr (STAGES == 2) {
+        wait_vmcnt<0>();
+      } else {
+        const int ahead = min(STAGES - 2, nk - 1 - kt);
+        if (ahead >= 2) wait_vmcnt<2 * PER_TILE>();
+        else if (ahead == 1) wait_vmcnt<PER_TILE>();
+        else wait_vmcnt<0>();
+      }
+      barrier_nowait();
+      if (kt + STAGES - 1 < nk) issue_tile(kt + STAGES - 1);
+
+      const lds_u8* As = smem + (kt % STAGES) * C::STAGE_BYTES;
+      const lds_u8* Bs = As + C::A_BYTES;
+#pragma unroll
+      for (int ks = 0; ks < C::NKSTEP; ++ks) {
+        Frag af[C::FM], bf[C::FN];
+#pragma unroll
+        for (int i = 0; i < C::FM; ++i) {
+          if constexpr (TA == 0) af[i] = frag_k<C::ES>(As + (wm * C::WTM + i * 32) * kRowBytes, ak0, ak1, ks);
+          else af[i] = frag_t<C::ES, AT>(As, aoff[i], ks);
+        }
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j) {
+          if constexpr (TB == 1) bf[j] = frag_k<C::ES>(Bs + (wn * C::WTN + j * 32) * kRowBytes, bk0, bk1, ks);
+          else bf[j] = frag_t<C::ES, BT>(Bs, boff[j], ks);
+        }
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+          for (int i = 0; i < C::FM; ++i) acc[j][i] = M::run(bf[j], af[i], acc[j][i]);
+      }
+    }
+    __syncthreads();  // every wave is done with the ring before the next tile refills it
+
+    // epilogue: block (j, i) holds C^T; accumulator r of lane l is
+    // n = 8*(r/4) + 4*(l/32) + r%4, m = l%32 -- 4 consecutive n per group of 4
+    const float s = p.scale;
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) {
+#pragma unroll
+      for (int i = 0; i < C::FM; ++i) {
+        const int row = m0 + wm * C::WTM + i * 32 + (lane & 31);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int col = n0 + wn * C::WTN + j * 32 + 8 * g + 4 * (lane >> 5);
+          const uint16_t h0 = to_out<DT>(acc[j][i][4 * g + 0] * s);
+          const uint16_t h1 = to_out<DT>(acc[j][i][4 * g + 1] * s);
+          const uint16_t h2 = to_out<DT>(acc[j][i][4 * g + 2] * s);
+          const uint16_t h3 = to_out<DT>(acc[j][i][4 * g + 3] * s);
+          if (row < Mrows) {
+            const int off = row * ldc_b + col * 2;
+            if (col + 4 <= Ncols && p.c_vec) {
+              u32x2 v;
+              v[0] = (unsigned)h0 | ((unsigned)h1 << 16);
+              v[1] = (unsigned)h2 | ((unsigned)h3 << 16);
+              __builtin_amdgcn_raw_buffer_store_b64(v, rc, off, 0, 0);
+            } else {
+              if (col + 0 < Ncols) __builtin_amdgcn_raw_buffer_store_b16(h0, rc, off + 0, 0, 0);
+              if (col + 1 < Ncols) __builtin_amdgcn_raw_buffer_store_b16(h1, rc, off + 2, 0, 0);
+              if (col + 2 < Ncols) __builtin_amdgcn_raw_buffer_store_b16(h2, rc, off + 4, 0, 0);
+              if (col + 3 < Ncols) __builtin_amdgcn_raw_buffer_store_b16(h3, rc, off + 6, 0, 0);
+            }
+          }
+        }
+      }
+    }
+  }
+}
+
+}  // namespace gdy
+
+#define GDY_KERNEL_D(DT, DTNAME, TA, TB, LAYOUT, BM, BN, WM, WN, ST)                              \
+  {DTNAME "_" LAYOUT "_" #BM "x" #BN "_w" #WM "x" #WN "_d" #ST,                                    \
+   DT, TA, TB, BM, BN, ::gdy::DCfg<DT, TA, TB, BM, BN, WM, WN, ST>::BK, WM * WN,                   \
+   32, ::gdy::DCfg<DT, TA, TB, BM, BN, WM, WN, ST>::LDS,                                            \
+   reinterpret_cast<const void*>(&::gdy::go_gemm_d<DT, TA, TB, BM, BN, WM, WN, ST>), 1}

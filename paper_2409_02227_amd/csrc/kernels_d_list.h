@@ -1,0 +1,21 @@
+// kernels_d_list.h -- catalogue of direct (global->LDS copy) GO-Kernels for
+// one input type; expanded by the kernels_d_*.hip units.  Large tiles only:
+// the staged family in kernels_list.h holds the same tiles for GEMMs the
+// direct kernels cannot take (K not a multiple of the K tile, unaligned).
+#define GDY_TILES_D(L, TA, TB)                                        \
+  GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 256, 256, 2, 4, 2),     \
+  GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 256, 128, 2, 2, 3),     \
+  GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 128, 256, 2, 2, 3),     \
+  GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 128, 128, 2, 2, 2),     \
+  GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 128, 128, 2, 2, 4)
+
+#define GDY_TILES_D_SMALL(L, TA, TB)                                  \
+  GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 256, 128, 2, 2, 3),     \
+  GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 128, 128, 2, 2, 2)
+
+static const ::gdy::KernelDesc kTableD[] = {
+    GDY_TILES_D("nn", 0, 0),
+    GDY_TILES_D("nt", 0, 1),
+    GDY_TILES_D_SMALL("tn", 1, 0),
+    GDY_TILES_D_SMALL("tt", 1, 1),
+};

@@ -68,7 +68,8 @@ class VariantDesc(ctypes.Structure):
                 ("trans_b", ctypes.c_int32), ("bm", ctypes.c_int32), ("bn", ctypes.c_int32),
                 ("bk", ctypes.c_int32), ("waves", ctypes.c_int32), ("mfma", ctypes.c_int32),
                 ("lds_bytes", ctypes.c_int32), ("vgprs", ctypes.c_int32),
-                ("occupancy", ctypes.c_int32), ("grid_cap_cus", ctypes.c_int32)]
+                ("occupancy", ctypes.c_int32), ("grid_cap_cus", ctypes.c_int32),
+                ("direct", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
         d = {f: getattr(self, f) for f, _ in self._fields_}

@@ -36,7 +36,7 @@ def test_struct_layouts_match_header():
     assert ctypes.sizeof(gdy.GemmDesc) == 3 * 8 + 5 * 4 + 4 + 6 * 8 + 2 * 4 + 2 * 4
     assert gdy.GemmDesc.a.offset == 48
     assert ctypes.sizeof(gdy.Plan) == 4 * 4 + 6 * 4 * gdy.MAX_GEMMS
-    assert ctypes.sizeof(gdy.VariantDesc) == 64 + 12 * 4
+    assert ctypes.sizeof(gdy.VariantDesc) == 64 + 13 * 4
     text = open(HEADER).read()
     assert "#define GDY_MAX_GEMMS 256" in text and "#define GDY_N_FEATURES 18" in text
 

@@ -220,3 +220,41 @@ def test_concurrent_kernels_overlap(ctx):
         assert best > 0.0, f"kernels never overlapped: {iv}"
     finally:
         ctx.set_timing(False)
+
+
+def _pad_to(n, mult):
+    return (-n) % mult
+
+
+def test_direct_kernels_ragged_mn(ctx):
+    """Each direct kernel (global->LDS copies, transpose reads) on ragged M
+    and N, K a whole number of K tiles, leading dimensions padded to 16-byte
+    multiples so the direct path is taken (checked in the plan)."""
+    for vid, v in _kernels(ctx):
+        if not v["direct"]:
+            continue
+        dt = DT_NAME[v["dtype"]]
+        es = 1 if dt == "fp8" else 2
+        m, n, k = 2 * v["bm"] - 5, v["bn"] + 3, 2 * v["bk"]
+        ta, tb = v["trans_a"], v["trans_b"]
+        a_cols = m if ta else k
+        b_cols = k if tb else n
+        spec = GemmSpec(m, n, k, dt, ta, tb, seed=4000 + vid, name=v["name"],
+                        pad_a=_pad_to(a_cols, 16 // es), pad_b=_pad_to(b_cols, 16 // es), pad_c=5)
+        mat = inputs.materialize(spec)
+        plan = _run(ctx, [mat], "forced", 1, [vid])
+        assert plan["variant_of"][0] == vid, f"{v['name']}: direct path not taken"
+        check(mat, label=v["name"])
+
+
+def test_direct_falls_back_when_ineligible(ctx):
+    """K not a multiple of the K tile: the plan binds the staged kernel of the
+    same tile, which gives a correct result."""
+    vid = ctx.find("bf16_nn_128x128_w2x2_d2_c0")
+    assert vid >= 0
+    spec = GemmSpec(200, 300, 100, "bf16", seed=9, name="fallback")
+    mat = inputs.materialize(spec)
+    plan = _run(ctx, [mat], "forced", 1, [vid])
+    ran = ctx.variant(plan["variant_of"][0])
+    assert not ran["direct"] and (ran["bm"], ran["bn"]) == (128, 128)
+    check(mat)
