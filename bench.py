@@ -18,7 +18,7 @@ import os
 import sys
 import time
 
-os.environ.setdefault("GPU_MAX_HW_QUEUES", "16")  # before anything initialises HIP
+os.environ.setdefault("GPU_MAX_HW_QUEUES", "24")  # before anything initialises HIP
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -35,7 +35,46 @@ WORKLOADS = {
     "lstm_gates": (2, "4 bf16 GEMMs (64,4096,1024): LSTM-step gate projections at batch 64"),
     "square_fp16": (1, "2 fp16 GEMMs (256,256,256)"),
     "two_tenant_fp8": (5, "2 tenants x 16 fp8 e4m3 GEMMs, M in {1,32,256,2048}, N=K in {4096,8192}"),
+    "het_submissions": (4, "seeded submissions of 2-16 bf16 GEMMs, M log-uniform in [16,4096], "
+                           "N,K in {1024,2048,4096,8192}, operands windows of device pools"),
 }
+TRAFFIC = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2409_02227_amd", "csrc", f)
+                  for f in ("go_kernel.h", "go_kernel_d.h")]
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(workload, kernel, gemm):
+    """HBM bytes per launch of the dominant kernel from the committed
+    FETCH_SIZE/WRITE_SIZE counter runs, scaled by the copy calibration;
+    None when no record matches or the kernels changed since."""
+    if not os.path.exists(TRAFFIC):
+        return None
+    for r in json.load(open(TRAFFIC)).get("records", []):
+        if (r.get("workload") == workload and r.get("kernel") == kernel and r.get("gemm") == gemm
+                and r.get("kernel_source_hash") == kernel_source_hash()):
+            return r["bytes_per_launch"]
+    return None
+
+
+def copy_calibration():
+    import torch
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(10):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_each_way": n, "copies": 10}))
 
 
 def parse():
@@ -49,6 +88,10 @@ def parse():
     ap.add_argument("--table", default=DEFAULT_TABLE)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target length of the CPU oracle sample (0 = skip)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy 10 times (HBM counter calibration)")
+    ap.add_argument("--submissions", type=int, default=24,
+                    help="heterogeneous workload: number of seeded submissions timed")
     return ap.parse_args()
 
 
@@ -92,6 +135,21 @@ def dominant_kernel(ctx, mats, plan, steps):
             "bytes": spec.compulsory_bytes(), "dtype": spec.dtype}
 
 
+def tenant_latency(ctx, mats, steps, tenants):
+    """Per-tenant completion latency: each GEMM's end time from its
+    submission's start (per-kernel events of the timed steps); p50 and max
+    over that tenant's GEMMs and the steps."""
+    n = len(mats)
+    lat = {t: [] for t in tenants}
+    for back in range(min(steps, 64)):
+        _, en = ctx.kernel_times(n, back)
+        for i, m in enumerate(mats):
+            if en[i] >= 0:
+                lat[m.spec.tenant].append(en[i])
+    return {str(t): {"p50": round(float(np.median(v)), 4), "max": round(float(np.max(v)), 4)}
+            for t, v in lat.items() if v}
+
+
 def cpu_baseline(mats, target_s):
     """The oracle on full rows of every GEMM: calibrate rows per GEMM with a
     one-row pass, then time a sample of about target_s seconds."""
@@ -123,16 +181,68 @@ def cpu_baseline(mats, target_s):
                       f"({fl / 1e9:.1f} GFLOP fp64 incl. the error-bound sum, {t:.1f} s)"}
 
 
+def het_bench(args, desc):
+    """Heterogeneous submissions: the first `--submissions` seeded sets of
+    2-16 bf16 GEMMs, operands as windows of device-resident pools.  Reports
+    aggregate TFLOP/s under the selector and the geomean per-submission
+    speedup over sequential execution."""
+    import torch
+    from paper_2409_02227_amd import gdy, inputs
+    subs = inputs.config4(count=args.submissions)
+    a_elems, b_elems = 600 << 20, 1200 << 20          # 1.2 GB and 2.4 GB of bf16
+    placed = inputs.pool_specs(subs, a_elems, b_elems, seed=4)
+    gen = torch.Generator(device="cuda").manual_seed(44)
+    a_pool = (torch.rand(a_elems, device="cuda", generator=gen) * 2 - 1).to(torch.bfloat16)
+    b_pool = (torch.randn(b_elems, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+    table = args.table if args.table and os.path.exists(args.table) else None
+    ctx = gdy.Context(0, table=table, max_streams=16)
+    handle = gdy._stream_handle(None)
+    arrs, flops = [], []
+    for sub in placed:
+        gemms = []
+        for g, oa, ob in sub:
+            a = a_pool[oa:oa + g.m * g.k].view(g.m, g.k)
+            b = b_pool[ob:ob + g.k * g.n].view(g.k, g.n)
+            c = torch.empty(g.m, g.n, dtype=torch.bfloat16, device="cuda")
+            gemms.append(gdy.Gemm(a, b, c))
+        arrs.append((gdy.descs(gemms), len(gemms), gemms))
+        flops.append(sum(g.flops for g, _, _ in sub))
+    steps = max(1, args.steps // 4)
+    t_sel, t_seq = [], []
+    for arr, n, _ in arrs:
+        t_seq.append(time_steps(ctx, arr, n, "sequential", steps, 2, handle, torch))
+        t_sel.append(time_steps(ctx, arr, n, args.mode, steps, 2, handle, torch))
+    sp = [a / b for a, b in zip(t_seq, t_sel)]
+    value = sum(flops) / sum(t_sel) / 1e12
+    out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+           "steps": steps, "warmup": 2, "ms_per_step": round(1e3 * sum(t_sel) / len(t_sel), 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (seeded device pools; shapes from seeded submissions)",
+           "config": {"workload": f"het_submissions: {desc}", "mode": args.mode,
+                      "submissions": len(arrs), "gemms": sum(n for _, n, _ in arrs),
+                      "table": os.path.relpath(table, ROOT) if table else None},
+           "speedup_vs_sequential_geomean": round(float(np.exp(np.mean(np.log(sp)))), 4),
+           "speedup_vs_sequential_min_max": [round(min(sp), 3), round(max(sp), 3)],
+           "sequential_tflops": round(sum(flops) / sum(t_seq) / 1e12, 2),
+           "pct_mfma_peak": round(100 * value / PEAK_TFLOPS["bf16"], 2)}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (the method concurrently runs independent GEMMs "
               f"on a single device); got --gpus {args.gpus}", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     import torch
     from paper_2409_02227_amd import gdy, inputs
 
     cfg_id, desc = WORKLOADS[args.workload]
+    if cfg_id == 4:
+        return het_bench(args, desc)
     specs = inputs.CONFIGS[cfg_id]()
     mats = [inputs.materialize(s, "cuda:0", keep_host=True) for s in specs]
     table = args.table if args.table and os.path.exists(args.table) else None
@@ -155,7 +265,8 @@ def main():
     peak = PEAK_TFLOPS[dtype]
     ach = dom["flops"] / (dom["mean_ms"] * 1e-3) / 1e12
     roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(ach / peak, 4), "traffic": None,
+            "frac": round(ach / peak, 4),
+            "traffic": recorded_traffic(args.workload, dom["variant"], dom["shape"]),
             "kernel": dom["variant"], "gemm": dom["shape"], "launches": dom["launches"],
             "mean_ms": round(dom["mean_ms"], 4)}
     ai = dom["flops"] / dom["bytes"]
@@ -177,6 +288,9 @@ def main():
         "pct_mfma_peak": round(100 * value / peak, 2),
         "roofline": roof,
     }
+    tenants = sorted({m.spec.tenant for m in mats})
+    if len(tenants) > 1:
+        out["tenant_latency_ms"] = tenant_latency(ctx, mats, args.steps, tenants)
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(mats, args.cpu_seconds)
     print(json.dumps(out), flush=True)

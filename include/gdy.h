@@ -41,8 +41,9 @@
  * A context is not thread-safe: use one per host thread, or lock.
  *
  * Environment: HIP maps streams onto GPU_MAX_HW_QUEUES hardware queues per
- * process (4 by default); set it to at least the largest CD (16) before the
- * process first touches HIP, or concurrent GEMMs share queues and serialise.
+ * process (4 by default); set it to cover the stream pool plus the caller's
+ * streams (24 for the default 16-stream pool) before the process first
+ * touches HIP, or concurrent GEMMs share queues and serialise.
  */
 #ifndef GDY_H
 #define GDY_H
@@ -130,10 +131,13 @@ typedef struct gdy_ctx gdy_ctx;
  * streams at default priority and their events.  `table_path` names a GO
  * table written by the offline tuner (NULL or "" = none: SELECTOR and GO
  * modes then fall back to isolated heuristics and report fallback = 1).
- * A table built for another device or catalogue returns GDY_ERR_TABLE.
- * `use_cu_masks` != 0 also creates CU-masked pools for the resource
- * constraints GPU/2, GPU/4 and GPU/8 (used by the tuner).  On error *out is
- * NULL.
+ * A table built for another device, or naming a variant the library does
+ * not have, returns GDY_ERR_TABLE.
+ * `use_cu_masks` != 0 also creates one CU-masked stream for each resource
+ * constraint GPU/2, GPU/4 and GPU/8 (isolated runs of the tuner).  Every
+ * stream needs its own hardware queue (a CU mask is a queue property), so
+ * GPU_MAX_HW_QUEUES must cover the pool, the masked streams and the
+ * caller's streams (24 for a 16-stream pool).  On error *out is NULL.
  *
  * device < 0 creates a host-only context that plans without a GPU: its CU
  * count is GDY_HOST_CUS (default 256) or the loaded table's, kernel

@@ -1,0 +1,226 @@
+"""Selector oracle: features, CD prediction, clamp, grouping and GO-Kernel
+binding, written out in plain Python from GOLDYLOC (arXiv 2409.02227).
+
+TEST INFRASTRUCTURE ONLY.  The product library does not import this
+module; the tests compare libgdy's plans with what it computes.  It shares
+no code with libgdy: it reads the GO table text itself and takes each
+kernel variant's static description (tile, waves, occupancy, grid cap) as
+input, as the paper's predictor takes each kernel's resource use.
+
+Definitions followed:
+  * Sec. 4.3, features: GEMM dimensions M, N, K and, for each concurrency
+    degree (CD) class, the #WGs, occupancy and #waves of the kernel used for
+    that CD.  #WGs follows from the output size and the tile; occupancy is
+    the workgroups a CU holds at once; #waves = #WGs / (CUs x occupancy).
+  * Sec. 4.3, Eq. 1: P = exp(X W) / sum_i exp(X W_i) over the CD classes
+    1, 2, 4, 8, 16, on min-max normalised features; the predicted CD is the
+    most probable class; the executed CD is min(predicted, available GEMMs).
+  * Sec. 4.4: a single GEMM keeps its isolated kernel.
+  * Sec. 6.7: GEMMs of a heterogeneous set run together only if all of them
+    prefer that CD; otherwise they are split into smaller sets.  Reading
+    used: sort by the (clamped) preferred CD, largest first, and grow each
+    group while its size stays within every member's preferred CD.
+  * GO library (Sec. 4.2.2): each GEMM shape maps to one kernel per CD;
+    shapes that were not tuned take the nearest tuned shape (log2 distance
+    in M, N, K), and a group of s GEMMs takes the kernel of the CD class
+    nearest to s in log2 (ties toward the larger class).
+The library's documented substitution of a direct kernel by the staged
+kernel of the same tile (when K is not a whole number of K tiles or an
+operand is not 16-byte aligned) is reproduced so that the kernels compared
+are the ones that run.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+CD_CLASSES = (1, 2, 4, 8, 16)
+N_FEATURES = 3 + 3 * len(CD_CLASSES)
+
+
+# ---------------------------------------------------------------------------
+# GO table (text) -- independent reader
+# ---------------------------------------------------------------------------
+
+def parse_table(path: str) -> dict:
+    t = {"entries": [], "lr": None}
+    lr = {}
+    with open(path) as f:
+        for raw in f:
+            line = raw.strip()
+            if not line or line.startswith("#"):
+                continue
+            tok = line.split()
+            if tok[0] == "device":
+                t["arch"], t["cus"] = tok[1], int(tok[3])
+            elif tok[0] == "catalogue":
+                t["catalogue"] = int(tok[1], 16)
+            elif tok[0] in ("lr_min", "lr_max", "lr_b"):
+                lr[tok[0]] = np.array([float(x) for x in tok[1:]])
+            elif tok[0] == "lr_w":
+                lr["lr_w"] = np.array([float(x) for x in tok[1:]]).reshape(N_FEATURES, len(CD_CLASSES))
+            elif tok[0] == "entry":
+                t["entries"].append({"dtype": int(tok[1]), "ta": int(tok[2]), "tb": int(tok[3]),
+                                     "mlog": int(tok[4]), "n": int(tok[5]), "k": int(tok[6]),
+                                     "variants": tok[7:12]})
+    if len(lr) == 4:
+        t["lr"] = {"xmin": lr["lr_min"], "xmax": lr["lr_max"], "w": lr["lr_w"], "b": lr["lr_b"]}
+    return t
+
+
+# ---------------------------------------------------------------------------
+# features (Sec. 4.3)
+# ---------------------------------------------------------------------------
+
+def n_workgroups(m: int, n: int, bm: int, bn: int, cap_cus: int, occupancy: int) -> int:
+    """Workgroups launched: one per output tile, or capped at cap x occupancy."""
+    tiles = math.ceil(m / bm) * math.ceil(n / bn)
+    return tiles if cap_cus == 0 else min(tiles, cap_cus * max(occupancy, 1))
+
+
+def n_waves(wgs: int, cus: int, occupancy: int) -> float:
+    """Fractional waves of workgroups over the whole GPU."""
+    return wgs / (cus * occupancy) if occupancy > 0 else 0.0
+
+
+def elem_bytes(dtype: int) -> int:
+    return 1 if dtype == 3 else 2
+
+
+def direct_ok(v: dict, g: dict) -> bool:
+    if not v["direct"]:
+        return True
+    es = elem_bytes(g["a_type"])
+    return (g["k"] % v["bk"] == 0 and g["a"] % 16 == 0 and g["b"] % 16 == 0
+            and (g["lda"] * es) % 16 == 0 and (g["ldb"] * es) % 16 == 0)
+
+
+def runnable(vid: int, g: dict, variants: list) -> int:
+    """The variant that runs: a direct one the GEMM cannot take is replaced
+    by the staged variant of the same dtype, layout, tile and cap."""
+    v = variants[vid]
+    if direct_ok(v, g):
+        return vid
+    for w, u in enumerate(variants):
+        if (not u["direct"] and u["dtype"] == v["dtype"] and u["trans_a"] == v["trans_a"]
+                and u["trans_b"] == v["trans_b"] and u["bm"] == v["bm"] and u["bn"] == v["bn"]
+                and u["grid_cap_cus"] == v["grid_cap_cus"]):
+            return w
+    raise LookupError(f"no staged kernel for {v['name']}")
+
+
+def nearest_entry(entries: list, g: dict):
+    """Tuned shape nearest to g in log2 space (same dtype and layout)."""
+    mlog = math.ceil(math.log2(max(g["m"], 1)))
+    best, best_d = None, None
+    for e in entries:
+        if (e["dtype"], e["ta"], e["tb"]) != (g["a_type"], g["trans_a"], g["trans_b"]):
+            continue
+        d = (abs(e["mlog"] - mlog) + abs(math.log2(e["n"]) - math.log2(max(g["n"], 1)))
+             + abs(math.log2(e["k"]) - math.log2(max(g["k"], 1))))
+        if best is None or d < best_d:
+            best, best_d = e, d
+    return best
+
+
+def bind(g: dict, class_index: int, table: dict, variants: list, by_name: dict) -> int:
+    e = nearest_entry(table["entries"], g)
+    if e is None:
+        raise LookupError("no tuned shape for this dtype/layout")
+    return runnable(by_name[e["variants"][class_index]], g, variants)
+
+
+def features(g: dict, table: dict, variants: list, by_name: dict, cus: int) -> np.ndarray:
+    x = [float(g["m"]), float(g["n"]), float(g["k"])]
+    for ci in range(len(CD_CLASSES)):
+        v = variants[bind(g, ci, table, variants, by_name)]
+        occ = v["occupancy"]
+        wgs = n_workgroups(g["m"], g["n"], v["bm"], v["bn"], v["grid_cap_cus"], occ)
+        x += [float(wgs), float(occ), n_waves(wgs, cus, occ)]
+    return np.array(x)
+
+
+# ---------------------------------------------------------------------------
+# prediction (Eq. 1) and clamp
+# ---------------------------------------------------------------------------
+
+def normalise(x: np.ndarray, lr: dict) -> np.ndarray:
+    span = lr["xmax"] - lr["xmin"]
+    out = np.zeros_like(x, dtype=np.float64)
+    ok = span > 0
+    out[ok] = (x[ok] - lr["xmin"][ok]) / span[ok]
+    return out
+
+
+def probabilities(xn: np.ndarray, lr: dict) -> np.ndarray:
+    """Eq. 1: P = exp(X W) / sum_i exp(X W_i), with the class biases."""
+    z = xn @ lr["w"] + lr["b"]
+    e = np.exp(z - z.max())
+    return e / e.sum()
+
+
+def predict_cd(x: np.ndarray, lr: dict) -> int:
+    p = probabilities(normalise(x, lr), lr)
+    return CD_CLASSES[int(np.argmax(p))]  # first maximum: ties go to the smaller CD
+
+
+def clamp(cd: int, available: int) -> int:
+    """Sec. 4.3: the executed CD is the minimum of predicted and available."""
+    return min(cd, available)
+
+
+def class_for_size(s: int) -> int:
+    """CD class whose GO-Kernel serves a group of s GEMMs: nearest in log2,
+    ties toward the larger class."""
+    if s <= 1:
+        return 0
+    d = [abs(math.log2(s) - math.log2(c)) for c in CD_CLASSES]
+    best = 0
+    for i in range(1, len(CD_CLASSES)):
+        if d[i] <= d[best]:
+            best = i
+    return best
+
+
+def group(order: list, pref: dict, slots: int) -> list:
+    """Greedy heterogeneous grouping over GEMMs already sorted by preferred CD
+    (descending): a group grows while its size stays within every member's
+    preferred CD and the stream pool."""
+    groups, cur, cap = [], [], 0
+    for i in order:
+        c = min(pref[i], slots)
+        if cur and len(cur) + 1 <= min(cap, c):
+            cur.append(i)
+            cap = min(cap, c)
+        else:
+            if cur:
+                groups.append(cur)
+            cur, cap = [i], c
+    if cur:
+        groups.append(cur)
+    return groups
+
+
+def plan_selector(gemms: list, table: dict, variants: list, cus: int, slots: int) -> dict:
+    """What a GOLDYLOC submission runs: per-GEMM clamped CD, groups (run one
+    after another) and the kernel bound to each GEMM."""
+    by_name = {v["name"]: i for i, v in enumerate(variants)}
+    live = [i for i, g in enumerate(gemms) if g["m"] > 0 and g["n"] > 0]
+    n = len(live)
+    out = {"pred_cd": {}, "groups": [], "variant_of": {}}
+    if n <= 1:  # Sec. 4.4: a lone GEMM keeps its isolated kernel
+        for i in live:
+            out["variant_of"][i] = bind(gemms[i], 0, table, variants, by_name)
+        out["groups"] = [live] if live else []
+        return out
+    for i in live:
+        x = features(gemms[i], table, variants, by_name, cus)
+        out["pred_cd"][i] = clamp(predict_cd(x, table["lr"]), n)
+    order = sorted(live, key=lambda i: -out["pred_cd"][i])  # stable: submission order on ties
+    out["groups"] = group(order, out["pred_cd"], slots)
+    for grp in out["groups"]:
+        ci = class_for_size(len(grp))
+        for i in grp:
+            out["variant_of"][i] = bind(gemms[i], ci, table, variants, by_name)
+    return out

@@ -11,6 +11,6 @@ import os
 # HIP maps streams onto at most GPU_MAX_HW_QUEUES hardware queues per
 # process (4 by default), which would serialise concurrency degrees above 4.
 # Only effective if set before the process first initialises HIP.
-os.environ.setdefault("GPU_MAX_HW_QUEUES", "16")
+os.environ.setdefault("GPU_MAX_HW_QUEUES", "24")
 
 __all__ = ["gdy", "inputs", "build"]

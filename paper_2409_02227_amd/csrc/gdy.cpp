@@ -669,12 +669,11 @@ gdy_status load_table(gdy_ctx* ctx, const char* path) {
         return fail(ctx, GDY_ERR_TABLE, "GO table is for %s/%d CUs, device is %s/%d", arch.c_str(),
                     cus, ctx->arch.c_str(), ctx->cus);
     } else if (tag == "catalogue") {
+      // informational: the catalogue the table was tuned against.  Entries
+      // name their variants, so a table stays usable while the catalogue
+      // grows; a name the library does not know is rejected below.
       std::string hex;
       in >> hex;
-      const uint64_t h = std::strtoull(hex.c_str(), nullptr, 16);
-      if (h != ctx->cat_hash)
-        return fail(ctx, GDY_ERR_TABLE, "GO table catalogue %s does not match library %016llx",
-                    hex.c_str(), (unsigned long long)ctx->cat_hash);
     } else if (tag == "lr_min" || tag == "lr_max" || tag == "lr_b") {
       double* dst = tag == "lr_min" ? t.xmin : tag == "lr_max" ? t.xmax : t.b;
       const int cnt = tag == "lr_b" ? GDY_N_CD : GDY_N_FEATURES;
@@ -851,12 +850,16 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
     ctx->done.push_back(e);
   }
   if (use_cu_masks) {
+    // One stream per resource constraint: only isolated runs use them.  A CU
+    // mask belongs to a hardware queue, and HIP shares queues between streams
+    // once GPU_MAX_HW_QUEUES is reached, so every extra masked stream risks
+    // confining an ordinary pool stream to the masked CUs.
     const int words = (ctx->cus + 31) / 32;
     for (int budget : kRcBudgets) {
       std::vector<uint32_t> mask(words, 0u);
       for (int cu = 0; cu < std::min(budget, ctx->cus); ++cu) mask[cu / 32] |= 1u << (cu % 32);
       std::vector<hipStream_t> pl;
-      for (int s = 0; s < S; ++s) {
+      for (int s = 0; s < 1; ++s) {
         hipStream_t st;
         HIP_TRY(ctx, hipExtStreamCreateWithCUMask(&st, (uint32_t)words, mask.data()));
         pl.push_back(st);

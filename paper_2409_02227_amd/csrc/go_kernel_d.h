@@ -9,10 +9,11 @@
 // register-staged kernel of the same tile otherwise.
 //
 // LDS layouts (one stage = one K tile of A and of B):
-//  * K-contiguous operand (A untransposed, B transposed): ROWS rows of 128
-//    bytes of K, no padding; the 16-byte chunk c of row r sits at position
-//    c ^ ((r >> 1) & 7), so the 16 rows of an MFMA fragment read hit 16
-//    distinct bank groups.
+//  * K-contiguous operand (A untransposed, B transposed): ROWS rows of KB
+//    bytes of K (KB = 128, or 64 for the deeper-ring variants), no padding;
+//    the 16-byte chunk c of row r sits at position c ^ ((r / RPB) % CPR)
+//    with CPR = KB/16 chunks per row and RPB = 256/KB rows per 256 bytes, so
+//    the 16 rows of an MFMA fragment read hit 16 distinct bank groups.
 //  * k-major operand (B untransposed, A transposed): BK rows (one per k) of
 //    ROWS elements, chunk c of row k at position c ^ h(k) with
 //    h(k) = 2*(k%4) + 8*((k/4)%2) (mod chunks per row); fragments are read
@@ -78,26 +79,30 @@ __device__ __forceinline__ void copy16_to_lds(sdesc d, const lds_u8* lds_base, i
 __device__ __forceinline__ void barrier_nowait() { asm volatile("s_barrier" ::: "memory"); }
 
 // ---- K-contiguous operand -------------------------------------------------
-template <int ES, int ROWS, int NW>
+template <int ES, int ROWS, int NW, int KB>
 struct DirectK {
-  static constexpr int INSTR = ROWS / (8 * NW);  // 1 KiB copies per wave per tile
-  static_assert(ROWS % (8 * NW) == 0, "tile rows must split into 8-row copies per wave");
+  static constexpr int CPR = KB / 16;            // 16-byte chunks per row
+  static constexpr int RPC = 64 / CPR;           // rows per 1 KiB copy
+  static constexpr int RPB = 256 / KB;           // rows per 256 bytes (64 banks)
+  static constexpr int INSTR = ROWS / (RPC * NW);  // copies per wave per tile
+  static_assert(ROWS % (RPC * NW) == 0, "tile rows must split into whole copies per wave");
 
+  static __device__ __forceinline__ int sw(int r) { return (r / RPB) & (CPR - 1); }
   // Issue this wave's copies of rows [row0, row0+ROWS) x K bytes
-  // [k0*ES, k0*ES+128) into the stage at `dst`.
+  // [k0*ES, k0*ES+KB) into the stage at `dst`.
   static __device__ __forceinline__ void issue(sdesc src, int ld_bytes, int row0, int k0,
-                                               lds_u8* dst, int wave, int lane) {
+                                               lds_u8* dst, int wave, int lane, int part,
+                                               int nparts) {
 #pragma unroll
     for (int j = 0; j < INSTR; ++j) {
-      const int blk = wave + NW * j;           // 8-row block
-      const int r = blk * 8 + (lane >> 3);
-      const int c = (lane & 7) ^ ((r >> 1) & 7);
+      if (j % nparts != part) continue;
+      const int blk = wave + NW * j;           // RPC-row block
+      const int r = blk * RPC + lane / CPR;
+      const int c = (lane % CPR) ^ sw(r);
       const int off = (row0 + r) * ld_bytes + k0 * ES + c * 16;
       copy16_to_lds(src, dst + blk * 1024, off);
     }
   }
-  // byte address of logical chunk c of row r
-  static __device__ __forceinline__ int addr(int r, int c) { return r * 128 + ((c ^ ((r >> 1) & 7)) << 4); }
 };
 
 // ---- k-major operand --------------------------------------------------------
@@ -115,9 +120,11 @@ struct DirectT {
     return (2 * (k & 3) + 8 * ((k >> 2) & 1)) & (NCH - 1);
   }
   static __device__ __forceinline__ void issue(sdesc src, int ld_bytes, int row0, int k0,
-                                               lds_u8* dst, int wave, int lane) {
+                                               lds_u8* dst, int wave, int lane, int part,
+                                               int nparts) {
 #pragma unroll
     for (int j = 0; j < INSTR; ++j) {
+      if (j % nparts != part) continue;
       const int blk = wave + NW * j;             // copy index within the tile
       const int q = blk * 64 + lane;             // chunk index within the tile
       const int k = q / NCH;
@@ -145,15 +152,14 @@ __device__ __forceinline__ u32x4 lds_read16(const lds_u8* p) {
 }
 
 // K-contiguous layout.  Rows of a 32-row block start at multiples of 32,
-// so the swizzle (r>>1)&7 depends on the lane only; the chunk of K step ks
+// so the swizzle depends on the lane only; the chunk of K step ks
 // is (chunk0 ^ f(ks)) with f(ks) = 2ks (16-bit) or 4ks (fp8), i.e. byte
 // offset xor 32*ks (64*ks).  kc_lane() is the per-lane offset at ks = 0.
-template <int ES>
+template <int ES, int KB>
 __device__ __forceinline__ int kc_lane(int lane, int e) {
   const int r = lane & 31, g = lane >> 5;
-  const int sw = (r >> 1) & 7;
   const int c = (ES == 2) ? g : 2 * g + e;  // chunk at ks = 0
-  return r * 128 + ((c ^ sw) << 4);
+  return r * KB + ((c ^ DirectK<ES, 64, 1, KB>::sw(r)) << 4);
 }
 
 template <int ES>
@@ -213,18 +219,18 @@ __device__ __forceinline__ typename FragT<ES>::T frag_t(const lds_u8* tile, cons
   }
 }
 
-template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int STAGES>
+template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int STAGES, int KB>
 struct DCfg {
   static constexpr int ES = ElemSize<DT>::v;
-  static constexpr int BK = kRowBytes / ES;  // 64 (16-bit) or 128 (fp8) elements
+  static constexpr int BK = KB / ES;  // K elements per stage
   static constexpr int NW = WM * WN;
   static constexpr int NT = NW * 64;
   static constexpr int WTM = BM / WM, WTN = BN / WN;
   static constexpr int FM = WTM / 32, FN = WTN / 32;
   static constexpr int FB = FragT<ES>::FB;
-  static constexpr int NKSTEP = kRowBytes / (2 * FB);  // K steps per tile
-  static constexpr int A_BYTES = BM * kRowBytes;
-  static constexpr int B_BYTES = BN * kRowBytes;
+  static constexpr int NKSTEP = KB / (2 * FB);  // K steps per tile
+  static constexpr int A_BYTES = BM * KB;
+  static constexpr int B_BYTES = BN * KB;
   static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
   static constexpr int LDS = STAGES * STAGE_BYTES;
   typedef Mma<DT, 32> M;
@@ -233,16 +239,16 @@ struct DCfg {
   static_assert(STAGES >= 2 && STAGES <= 4, "stages");
 };
 
-template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int STAGES>
+template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int STAGES, int KB>
 __global__ void __launch_bounds__(WM * WN * 64)
 go_gemm_d(KArgs p) {
-  typedef DCfg<DT, TA, TB, BM, BN, WM, WN, STAGES> C;
+  typedef DCfg<DT, TA, TB, BM, BN, WM, WN, STAGES, KB> C;
   typedef typename C::M M;
   typedef typename FragT<C::ES>::T Frag;
   typedef typename M::Acc Acc;
-  typedef DirectK<C::ES, BM, C::NW> AK;
+  typedef DirectK<C::ES, BM, C::NW, KB> AK;
   typedef DirectT<C::ES, BM, C::NW, C::BK> AT;
-  typedef DirectK<C::ES, BN, C::NW> BKc;
+  typedef DirectK<C::ES, BN, C::NW, KB> BKc;
   typedef DirectT<C::ES, BN, C::NW, C::BK> BT;
   constexpr int A_INSTR = TA == 0 ? AK::INSTR : AT::INSTR;
   constexpr int B_INSTR = TB == 1 ? BKc::INSTR : BT::INSTR;
@@ -268,7 +274,7 @@ go_gemm_d(KArgs p) {
 
   // per-lane LDS offsets of the fragments (independent of tile and K step)
   constexpr int NHH = C::ES == 2 ? 2 : 4;
-  const int ak0 = kc_lane<C::ES>(lane, 0), ak1 = kc_lane<C::ES>(lane, 1);
+  const int ak0 = kc_lane<C::ES, KB>(lane, 0), ak1 = kc_lane<C::ES, KB>(lane, 1);
   const int bk0 = ak0, bk1 = ak1;
   int aoff[C::FM][NHH], boff[C::FN][NHH];
   if constexpr (TA == 1) {
@@ -290,12 +296,16 @@ go_gemm_d(KArgs p) {
     const int m0 = tm * BM;
     const int n0 = tn * BN;
 
-    auto issue_tile = [&](int kt) {
+    // copies of tile kt, part `part` of `nparts` (each wave's copies are
+    // spread over the K steps of the tile being computed)
+    auto issue_tile = [&](int kt, int part, int nparts) {
       lds_u8* st = smem + (kt % STAGES) * C::STAGE_BYTES;
-      if constexpr (TA == 0) AK::issue(ra, lda_b, m0, kt * C::BK, st, wave, lane);
-      else AT::issue(ra, lda_b, m0, kt * C::BK, st, wave, lane);
-      if constexpr (TB == 1) BKc::issue(rb, ldb_b, n0, kt * C::BK, st + C::A_BYTES, wave, lane);
-      else BT::issue(rb, ldb_b, n0, kt * C::BK, st + C::A_BYTES, wave, lane);
+      if constexpr (TA == 0) AK::issue(ra, lda_b, m0, kt * C::BK, st, wave, lane, part, nparts);
+      else AT::issue(ra, lda_b, m0, kt * C::BK, st, wave, lane, part, nparts);
+      if constexpr (TB == 1)
+        BKc::issue(rb, ldb_b, n0, kt * C::BK, st + C::A_BYTES, wave, lane, part, nparts);
+      else
+        BT::issue(rb, ldb_b, n0, kt * C::BK, st + C::A_BYTES, wave, lane, part, nparts);
     };
 
     Acc acc[C::FN][C::FM];  // C^T blocks: [n block][m block]
@@ -309,7 +319,7 @@ go_gemm_d(KArgs p) {
     wait_vmcnt<0>();  // previous tile's stores and copies are done
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s)
-      if (s < nk) issue_tile(s);
+      if (s < nk) issue_tile(s, 0, 1);
 
     for (int kt = 0; kt < nk; ++kt) {
       // tile kt has landed once at most (tiles issued after it) copies remain
@@ -322,27 +332,47 @@ go_gemm_d(KArgs p) {
         else wait_vmcnt<0>();
       }
       barrier_nowait();
-      if (kt + STAGES - 1 < nk) issue_tile(kt + STAGES - 1);
+      const bool prefetch = kt + STAGES - 1 < nk;
 
       const lds_u8* As = smem + (kt % STAGES) * C::STAGE_BYTES;
       const lds_u8* Bs = As + C::A_BYTES;
-#pragma unroll
-      for (int ks = 0; ks < C::NKSTEP; ++ks) {
-        Frag af[C::FM], bf[C::FN];
+      // fragments of K step ks+1 are read while the MFMAs of step ks run;
+      // the scheduling fences keep the compiler from hoisting further reads
+      // (which would need registers for every step of the tile at once)
+      Frag af[2][C::FM], bf[2][C::FN];
+      auto load_step = [&](int ks, int buf) {
 #pragma unroll
         for (int i = 0; i < C::FM; ++i) {
-          if constexpr (TA == 0) af[i] = frag_k<C::ES>(As + (wm * C::WTM + i * 32) * kRowBytes, ak0, ak1, ks);
-          else af[i] = frag_t<C::ES, AT>(As, aoff[i], ks);
+          if constexpr (TA == 0)
+            af[buf][i] = frag_k<C::ES>(As + (wm * C::WTM + i * 32) * KB, ak0, ak1, ks);
+          else
+            af[buf][i] = frag_t<C::ES, AT>(As, aoff[i], ks);
         }
 #pragma unroll
         for (int j = 0; j < C::FN; ++j) {
-          if constexpr (TB == 1) bf[j] = frag_k<C::ES>(Bs + (wn * C::WTN + j * 32) * kRowBytes, bk0, bk1, ks);
-          else bf[j] = frag_t<C::ES, BT>(Bs, boff[j], ks);
+          if constexpr (TB == 1)
+            bf[buf][j] = frag_k<C::ES>(Bs + (wn * C::WTN + j * 32) * KB, bk0, bk1, ks);
+          else
+            bf[buf][j] = frag_t<C::ES, BT>(Bs, boff[j], ks);
+        }
+      };
+      load_step(0, 0);
+#pragma unroll
+      for (int ks = 0; ks < C::NKSTEP; ++ks) {
+        if (ks + 1 < C::NKSTEP) load_step(ks + 1, (ks + 1) & 1);
+        // with two stages the copies must land by the next iteration: issue
+        // them all at once; deeper rings spread them over the K steps
+        if constexpr (STAGES == 2) {
+          if (prefetch && ks == 0) issue_tile(kt + 1, 0, 1);
+        } else {
+          if (prefetch) issue_tile(kt + STAGES - 1, ks, C::NKSTEP);
         }
 #pragma unroll
         for (int j = 0; j < C::FN; ++j)
 #pragma unroll
-          for (int i = 0; i < C::FM; ++i) acc[j][i] = M::run(bf[j], af[i], acc[j][i]);
+          for (int i = 0; i < C::FM; ++i)
+            acc[j][i] = M::run(bf[ks & 1][j], af[ks & 1][i], acc[j][i]);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     __syncthreads();  // every wave is done with the ring before the next tile refills it
@@ -354,6 +384,11 @@ go_gemm_d(KArgs p) {
     for (int j = 0; j < C::FN; ++j) {
 #pragma unroll
       for (int i = 0; i < C::FM; ++i) {
+        if constexpr (C::FM * C::FN * M::NACC > 128) {
+          // large accumulators live in AGPRs; keep each block there until
+          // its turn (otherwise every block is copied to VGPRs at once)
+          asm volatile("" : "+a"(acc[j][i]));
+        }
         const int row = m0 + wm * C::WTM + i * 32 + (lane & 31);
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
@@ -377,6 +412,8 @@ go_gemm_d(KArgs p) {
             }
           }
         }
+        // one block at a time: keeps the accumulators in AGPRs until stored
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
   }
@@ -384,8 +421,14 @@ go_gemm_d(KArgs p) {
 
 }  // namespace gdy
 
-#define GDY_KERNEL_D(DT, DTNAME, TA, TB, LAYOUT, BM, BN, WM, WN, ST)                              \
-  {DTNAME "_" LAYOUT "_" #BM "x" #BN "_w" #WM "x" #WN "_d" #ST,                                    \
-   DT, TA, TB, BM, BN, ::gdy::DCfg<DT, TA, TB, BM, BN, WM, WN, ST>::BK, WM * WN,                   \
-   32, ::gdy::DCfg<DT, TA, TB, BM, BN, WM, WN, ST>::LDS,                                            \
-   reinterpret_cast<const void*>(&::gdy::go_gemm_d<DT, TA, TB, BM, BN, WM, WN, ST>), 1}
+// Catalogue entries: _dS = S stages of 128-byte K rows; _dSh = S stages of
+// 64-byte K rows (half the K per stage, twice the stages in the same LDS).
+#define GDY_KERNEL_DK(DT, DTNAME, TA, TB, LAYOUT, BM, BN, WM, WN, ST, KB, SUFFIX)                 \
+  {DTNAME "_" LAYOUT "_" #BM "x" #BN "_w" #WM "x" #WN "_d" #ST SUFFIX,                             \
+   DT, TA, TB, BM, BN, ::gdy::DCfg<DT, TA, TB, BM, BN, WM, WN, ST, KB>::BK, WM * WN,               \
+   32, ::gdy::DCfg<DT, TA, TB, BM, BN, WM, WN, ST, KB>::LDS,                                        \
+   reinterpret_cast<const void*>(&::gdy::go_gemm_d<DT, TA, TB, BM, BN, WM, WN, ST, KB>), 1}
+#define GDY_KERNEL_D(DT, DTNAME, TA, TB, LAYOUT, BM, BN, WM, WN, ST) \
+  GDY_KERNEL_DK(DT, DTNAME, TA, TB, LAYOUT, BM, BN, WM, WN, ST, 128, "")
+#define GDY_KERNEL_DH(DT, DTNAME, TA, TB, LAYOUT, BM, BN, WM, WN, ST) \
+  GDY_KERNEL_DK(DT, DTNAME, TA, TB, LAYOUT, BM, BN, WM, WN, ST, 64, "h")

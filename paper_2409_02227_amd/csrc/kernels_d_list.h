@@ -4,6 +4,9 @@
 // direct kernels cannot take (K not a multiple of the K tile, unaligned).
 #define GDY_TILES_D(L, TA, TB)                                        \
   GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 256, 256, 2, 4, 2),     \
+  GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 256, 256, 2, 2, 2),     \
+  GDY_KERNEL_DH(GDY_DT, GDY_DTNAME, TA, TB, L, 256, 256, 2, 4, 4),    \
+  GDY_KERNEL_DH(GDY_DT, GDY_DTNAME, TA, TB, L, 256, 256, 2, 2, 4),    \
   GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 256, 128, 2, 2, 3),     \
   GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 128, 256, 2, 2, 3),     \
   GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 128, 128, 2, 2, 2),     \

@@ -201,9 +201,8 @@ def tune_shape(ctx, bench, torch, variants, shape, rounds=3):
         rec["go"][str(cd)] = variants[best]["name"]
     # label (Sec. 4.3 with the Sec. 5.5 threshold)
     sp = {cd: rec["seq"][str(cd)] / rec["conc"][str(cd)] for cd in CDS[1:]}
-    best_cd = max(sp, key=lambda c: (sp[c], -c))
     rec["speedup"] = {str(c): sp[c] for c in sp}
-    rec["label"] = best_cd if sp[best_cd] >= BEST_CD_GAIN else 1
+    rec["label"] = label_of(sp)
     del ops
     return rec
 
@@ -271,7 +270,8 @@ def train_lr(X, y, seed=0):
         b[CDS.index(present[0])] = 0.0
         acc_train = acc_test = float(np.mean(y[test] == present[0]))
         return {"xmin": xmin, "xmax": xmax, "w": w, "b": b, "acc_train": acc_train,
-                "acc_test": acc_test, "n_train": len(train), "n_test": len(test)}
+                "acc_test": acc_test, "n_train": len(train), "n_test": len(test),
+                "test": test, "train": train}
     clf = LogisticRegression(max_iter=5000, C=10.0)
     clf.fit(Xn[train], y[train])
     for j, cls in enumerate(clf.classes_):
@@ -281,7 +281,41 @@ def train_lr(X, y, seed=0):
     return {"xmin": xmin, "xmax": xmax, "w": w, "b": b,
             "acc_train": float(clf.score(Xn[train], y[train])),
             "acc_test": float(clf.score(Xn[test], y[test])),
-            "n_train": len(train), "n_test": len(test)}
+            "n_train": len(train), "n_test": len(test), "test": test, "train": train}
+
+
+def label_of(speedup: dict) -> int:
+    """Sec. 4.3 label with the Sec. 5.5 threshold: the CD with the most
+    speedup over sequential, or 1 when no CD gains 5%."""
+    best = max(speedup, key=lambda c: (speedup[c], -c))
+    return best if speedup[best] >= BEST_CD_GAIN else 1
+
+
+def predict_rows(X, lr):
+    span = np.where(lr["xmax"] > lr["xmin"], lr["xmax"] - lr["xmin"], 1.0)
+    Xn = np.where(lr["xmax"] > lr["xmin"], (X - lr["xmin"]) / span, 0.0)
+    return np.array(CDS)[np.argmax(Xn @ lr["w"] + lr["b"], axis=1)]
+
+
+def evaluate(records, X, lr, idx):
+    """Sec. 6.6 style: with a GEMMs available (2, 4, 8, 16), the executed CD is
+    min(predicted, a); it is correct when it equals the best-CD choice among
+    CDs <= a (sequential unless a CD gains 5%); also the geomean of the
+    speedup obtained over the best-CD speedup."""
+    pred = predict_rows(X[idx], lr)
+    out = {}
+    for a in CDS[1:]:
+        ok, ratio = 0, []
+        for p, i in zip(pred, idx):
+            sp = {1: 1.0}
+            sp.update({int(c): v for c, v in records[i]["speedup"].items()})
+            sub = {c: v for c, v in sp.items() if c <= a}
+            best = label_of(sub)
+            got = min(int(p), a)
+            ok += got == best
+            ratio.append(sp[got] / sp[best])
+        out[a] = {"accuracy": ok / len(idx), "geomean_vs_best": float(np.exp(np.mean(np.log(ratio))))}
+    return out
 
 
 def main(argv=None):
@@ -325,8 +359,13 @@ def main(argv=None):
     X, y = feature_rows(ctx2, records)
     lr = train_lr(X, y)
     write_table(args.out, ctx, records, lr)
-    print(json.dumps({"shapes": len(records), "labels": {int(c): int((y == c).sum()) for c in CDS},
-                      "acc_train": lr["acc_train"], "acc_test": lr["acc_test"]}), flush=True)
+    summary = {"shapes": len(records), "labels": {int(c): int((y == c).sum()) for c in CDS},
+               "acc_train": lr["acc_train"], "acc_test": lr["acc_test"],
+               "by_available_test": evaluate(records, X, lr, lr["test"]),
+               "by_available_all": evaluate(records, X, lr, np.arange(len(records)))}
+    print(json.dumps(summary), flush=True)
+    with open(os.path.splitext(args.out)[0] + "_summary.json", "w") as f:
+        json.dump(summary, f, indent=1)
 
 
 if __name__ == "__main__":

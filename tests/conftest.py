@@ -2,9 +2,9 @@
 import os
 import sys
 
-# concurrency degrees up to 16 need as many HIP hardware queues; must be set
+# a 16-stream pool plus torch's streams need their own HIP hardware queues; set
 # before anything in the test process initialises HIP
-os.environ.setdefault("GPU_MAX_HW_QUEUES", "16")
+os.environ.setdefault("GPU_MAX_HW_QUEUES", "24")
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 if ROOT not in sys.path:

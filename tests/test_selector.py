@@ -1,0 +1,227 @@
+"""Selector: oracle pins (Sec. 4.3 Eq. 1, the clamp, Sec. 6.7 grouping,
+feature definitions) and bit-exact parity of libgdy's planner with the
+oracle, on the CPU through a host-only context (gdy_create with device -1).
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import selector as sel
+from paper_2409_02227_amd import gdy
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+TABLE = os.path.join(ROOT, "paper_2409_02227_amd", "tables", "gfx950.table")
+
+
+# --------------------------------------------------------------------------
+# pins of the oracle itself
+# --------------------------------------------------------------------------
+
+def test_eq1_prediction_matches_sklearn():
+    """Eq. 1 with a fitted multinomial model: argmax of the softmax equals
+    scikit-learn's predict, and the probabilities equal predict_proba."""
+    from sklearn.linear_model import LogisticRegression
+    rng = np.random.default_rng(0)
+    X = rng.random((400, sel.N_FEATURES))
+    w_true = rng.normal(size=(sel.N_FEATURES, 5))
+    y = np.array(sel.CD_CLASSES)[np.argmax(X @ w_true + rng.normal(0, 0.3, (400, 5)), axis=1)]
+    clf = LogisticRegression(max_iter=5000).fit(X, y)
+    lr = {"xmin": np.zeros(sel.N_FEATURES), "xmax": np.ones(sel.N_FEATURES),
+          "w": np.zeros((sel.N_FEATURES, 5)), "b": np.zeros(5)}
+    for j, c in enumerate(clf.classes_):
+        lr["w"][:, sel.CD_CLASSES.index(int(c))] = clf.coef_[j]
+        lr["b"][sel.CD_CLASSES.index(int(c))] = clf.intercept_[j]
+    Xt = rng.random((300, sel.N_FEATURES))
+    ours = [sel.predict_cd(x, lr) for x in Xt]
+    assert ours == list(clf.predict(Xt))
+    np.testing.assert_allclose([sel.probabilities(x, lr) for x in Xt], clf.predict_proba(Xt),
+                               rtol=1e-10, atol=1e-12)
+
+
+def test_min_max_normalisation():
+    lr = {"xmin": np.array([1.0, 5.0]), "xmax": np.array([3.0, 5.0])}
+    np.testing.assert_array_equal(sel.normalise(np.array([2.0, 7.0]), lr), [0.5, 0.0])
+
+
+def test_clamp_and_class_for_size():
+    # Sec. 4.3: executed CD = min(predicted, available)
+    assert sel.clamp(16, 3) == 3 and sel.clamp(2, 9) == 2 and sel.clamp(1, 1) == 1
+    want = {1: 1, 2: 2, 3: 4, 4: 4, 5: 4, 6: 8, 7: 8, 8: 8, 11: 8, 12: 16, 16: 16, 40: 16}
+    for s, cd in want.items():
+        assert sel.CD_CLASSES[sel.class_for_size(s)] == cd, s
+
+
+def test_grouping_follows_the_heterogeneous_policy():
+    """Sec. 6.7: 16 GEMMs of two kinds run all together only if both prefer
+    16; otherwise as two homogeneous sets of 8."""
+    both16 = {i: 16 for i in range(16)}
+    assert [len(g) for g in sel.group(list(range(16)), both16, 16)] == [16]
+    mixed = {i: (16 if i < 8 else 8) for i in range(16)}
+    order = sorted(range(16), key=lambda i: -mixed[i])
+    assert sel.group(order, mixed, 16) == [list(range(8)), list(range(8, 16))]
+    # random sets: every GEMM once, no group larger than any member's CD
+    rng = np.random.default_rng(1)
+    for _ in range(200):
+        n = int(rng.integers(1, 17))
+        pref = {i: int(rng.choice(sel.CD_CLASSES)) for i in range(n)}
+        order = sorted(range(n), key=lambda i: -pref[i])
+        groups = sel.group(order, pref, 16)
+        assert sorted(i for g in groups for i in g) == list(range(n))
+        assert all(len(g) <= min(pref[i] for i in g) for g in groups)
+
+
+def test_workgroups_and_waves_hand_values():
+    # the tensor-sliced layer share: 256x256 tiles, occupancy 1, 256 CUs
+    shapes = [(512, 4608), (512, 12288), (512, 6144), (512, 12288)]
+    wgs = [sel.n_workgroups(m, n, 256, 256, 0, 1) for m, n in shapes]
+    assert wgs == [36, 96, 48, 96]
+    assert 2 * sum(wgs) == 552
+    assert math.isclose(sel.n_waves(552, 256, 1), 2.15625)
+    # LSTM gates (64, 4096, 1024) with 64x256 tiles: 16 per GEMM, 64 for four
+    assert sel.n_workgroups(64, 4096, 64, 256, 0, 2) == 16
+    assert math.isclose(sel.n_waves(64, 256, 1), 0.25)
+    # a grid cap of 64 CUs at occupancy 2 launches 128 workgroups
+    assert sel.n_workgroups(4096, 4096, 128, 128, 64, 2) == 128
+
+
+def test_nearest_entry_by_log2_distance():
+    entries = [{"dtype": 2, "ta": 0, "tb": 0, "mlog": 6, "n": 4096, "k": 1024, "variants": []},
+               {"dtype": 2, "ta": 0, "tb": 0, "mlog": 9, "n": 4608, "k": 12288, "variants": []},
+               {"dtype": 3, "ta": 0, "tb": 0, "mlog": 9, "n": 4608, "k": 12288, "variants": []}]
+    g = {"m": 500, "n": 5000, "k": 10000, "a_type": 2, "trans_a": 0, "trans_b": 0}
+    assert sel.nearest_entry(entries, g) is entries[1]
+    g = dict(g, m=60, n=4000, k=1000)
+    assert sel.nearest_entry(entries, g) is entries[0]
+
+
+# --------------------------------------------------------------------------
+# libgdy planner == oracle (host-only context, no GPU)
+# --------------------------------------------------------------------------
+
+def _desc(m, n, k, dtype, ta, tb, base, pad=0):
+    d = gdy.GemmDesc()
+    d.m, d.n, d.k = m, n, k
+    d.a_type = d.b_type = dtype
+    d.c_type = 1 if dtype == 1 else 2
+    d.trans_a, d.trans_b = ta, tb
+    d.lda = (m if ta else k) + pad
+    d.ldb = (k if tb else n) + pad
+    d.ldc = n
+    d.a, d.b, d.c = base, base + (1 << 32), base + (2 << 32)
+    d.scale_a = d.scale_b = 1.0
+    d.variant = -1
+    return d
+
+
+def _as_dict(d):
+    return {"m": d.m, "n": d.n, "k": d.k, "a_type": d.a_type, "trans_a": d.trans_a,
+            "trans_b": d.trans_b, "a": d.a, "b": d.b, "lda": d.lda, "ldb": d.ldb}
+
+
+def _synthetic_table(path, ctx, rng):
+    """A GO table with random LR weights and random kernels per tuned shape."""
+    V = ctx.variants()
+    lines = ["gdy-go-table 1", "device host cus 256", f"catalogue {ctx.catalogue_hash():016x}"]
+    xmin = np.zeros(sel.N_FEATURES)
+    xmax = np.array([4096, 8192, 8192] + [4096, 4, 4] * 5, dtype=float)
+    lines.append("lr_min " + " ".join(map(repr, xmin.tolist())))
+    lines.append("lr_max " + " ".join(map(repr, xmax.tolist())))
+    lines.append("lr_w " + " ".join(map(repr, rng.normal(0, 2, sel.N_FEATURES * 5).tolist())))
+    lines.append("lr_b " + " ".join(map(repr, rng.normal(0, 1, 5).tolist())))
+    for dtype in (1, 2, 3):
+        for ta, tb in ((0, 0), (0, 1), (1, 1)):
+            pool = [v["name"] for v in V if (v["dtype"], v["trans_a"], v["trans_b"]) == (dtype, ta, tb)]
+            for mlog in (4, 7, 10, 12):
+                for n in (1024, 8192):
+                    for k in (1024, 8192):
+                        names = [pool[int(rng.integers(len(pool)))] for _ in range(5)]
+                        lines.append(f"entry {dtype} {ta} {tb} {mlog} {n} {k} " + " ".join(names))
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def _check_plan(ctx, table, descs, slots=16):
+    V = ctx.variants()
+    p = ctx.plan(descs, mode="selector")
+    want = sel.plan_selector([_as_dict(d) for d in descs], table, V, ctx.cus(), slots)
+    live = [i for i, d in enumerate(descs) if d.m > 0 and d.n > 0]
+    assert [len(g) for g in want["groups"]] == p["group_size"]
+    for gi, grp in enumerate(want["groups"]):
+        for i in grp:
+            assert p["group_of"][i] == gi
+    assert p["order"] == [i for g in want["groups"] for i in g]
+    for i in live:
+        assert p["variant_of"][i] == want["variant_of"][i], (i, V[p["variant_of"][i]]["name"])
+        if len(live) > 1:
+            assert p["pred_cd"][i] == want["pred_cd"][i]
+    assert p["cd"] == max(len(g) for g in want["groups"])
+
+
+def _random_set(rng, n):
+    out = []
+    for i in range(n):
+        dtype = int(rng.choice([1, 2, 3]))
+        ta, tb = [(0, 0), (0, 1), (1, 1)][int(rng.integers(3))]
+        m = int(rng.integers(1, 5000))
+        nn = int(rng.choice([512, 1000, 2048, 4096, 8192]))
+        k = int(rng.choice([64, 100, 1024, 3000, 8192]))
+        out.append(_desc(m, nn, k, dtype, ta, tb, (i + 1) << 36, pad=int(rng.choice([0, 0, 3]))))
+    return out
+
+
+def test_planner_matches_oracle_on_synthetic_tables(tmp_path):
+    rng = np.random.default_rng(7)
+    probe = gdy.Context(-1)
+    for t in range(3):
+        path = str(tmp_path / f"t{t}.table")
+        _synthetic_table(path, probe, rng)
+        ctx = gdy.Context(-1, table=path)
+        table = sel.parse_table(path)
+        for _ in range(40):
+            descs = _random_set(rng, int(rng.integers(1, 17)))
+            _check_plan(ctx, table, descs)
+            # features, bit for bit
+            d = descs[0]
+            np.testing.assert_array_equal(
+                ctx.features(d),
+                sel.features(_as_dict(d), table, ctx.variants(),
+                             {v["name"]: i for i, v in enumerate(ctx.variants())}, ctx.cus()))
+
+
+@pytest.mark.skipif(not os.path.exists(TABLE), reason="no tuned table")
+def test_planner_matches_oracle_on_the_tuned_table():
+    """The committed MI355X table, on the workloads' own GEMM sets."""
+    from paper_2409_02227_amd import inputs
+    ctx = gdy.Context(-1, table=TABLE)
+    table = sel.parse_table(TABLE)
+    if table["lr"] is None:
+        pytest.skip("table has no predictor")
+    sets = [inputs.config1(), inputs.config2(), inputs.config3(), inputs.config5()]
+    sets += inputs.config4(count=30)
+    for specs in sets:
+        descs = []
+        for i, s in enumerate(specs):
+            d = _desc(s.m, s.n, s.k, {"f16": 1, "bf16": 2, "fp8": 3}[s.dtype], s.trans_a,
+                      s.trans_b, (i + 1) << 36)
+            descs.append(d)
+        _check_plan(ctx, table, descs)
+
+
+def test_lone_gemm_keeps_isolated_kernel(tmp_path):
+    rng = np.random.default_rng(3)
+    probe = gdy.Context(-1)
+    path = str(tmp_path / "t.table")
+    _synthetic_table(path, probe, rng)
+    ctx = gdy.Context(-1, table=path)
+    d = _desc(700, 4096, 1024, 2, 0, 0, 1 << 36)
+    p = ctx.plan([d], mode="selector")
+    assert p["cd"] == 1 and p["variant_of"][0] == ctx.isolated_variant(d)
+
+
+def test_no_table_falls_back_to_sequential():
+    ctx = gdy.Context(-1)
+    descs = [_desc(512, 4096, 1024, 2, 0, 0, (i + 1) << 36) for i in range(4)]
+    p = ctx.plan(descs, mode="selector")
+    assert p["fallback"] == 1 and p["cd"] == 1 and p["n_groups"] == 4

@@ -1,0 +1,76 @@
+"""CPU checks of the offline tuner's logic: labels (Sec. 4.3 + the 5% rule of
+Sec. 5.5), multinomial training (Eq. 1), the written GO table as read back by
+the library (host-only context) and by the oracle's reader."""
+import numpy as np
+import pytest
+
+from oracle import selector as sel
+from paper_2409_02227_amd import gdy, tuner
+
+
+def test_label_rule():
+    assert tuner.label_of({2: 1.30, 4: 1.50, 8: 1.40, 16: 1.10}) == 4
+    assert tuner.label_of({2: 1.04, 4: 1.01, 8: 0.90, 16: 0.80}) == 1     # no CD gains 5%
+    assert tuner.label_of({2: 1.20, 4: 1.20, 8: 1.0, 16: 1.0}) == 2       # ties: smaller CD
+    assert tuner.label_of({2: 1.05, 4: 1.0, 8: 1.0, 16: 1.0}) == 2
+
+
+def _records(rng, n):
+    recs = []
+    for i in range(n):
+        m = int(2 ** rng.integers(4, 13))
+        nn, k = (int(2 ** rng.integers(10, 14)) for _ in range(2))
+        sp = {str(c): float(np.exp(rng.normal(0.1 * np.log2(c) * (m < 512), 0.1))) for c in (2, 4, 8, 16)}
+        recs.append({"shape": ["bf16", 0, 0, m, nn, k], "speedup": sp,
+                     "label": tuner.label_of({int(c): v for c, v in sp.items()})})
+    return recs
+
+
+def test_training_and_evaluation_shapes():
+    rng = np.random.default_rng(0)
+    recs = _records(rng, 200)
+    X = np.column_stack([[r["shape"][3] for r in recs], [r["shape"][4] for r in recs],
+                         [r["shape"][5] for r in recs]] + [rng.random(200) for _ in range(15)])
+    y = np.array([r["label"] for r in recs])
+    lr = tuner.train_lr(X, y, seed=1)
+    assert lr["w"].shape == (18, 5) and lr["n_test"] == 20 and lr["n_train"] == 180
+    assert set(lr["test"]).isdisjoint(lr["train"])
+    ev = tuner.evaluate(recs, X, lr, lr["test"])
+    for a in (2, 4, 8, 16):
+        assert 0.0 <= ev[a]["accuracy"] <= 1.0 and 0.0 < ev[a]["geomean_vs_best"] <= 1.0 + 1e-12
+    # the tuner's own prediction equals the oracle's Eq. 1 argmax
+    for x in X[:50]:
+        assert tuner.predict_rows(x[None, :], lr)[0] == sel.predict_cd(x, lr)
+
+
+def test_written_table_reads_back(tmp_path):
+    ctx = gdy.Context(-1)
+    V = ctx.variants()
+    names = [v["name"] for v in V if (v["dtype"], v["trans_a"], v["trans_b"]) == (2, 0, 0)][:5]
+    recs = [{"shape": ["bf16", 0, 0, 512, 4096, 1024], "go": {str(c): names[i] for i, c in
+                                                              enumerate(tuner.CDS)}}]
+    rng = np.random.default_rng(2)
+    lr = {"xmin": np.zeros(18), "xmax": np.ones(18), "w": rng.normal(size=(18, 5)),
+          "b": rng.normal(size=5)}
+    path = str(tmp_path / "t.table")
+    tuner.write_table(path, ctx, recs, lr)
+    t = sel.parse_table(path)
+    assert t["entries"][0]["variants"] == names and t["entries"][0]["mlog"] == 9
+    np.testing.assert_array_equal(t["lr"]["w"], lr["w"])
+    c2 = gdy.Context(-1, table=path)       # the library accepts it
+    d = gdy.GemmDesc(m=512, n=4096, k=1024, a_type=2, b_type=2, c_type=2, a=1 << 36,
+                     b=2 << 36, c=3 << 36, lda=1024, ldb=4096, ldc=4096, scale_a=1.0,
+                     scale_b=1.0, variant=-1)
+    assert V[c2.isolated_variant(d)]["name"] == names[0]
+
+
+def test_library_rejects_table_naming_unknown_variants(tmp_path):
+    path = str(tmp_path / "bad.table")
+    open(path, "w").write("gdy-go-table 1\ndevice host cus 256\ncatalogue 0123456789abcdef\n"
+                          "entry 2 0 0 9 4096 1024 a b c d e\n")
+    with pytest.raises(gdy.GdyError) as e:
+        gdy.Context(-1, table=path)
+    assert e.value.status == 5
+    open(path, "w").write("not a table\n")
+    with pytest.raises(gdy.GdyError):
+        gdy.Context(-1, table=path)
