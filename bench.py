@@ -256,6 +256,12 @@ def main():
     dtype = specs[0].dtype
 
     plan = ctx.plan(gemms, mode=args.mode)
+    # the paper's execution configurations (Sec. 5.5) on the same set
+    mode_tflops = {}
+    for mode in ("default", "go"):
+        if mode != args.mode:
+            t = time_steps(ctx, arr, n, mode, args.steps, args.warmup, handle, torch)
+            mode_tflops[mode] = round(flops / t / 1e12, 2)
     t_seq = time_steps(ctx, arr, n, "sequential", args.steps, args.warmup, handle, torch)
     t_mode = time_steps(ctx, arr, n, args.mode, args.steps, args.warmup, handle, torch,
                         timing=True)
@@ -285,6 +291,8 @@ def main():
                    "fallback": plan["fallback"]},
         "speedup_vs_sequential": round(t_seq / t_mode, 4),
         "sequential_tflops": round(flops / t_seq / 1e12, 2),
+        "mode_tflops": dict(mode_tflops, sequential=round(flops / t_seq / 1e12, 2),
+                            **{args.mode: round(value, 2)}),
         "pct_mfma_peak": round(100 * value / peak, 2),
         "roofline": roof,
     }

@@ -218,7 +218,10 @@ def plan_selector(gemms: list, table: dict, variants: list, cus: int, slots: int
         x = features(gemms[i], table, variants, by_name, cus)
         out["pred_cd"][i] = clamp(predict_cd(x, table["lr"]), n)
     order = sorted(live, key=lambda i: -out["pred_cd"][i])  # stable: submission order on ties
-    out["groups"] = group(order, out["pred_cd"], slots)
+    groups = group(order, out["pred_cd"], slots)
+    # within a group, longest (2MNK) first; stable
+    out["groups"] = [sorted(grp, key=lambda i: -(gemms[i]["m"] * gemms[i]["n"] * gemms[i]["k"]))
+                     for grp in groups]
     for grp in out["groups"]:
         ci = class_for_size(len(grp))
         for i in grp:

@@ -454,8 +454,8 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
   // GDY_SELECTOR (Sec. 4.3, Sec. 6.7): per-GEMM CD = min(predicted, n);
   // sort by it (descending, stable); greedily form groups whose size never
   // exceeds any member's CD; groups run one after another, each GEMM of a
-  // group on its own stream, bound to the GO-Kernel tuned for the group's
-  // size.  Without a trained predictor every GEMM keeps CD 1.
+  // group on its own stream (longest first), bound to the GO-Kernel tuned
+  // for the group's size.  Without a trained predictor every GEMM keeps CD 1.
   std::vector<int> pred(n, 0);
   for (int t = 0; t < L; ++t) {
     const int i = live[t];
@@ -472,32 +472,38 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
   }
   std::vector<int> ord(live);
   std::stable_sort(ord.begin(), ord.end(), [&](int a, int b) { return pred[a] > pred[b]; });
-  int grp = -1, gsize = 0, gcap = 0;
-  std::vector<int> start;  // first position of each group in ord
+  std::vector<std::vector<int>> groups;
+  int gcap = 0;
   for (int t = 0; t < L; ++t) {
     const int i = ord[t];
     const int cap = std::min(pred[i], S);
-    if (grp < 0 || gsize + 1 > std::min(gcap, cap)) {
-      ++grp;
-      start.push_back(t);
-      gsize = 0;
+    if (groups.empty() || (int)groups.back().size() + 1 > std::min(gcap, cap)) {
+      groups.emplace_back();
       gcap = cap;
     }
     gcap = std::min(gcap, cap);
-    p->order[t] = i;
-    p->group_of[i] = grp;
-    p->stream_of[i] = gsize;
-    ++gsize;
-    p->group_size[grp] = gsize;
+    groups.back().push_back(i);
   }
-  p->n_groups = grp + 1;
+  // within a group, longest first (estimated by 2MNK): the GEMMs whose
+  // tiles take longest are dispatched first
+  int t = 0;
+  p->n_groups = (int)groups.size();
   p->cd = 0;
-  for (int q = 0; q < p->n_groups; ++q) p->cd = std::max(p->cd, p->group_size[q]);
-  for (int t = 0; t < L; ++t) {
-    const int i = ord[t];
-    const int s = p->group_size[p->group_of[i]];
-    p->variant_of[i] = bind_variant(ctx, g[i], class_for_size(s), &fb);
-    if (s == 1) p->stream_of[i] = 0;
+  for (int q = 0; q < p->n_groups; ++q) {
+    std::vector<int>& grp = groups[q];
+    std::stable_sort(grp.begin(), grp.end(), [&](int a, int b) {
+      return g[a].m * g[a].n * g[a].k > g[b].m * g[b].n * g[b].k;
+    });
+    const int s = (int)grp.size();
+    p->group_size[q] = s;
+    p->cd = std::max(p->cd, s);
+    for (int u = 0; u < s; ++u) {
+      const int i = grp[u];
+      p->order[t++] = i;
+      p->group_of[i] = q;
+      p->stream_of[i] = u;
+      p->variant_of[i] = bind_variant(ctx, g[i], class_for_size(s), &fb);
+    }
   }
   p->fallback = fb ? 1 : 0;
 }

@@ -16,7 +16,8 @@
 //    the 16 rows of an MFMA fragment read hit 16 distinct bank groups.
 //  * k-major operand (B untransposed, A transposed): BK rows (one per k) of
 //    ROWS elements, chunk c of row k at position c ^ h(k) with
-//    h(k) = 2*(k%4) + 8*((k/4)%2) (mod chunks per row); fragments are read
+//    h(k) = 4*(k%4) for 16-bit and 2*(k%8) for 8-bit data (mod chunks per
+//    row), which keeps the transpose reads free of bank conflicts; read
 //    with ds_read_b64_tr_b16 / ds_read_b64_tr_b8, which transpose within
 //    each group of 16 lanes: with 16-bit data, output lane i, element j
 //    comes from the address of lane i/4 + 4j, element i%4; with 8-bit data,
@@ -116,8 +117,12 @@ struct DirectT {
   static_assert(BK % (KPI * NW) == 0, "K tile must split into copies per wave");
   static_assert(NCH >= 4, "at least 4 chunks per k-row");
 
+  // k-row swizzle.  A transpose read is serviced 32 lanes at a time: two
+  // 16-lane groups reading 4 (16-bit) or 2 (8-bit) adjacent chunks of the
+  // same 4 (8) k-rows, whose rows all start on bank 0.  XOR-ing the chunk
+  // with 4*(k%4) (2*(k%8)) moves each row's chunks to a distinct bank group.
   static __device__ __forceinline__ int h(int k) {
-    return (2 * (k & 3) + 8 * ((k >> 2) & 1)) & (NCH - 1);
+    return (ES == 2 ? 4 * (k & 3) : 2 * (k & 7)) & (NCH - 1);
   }
   static __device__ __forceinline__ void issue(sdesc src, int ld_bytes, int row0, int k0,
                                                lds_u8* dst, int wave, int lane, int part,

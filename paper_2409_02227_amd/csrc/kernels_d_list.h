@@ -16,7 +16,17 @@
   GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 256, 128, 2, 2, 3),     \
   GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 128, 128, 2, 2, 2)
 
+// 16 waves of 64x64 (4 per SIMD): 16-bit types only (fp8 fragments are
+// twice as wide and would not fit in 128 registers).
+#if GDY_DT16
+#define GDY_TILES_D_WIDE(L, TA, TB) GDY_KERNEL_D(GDY_DT, GDY_DTNAME, TA, TB, L, 256, 256, 4, 4, 2),
+#else
+#define GDY_TILES_D_WIDE(L, TA, TB)
+#endif
+
 static const ::gdy::KernelDesc kTableD[] = {
+    GDY_TILES_D_WIDE("nn", 0, 0)
+    GDY_TILES_D_WIDE("nt", 0, 1)
     GDY_TILES_D("nn", 0, 0),
     GDY_TILES_D("nt", 0, 1),
     GDY_TILES_D_SMALL("tn", 1, 0),
