@@ -75,10 +75,28 @@ typedef enum { GDY_F16 = 1, GDY_BF16 = 2, GDY_FP8_E4M3 = 3 } gdy_dtype;
 typedef enum {
   GDY_SEQUENTIAL = 0, /* isolation-tuned kernel per GEMM, one after another on the origin stream */
   GDY_DEFAULT = 1,    /* isolation-tuned kernels, all n GEMMs at once, one stream each           */
-  GDY_GO = 2,         /* GO-Kernels for CD = n (or forced_cd), all at once                      */
+  GDY_GO = 2,         /* GO-Kernels for CD = n, all at once (forced_cd > 0: groups of forced_cd
+                         in submission order, one after another)                          */
   GDY_SELECTOR = 3,   /* GOLDYLOC: predicted CD per GEMM, grouping, GO-Kernels per group        */
-  GDY_FORCED = 4      /* each GEMM's `variant`, round-robin over forced_cd streams (tuning)     */
+  GDY_FORCED = 4,     /* each GEMM's `variant`, round-robin over forced_cd streams (tuning)     */
+  GDY_FORCED_GROUPED = 5 /* each GEMM's `variant`; consecutive runs of forced_cd GEMMs form
+                            groups run one after another, dispatched as GO and SELECTOR
+                            groups are (tuning)                                             */
 } gdy_mode;
+
+/*
+ * Dispatch of a group (GO, SELECTOR, FORCED_GROUPED): the GEMMs of a group
+ * that are bound to the same kernel share ONE kernel dispatch (up to 16 per
+ * dispatch; each GEMM keeps its own grid cap as its share of the grid) in
+ * launch order.  The first dispatch of a group runs on the origin stream,
+ * further ones on pool streams forked from and joined back to it.  A
+ * hardware queue switch costs tens of microseconds on MI355X, far more than
+ * the small GEMMs of a group take, so the concurrency of a group lives in one
+ * grid wherever its kernels allow.  Each tile is computed by the same code as
+ * in an isolated launch, so results are bit-identical.  SEQUENTIAL, DEFAULT
+ * and FORCED launch one dispatch per GEMM.
+ */
+#define GDY_MAX_FUSED 16
 
 /* One GEMM of a submission. */
 typedef struct {
@@ -101,10 +119,13 @@ typedef struct {
   int32_t fallback;                     /* 1: no GO table, isolated heuristics were used    */
   int32_t order[GDY_MAX_GEMMS];         /* launch order: order[t] is a GEMM index          */
   int32_t group_of[GDY_MAX_GEMMS];      /* group of GEMM i                                 */
-  int32_t stream_of[GDY_MAX_GEMMS];     /* pool stream slot of GEMM i (-1: origin stream)  */
+  int32_t stream_of[GDY_MAX_GEMMS];     /* pool stream slot of GEMM i's dispatch (-1: origin) */
   int32_t variant_of[GDY_MAX_GEMMS];    /* variant id bound to GEMM i (-1: not launched)   */
   int32_t pred_cd[GDY_MAX_GEMMS];       /* selector: min(predicted CD, n) of GEMM i, else 0 */
   int32_t group_size[GDY_MAX_GEMMS];    /* size of group g (first n_groups entries)        */
+  int32_t n_dispatches;                 /* kernel dispatches of the submission              */
+  int32_t dispatch_of[GDY_MAX_GEMMS];   /* dispatch that runs GEMM i (-1: none); dispatches
+                                           are numbered in launch order                    */
 } gdy_plan_t;
 
 /* Static description of one catalogue variant (a kernel plus its grid cap). */
@@ -178,12 +199,13 @@ gdy_status gdy_execute(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t m
                        int32_t forced_cd, void* hip_stream, gdy_plan_t* out);
 
 /*
- * Per-kernel timing.  When enabled, every launch of gdy_execute records a
+ * Per-kernel timing.  When enabled, every dispatch of gdy_execute records a
  * start and a stop event on the stream it runs on (hipExtLaunchKernel), and
  * a submission start event on the origin stream.  After the caller has
  * synchronised, gdy_last_kernel_times fills start_ms[i] / end_ms[i]
  * (milliseconds from the submission start) for GEMM i of the last
- * submission; GEMMs that launched nothing get -1.
+ * submission; GEMMs that launched nothing get -1.  GEMMs that share a
+ * dispatch report that dispatch's interval.
  */
 gdy_status gdy_set_timing(gdy_ctx* ctx, int32_t enable);
 gdy_status gdy_last_kernel_times(gdy_ctx* ctx, float* start_ms, float* end_ms, int32_t n);

@@ -20,6 +20,11 @@ Definitions followed:
     prefer that CD; otherwise they are split into smaller sets.  Reading
     used: sort by the (clamped) preferred CD, largest first, and grow each
     group while its size stays within every member's preferred CD.
+  * Launch of a group (a property of the library, not of the paper): the
+    GEMMs of a group bound to the same kernel (variant name without its
+    grid-cap suffix) share one dispatch, at most 16 each, numbered in order
+    of first use; a group's first dispatch runs on the origin stream (-1),
+    the others round-robin on the pool streams.
   * GO library (Sec. 4.2.2): each GEMM shape maps to one kernel per CD;
     shapes that were not tuned take the nearest tuned shape (log2 distance
     in M, N, K), and a group of s GEMMs takes the kernel of the CD class
@@ -202,6 +207,33 @@ def group(order: list, pref: dict, slots: int) -> list:
     return groups
 
 
+MAX_FUSED = 16
+
+
+def kernel_of(name: str) -> str:
+    return name.rsplit("_c", 1)[0]
+
+
+def dispatches(groups: list, variant_of: dict, variants: list, slots: int):
+    """dispatch_of and stream_of per GEMM for groups launched one after another."""
+    dispatch_of, stream_of, nxt = {}, {}, 0
+    for grp in groups:
+        opened = []  # [kernel, dispatch id, members]
+        for i in grp:
+            k = kernel_of(variants[variant_of[i]]["name"])
+            hit = [u for u, o in enumerate(opened) if o[0] == k and o[2] < MAX_FUSED]
+            if hit:
+                u = hit[-1]
+            else:
+                opened.append([k, nxt, 0])
+                nxt += 1
+                u = len(opened) - 1
+            opened[u][2] += 1
+            dispatch_of[i] = opened[u][1]
+            stream_of[i] = -1 if u == 0 else (u - 1) % max(slots, 1)
+    return dispatch_of, stream_of, nxt
+
+
 def plan_selector(gemms: list, table: dict, variants: list, cus: int, slots: int) -> dict:
     """What a GOLDYLOC submission runs: per-GEMM clamped CD, groups (run one
     after another) and the kernel bound to each GEMM."""
@@ -213,6 +245,8 @@ def plan_selector(gemms: list, table: dict, variants: list, cus: int, slots: int
         for i in live:
             out["variant_of"][i] = bind(gemms[i], 0, table, variants, by_name)
         out["groups"] = [live] if live else []
+        out["dispatch_of"], out["stream_of"], out["n_dispatches"] = dispatches(
+            out["groups"], out["variant_of"], variants, slots)
         return out
     for i in live:
         x = features(gemms[i], table, variants, by_name, cus)
@@ -226,4 +260,6 @@ def plan_selector(gemms: list, table: dict, variants: list, cus: int, slots: int
         ci = class_for_size(len(grp))
         for i in grp:
             out["variant_of"][i] = bind(gemms[i], ci, table, variants, by_name)
+    out["dispatch_of"], out["stream_of"], out["n_dispatches"] = dispatches(
+        out["groups"], out["variant_of"], variants, slots)
     return out

@@ -83,8 +83,9 @@ uint64_t fnv1a(const std::string& s, uint64_t h) {
 // Per-kernel timing events of one submission (created on first use).
 struct TimingSlot {
   hipEvent_t sub_start = nullptr;
-  std::vector<hipEvent_t> start, stop;
-  std::vector<char> launched;
+  std::vector<hipEvent_t> start, stop;  // per dispatch
+  std::vector<char> launched;           // per dispatch
+  std::vector<int> dispatch_of;         // per GEMM
   int n = 0;
 };
 const int kTimingRing = 64;
@@ -356,12 +357,13 @@ gdy_status validate(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode
   if (n < 0) return fail(ctx, GDY_ERR_INVALID_ARG, "n < 0");
   if (n > GDY_MAX_GEMMS) return fail(ctx, GDY_ERR_TOO_MANY, "n = %d > %d", n, GDY_MAX_GEMMS);
   if (n > 0 && !gemms) return fail(ctx, GDY_ERR_INVALID_ARG, "null gemm array");
-  if (mode < GDY_SEQUENTIAL || mode > GDY_FORCED) return fail(ctx, GDY_ERR_INVALID_ARG, "bad mode %d", mode);
+  if (mode < GDY_SEQUENTIAL || mode > GDY_FORCED_GROUPED)
+    return fail(ctx, GDY_ERR_INVALID_ARG, "bad mode %d", mode);
   std::vector<Extent> ea(n), eb(n), ec(n);
   for (int i = 0; i < n; ++i) {
     gdy_status s = validate_one(ctx, gemms[i], i, &ea[i], &eb[i], &ec[i]);
     if (s != GDY_OK) return s;
-    if (mode == GDY_FORCED && gemms[i].m > 0 && gemms[i].n > 0 &&
+    if ((mode == GDY_FORCED || mode == GDY_FORCED_GROUPED) && gemms[i].m > 0 && gemms[i].n > 0 &&
         !variant_fits(ctx, gemms[i].variant, gemms[i]))
       return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: variant %d does not fit its dtype/layout", i,
                   gemms[i].variant);
@@ -388,6 +390,30 @@ void plan_reset(gdy_plan_t* p, int n) {
     p->group_of[i] = -1;
     p->stream_of[i] = -1;
     p->variant_of[i] = -1;
+    p->dispatch_of[i] = -1;
+  }
+}
+
+// Dispatches of one group (members in launch order, variants bound): GEMMs
+// of the same kernel share a dispatch, at most kMaxFused each, numbered in
+// order of first use.  The group's first dispatch runs on the origin
+// stream, the others round-robin on the pool.
+void form_dispatches(const gdy_ctx* ctx, const std::vector<int>& members, int S, gdy_plan_t* p) {
+  std::vector<int> kern, id, cnt;
+  for (int i : members) {
+    const int k = ctx->variants[p->variant_of[i]].kernel;
+    int d = -1;
+    for (size_t u = 0; u < kern.size(); ++u)
+      if (kern[u] == k && cnt[u] < kMaxFused) d = (int)u;
+    if (d < 0) {
+      d = (int)kern.size();
+      kern.push_back(k);
+      id.push_back(p->n_dispatches++);
+      cnt.push_back(0);
+    }
+    ++cnt[d];
+    p->dispatch_of[i] = id[d];
+    p->stream_of[i] = d == 0 ? -1 : (d - 1) % std::max(S, 1);
   }
 }
 
@@ -418,44 +444,72 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
       p->order[t] = i;
       p->group_of[i] = 0;
       p->stream_of[i] = -1;
+      p->dispatch_of[i] = t;
       p->variant_of[i] = bind_variant(ctx, g[i], 0, &fb);
     }
     p->n_groups = L > 0 ? 1 : 0;
     p->group_size[0] = L;
+    p->n_dispatches = L;
     p->cd = L > 0 ? 1 : 0;
     p->fallback = (fb || !ctx->table.loaded) ? 1 : 0;
     return;
   }
 
-  if (mode == GDY_DEFAULT || mode == GDY_GO || mode == GDY_FORCED) {
+  if (mode == GDY_DEFAULT || mode == GDY_FORCED) {
+    // Sec. 5.5 default concurrency: one stream per GEMM (round-robin over
+    // forced_cd streams for FORCED), one dispatch each
     int cd = L;
-    if ((mode == GDY_GO || mode == GDY_FORCED) && forced_cd > 0) cd = std::min(forced_cd, std::max(L, 1));
+    if (mode == GDY_FORCED && forced_cd > 0) cd = std::min(forced_cd, std::max(L, 1));
     cd = std::max(1, std::min(cd, S));
-    const int ci = class_for_size(mode == GDY_GO && forced_cd > 0 ? forced_cd : L);
     for (int t = 0; t < L; ++t) {
       const int i = live[t];
       p->order[t] = i;
       p->group_of[i] = 0;
       p->stream_of[i] = t % cd;
-      if (mode == GDY_DEFAULT)
-        p->variant_of[i] = bind_variant(ctx, g[i], 0, &fb);
-      else if (mode == GDY_GO)
-        p->variant_of[i] = bind_variant(ctx, g[i], ci, &fb);
-      else
-        p->variant_of[i] = runnable(ctx, g[i].variant, g[i]);
+      p->dispatch_of[i] = t;
+      p->variant_of[i] = mode == GDY_DEFAULT ? bind_variant(ctx, g[i], 0, &fb)
+                                             : runnable(ctx, g[i].variant, g[i]);
     }
     p->n_groups = L > 0 ? 1 : 0;
     p->group_size[0] = L;
+    p->n_dispatches = L;
     p->cd = L > 0 ? cd : 0;
     p->fallback = (mode != GDY_FORCED && (fb || !ctx->table.loaded)) ? 1 : 0;
     return;
   }
 
+  if (mode == GDY_GO || mode == GDY_FORCED_GROUPED) {
+    // GO: the GO-Kernels of CD = n (Sec. 5.5), or groups of forced_cd in
+    // submission order; FORCED_GROUPED: the same grouping with each GEMM's
+    // own variant (tuning of the grouped launch)
+    const int size = forced_cd > 0 ? forced_cd : std::max(L, 1);
+    int t = 0;
+    for (int q = 0; t < L; ++q) {
+      std::vector<int> grp;
+      for (; t < L && (int)grp.size() < size; ++t) grp.push_back(live[t]);
+      const int ci = class_for_size(mode == GDY_GO && forced_cd > 0 ? forced_cd : (int)grp.size());
+      for (size_t u = 0; u < grp.size(); ++u) {
+        const int i = grp[u];
+        p->order[t - (int)grp.size() + (int)u] = i;
+        p->group_of[i] = q;
+        p->variant_of[i] = mode == GDY_GO ? bind_variant(ctx, g[i], ci, &fb)
+                                          : runnable(ctx, g[i].variant, g[i]);
+      }
+      p->group_size[q] = (int)grp.size();
+      p->n_groups = q + 1;
+      p->cd = std::max(p->cd, (int)grp.size());
+      form_dispatches(ctx, grp, S, p);
+    }
+    p->fallback = (mode == GDY_GO && (fb || !ctx->table.loaded)) ? 1 : 0;
+    return;
+  }
+
   // GDY_SELECTOR (Sec. 4.3, Sec. 6.7): per-GEMM CD = min(predicted, n);
   // sort by it (descending, stable); greedily form groups whose size never
-  // exceeds any member's CD; groups run one after another, each GEMM of a
-  // group on its own stream (longest first), bound to the GO-Kernel tuned
-  // for the group's size.  Without a trained predictor every GEMM keeps CD 1.
+  // exceeds any member's CD; groups run one after another, longest GEMM
+  // first within a group, each bound to the GO-Kernel tuned for the group's
+  // size and dispatched with the group's other GEMMs of the same kernel.
+  // Without a trained predictor every GEMM keeps CD 1.
   std::vector<int> pred(n, 0);
   for (int t = 0; t < L; ++t) {
     const int i = live[t];
@@ -501,9 +555,9 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
       const int i = grp[u];
       p->order[t++] = i;
       p->group_of[i] = q;
-      p->stream_of[i] = u;
       p->variant_of[i] = bind_variant(ctx, g[i], class_for_size(s), &fb);
     }
+    form_dispatches(ctx, grp, S, p);
   }
   p->fallback = fb ? 1 : 0;
 }
@@ -571,14 +625,40 @@ hipStream_t slot_stream(const gdy_ctx* ctx, int slot) {
   return ctx->pool[slot];
 }
 
+// Workgroup ranges of one dispatch: each GEMM gets its own grid (tiles, or
+// its cap x occupancy), every range but the last rounded up to a multiple
+// of 8 so each GEMM starts on XCD 0 (the extra workgroups find no tile).
+gdy_status build_launch(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p,
+                        const std::vector<int>& members, KLaunch* L, int* grid) {
+  std::memset(L, 0, sizeof *L);
+  L->count = (int)members.size();
+  int64_t wg = 0;
+  for (int u = 0; u < L->count; ++u) {
+    const int i = members[u];
+    Geometry geo;
+    L->g[u] = make_args(ctx, p.variant_of[i], g[i], &geo);
+    L->first[u] = (int32_t)wg;
+    int span = std::max(geo.grid, 1);
+    if (u + 1 < L->count) span = (span + 7) & ~7;
+    wg += span;
+  }
+  if (wg > INT32_MAX) return fail(ctx, GDY_ERR_UNSUPPORTED, "dispatch grid of %lld workgroups", (long long)wg);
+  L->first[L->count] = (int32_t)wg;
+  *grid = (int)wg;
+  return GDY_OK;
+}
+
 gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, hipStream_t origin) {
   gdy_status st = GDY_OK;
   const int n = p.n;
+  int L = 0;
+  while (L < GDY_MAX_GEMMS && p.order[L] >= 0) ++L;
+  const int D = p.n_dispatches;
   TimingSlot* ts = nullptr;
   if (ctx->timing) {
     ts = &ctx->ring[ctx->submissions % kTimingRing];
     if (!ts->sub_start) HIP_TRY(ctx, hipEventCreate(&ts->sub_start));
-    while ((int)ts->start.size() < n) {
+    while ((int)ts->start.size() < D) {
       hipEvent_t a, b;
       HIP_TRY(ctx, hipEventCreate(&a));
       HIP_TRY(ctx, hipEventCreate(&b));
@@ -586,64 +666,63 @@ gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, hip
       ts->stop.push_back(b);
     }
     ts->n = n;
-    ts->launched.assign(n, 0);
+    ts->dispatch_of.assign(p.dispatch_of, p.dispatch_of + n);
+    ts->launched.assign(D, 0);
     ++ctx->submissions;
     HIP_TRY(ctx, hipEventRecord(ts->sub_start, origin));
   }
 
-  // launch order is p.order; groups are contiguous in it
-  std::vector<int> prev_slots;  // slots used by the previous group
-  bool forked = false;
+  // launch order is p.order; groups are contiguous in it, and so are the
+  // members of a dispatch once its first member has appeared
   int t = 0;
-  int L = 0;
-  while (L < GDY_MAX_GEMMS && p.order[L] >= 0) ++L;
-  for (int grp = 0; grp < p.n_groups; ++grp) {
-    std::vector<int> slots;
-    const int t0 = t;
-    while (t < L && p.group_of[p.order[t]] == grp) {
-      const int s = p.stream_of[p.order[t]];
-      if (s >= 0 && std::find(slots.begin(), slots.end(), s) == slots.end()) slots.push_back(s);
-      ++t;
-    }
-    // order this group's streams after the origin (first group) or the
-    // previous group
-    for (int s : slots) {
-      hipStream_t hs = slot_stream(ctx, s);
-      if (grp == 0 || prev_slots.empty()) {
-        if (!forked) {
-          HIP_TRY(ctx, hipEventRecord(ctx->fork_ev, origin));
-          forked = true;
-        }
-        HIP_TRY(ctx, hipStreamWaitEvent(hs, ctx->fork_ev, 0));
-      } else {
-        for (int q : prev_slots)
-          if (q != s) HIP_TRY(ctx, hipStreamWaitEvent(hs, ctx->done[q], 0));
+  for (int grp = 0; grp < p.n_groups && st == GDY_OK; ++grp) {
+    std::vector<int> ids;                    // dispatches of this group, launch order
+    std::vector<std::vector<int>> members;  // their GEMMs
+    std::vector<int> slots;                  // pool slots the group uses
+    for (; t < L && p.group_of[p.order[t]] == grp; ++t) {
+      const int i = p.order[t];
+      const int d = p.dispatch_of[i];
+      size_t u = 0;
+      while (u < ids.size() && ids[u] != d) ++u;
+      if (u == ids.size()) {
+        ids.push_back(d);
+        members.emplace_back();
+        const int s = p.stream_of[i];
+        if (s >= 0 && std::find(slots.begin(), slots.end(), s) == slots.end()) slots.push_back(s);
       }
+      members[u].push_back(i);
     }
-    for (int u = t0; u < t && st == GDY_OK; ++u) {
-      const int i = p.order[u];
-      const int vid = p.variant_of[i];
+    // fork: pool streams start after what the origin holds
+    if (!slots.empty()) {
+      HIP_TRY(ctx, hipEventRecord(ctx->fork_ev, origin));
+      for (int s : slots) HIP_TRY(ctx, hipStreamWaitEvent(slot_stream(ctx, s), ctx->fork_ev, 0));
+    }
+    for (size_t u = 0; u < ids.size(); ++u) {
+      const int i0 = members[u][0];
+      const int vid = p.variant_of[i0];
       const Kernel& k = ctx->kernels[ctx->variants[vid].kernel];
-      Geometry geo;
-      KArgs args = make_args(ctx, vid, g[i], &geo);
-      void* argv[] = {&args};
-      hipStream_t hs = p.stream_of[i] >= 0 ? slot_stream(ctx, p.stream_of[i]) : origin;
-      hipError_t e = hipExtLaunchKernel(k.d->func, dim3(std::max(geo.grid, 1)), dim3(k.d->waves * 64),
-                                        argv, 0, hs, ts ? ts->start[i] : nullptr,
-                                        ts ? ts->stop[i] : nullptr, 0);
+      KLaunch launch;
+      int grid = 0;
+      st = build_launch(ctx, g, p, members[u], &launch, &grid);
+      if (st != GDY_OK) break;
+      void* argv[] = {&launch};
+      const int d = ids[u];
+      hipStream_t hs = p.stream_of[i0] >= 0 ? slot_stream(ctx, p.stream_of[i0]) : origin;
+      hipError_t e = hipExtLaunchKernel(k.d->func, dim3(grid), dim3(k.d->waves * 64), argv, 0, hs,
+                                        ts ? ts->start[d] : nullptr, ts ? ts->stop[d] : nullptr, 0);
       if (e != hipSuccess) {
-        st = fail(ctx, GDY_ERR_HIP, "launch of %s for gemm %d failed: %s",
-                  ctx->variants[vid].name.c_str(), i, hipGetErrorString(e));
+        st = fail(ctx, GDY_ERR_HIP, "launch of %s (%d GEMMs, first %d) failed: %s",
+                  ctx->variants[vid].name.c_str(), (int)members[u].size(), i0, hipGetErrorString(e));
         break;
       }
-      if (ts) ts->launched[i] = 1;
+      if (ts) ts->launched[d] = 1;
     }
-    for (int s : slots) HIP_TRY(ctx, hipEventRecord(ctx->done[s], slot_stream(ctx, s)));
-    if (!slots.empty()) prev_slots = slots;
-    if (st != GDY_OK) break;
+    // join: the origin continues after the group's pool streams
+    for (int s : slots) {
+      HIP_TRY(ctx, hipEventRecord(ctx->done[s], slot_stream(ctx, s)));
+      HIP_TRY(ctx, hipStreamWaitEvent(origin, ctx->done[s], 0));
+    }
   }
-  // join: the origin waits for the streams of the last group that used the pool
-  for (int s : prev_slots) HIP_TRY(ctx, hipStreamWaitEvent(origin, ctx->done[s], 0));
   return st;
 }
 
@@ -978,9 +1057,11 @@ gdy_status gdy_kernel_times(gdy_ctx* ctx, int32_t back, float* start_ms, float* 
   const TimingSlot& ts = ctx->ring[(ctx->submissions - 1 - back) % kTimingRing];
   for (int i = 0; i < n; ++i) {
     start_ms[i] = end_ms[i] = -1.f;
-    if (i >= ts.n || !ts.launched[i]) continue;
-    HIP_TRY(ctx, hipEventElapsedTime(&start_ms[i], ts.sub_start, ts.start[i]));
-    HIP_TRY(ctx, hipEventElapsedTime(&end_ms[i], ts.sub_start, ts.stop[i]));
+    if (i >= ts.n) continue;
+    const int d = ts.dispatch_of[i];
+    if (d < 0 || !ts.launched[d]) continue;
+    HIP_TRY(ctx, hipEventElapsedTime(&start_ms[i], ts.sub_start, ts.start[d]));
+    HIP_TRY(ctx, hipEventElapsedTime(&end_ms[i], ts.sub_start, ts.stop[d]));
   }
   return GDY_OK;
 }

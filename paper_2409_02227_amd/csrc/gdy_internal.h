@@ -31,6 +31,19 @@ struct KArgs {
   int32_t xcd_remap;  // 1: keep consecutive tiles on one XCD
 };
 
+// One kernel dispatch: up to kMaxFused GEMMs that use the same kernel share
+// one grid.  GEMM i owns workgroups [first[i], first[i+1]) and walks its own
+// tiles with that range's length as the stride, so a tile is computed by
+// exactly the same code (and gives the same bits) whether the GEMM runs
+// alone or fused with others.  first[i] is a multiple of 8 for i > 0 so a
+// GEMM's local workgroup index keeps the hardware's XCD round-robin phase.
+constexpr int kMaxFused = 16;
+struct KLaunch {
+  int32_t count;                  // GEMMs in this dispatch, 1..kMaxFused
+  int32_t first[kMaxFused + 1];   // workgroup ranges; first[count] = grid size
+  KArgs g[kMaxFused];
+};
+
 // Compile-time description of one instantiated kernel.
 struct KernelDesc {
   const char* name;   // e.g. "bf16_nn_256x256_w8_m32"

@@ -332,6 +332,15 @@ __device__ __forceinline__ void tile_coords(int t, const KArgs& p, int& tm, int&
   tn = in_group / rows_here;
 }
 
+// The GEMM of a fused dispatch that owns this workgroup (uniform per
+// workgroup: a short scalar scan of the workgroup ranges).
+__device__ __forceinline__ int owner_of(const KLaunch& L) {
+  const int b = (int)blockIdx.x;
+  int i = 0;
+  while (i + 1 < L.count && b >= L.first[i + 1]) ++i;
+  return i;
+}
+
 template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int MM>
 struct GoCfg {
   static constexpr int ES = ElemSize<DT>::v;
@@ -355,7 +364,7 @@ struct GoCfg {
 
 template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int MM>
 __global__ void __launch_bounds__(WM * WN * 64)
-go_gemm(KArgs p) {
+go_gemm(KLaunch L) {
   typedef GoCfg<DT, TA, TB, BM, BN, WM, WN, MM> C;
   typedef typename C::M M;
   typedef typename M::Frag Frag;
@@ -364,6 +373,11 @@ go_gemm(KArgs p) {
   typedef typename StageSel<TB == 1, C::ES, BN, C::NT>::T StB;
 
   __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
+
+  const int gi = owner_of(L);
+  const KArgs& p = L.g[gi];
+  const int wg0 = L.first[gi];
+  const int nwg = L.first[gi + 1] - wg0;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -381,7 +395,7 @@ go_gemm(KArgs p) {
   const int ldc_b = (int)p.ldc * 2;
   const int Mrows = (int)p.m, Ncols = (int)p.n;
 
-  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+  for (int t = (int)blockIdx.x - wg0; t < ntiles; t += nwg) {
     int tm, tn;
     tile_coords(t, p, tm, tn);
     const int m0 = tm * BM;

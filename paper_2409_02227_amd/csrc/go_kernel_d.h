@@ -246,7 +246,7 @@ struct DCfg {
 
 template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int STAGES, int KB>
 __global__ void __launch_bounds__(WM * WN * 64)
-go_gemm_d(KArgs p) {
+go_gemm_d(KLaunch L) {
   typedef DCfg<DT, TA, TB, BM, BN, WM, WN, STAGES, KB> C;
   typedef typename C::M M;
   typedef typename FragT<C::ES>::T Frag;
@@ -261,6 +261,11 @@ go_gemm_d(KArgs p) {
 
   __shared__ __attribute__((aligned(1024))) uint8_t smem_raw[C::LDS];
   lds_u8* smem = (lds_u8*)smem_raw;
+
+  const int gi = owner_of(L);
+  const KArgs& p = L.g[gi];
+  const int wg0 = L.first[gi];
+  const int nwg = L.first[gi + 1] - wg0;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -295,7 +300,7 @@ go_gemm_d(KArgs p) {
       for (int hh = 0; hh < NHH; ++hh) boff[j][hh] = kt_lane<C::ES, BT>(lane, wn * C::WTN + j * 32, hh);
   }
 
-  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+  for (int t = (int)blockIdx.x - wg0; t < ntiles; t += nwg) {
     int tm, tn;
     tile_coords(t, p, tm, tn);
     const int m0 = tm * BM;

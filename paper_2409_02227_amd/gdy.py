@@ -22,9 +22,9 @@ CD_CLASSES = (1, 2, 4, 8, 16)
 # gdy_dtype
 F16, BF16, FP8_E4M3 = 1, 2, 3
 # gdy_mode
-SEQUENTIAL, DEFAULT, GO, SELECTOR, FORCED = 0, 1, 2, 3, 4
+SEQUENTIAL, DEFAULT, GO, SELECTOR, FORCED, FORCED_GROUPED = 0, 1, 2, 3, 4, 5
 MODES = {"sequential": SEQUENTIAL, "default": DEFAULT, "go": GO,
-         "selector": SELECTOR, "forced": FORCED}
+         "selector": SELECTOR, "forced": FORCED, "forced_grouped": FORCED_GROUPED}
 
 STATUS = {0: "GDY_OK", 1: "GDY_ERR_INVALID_ARG", 2: "GDY_ERR_UNSUPPORTED", 3: "GDY_ERR_ALIAS",
           4: "GDY_ERR_TOO_MANY", 5: "GDY_ERR_TABLE", 6: "GDY_ERR_HIP", 7: "GDY_ERR_NOMEM"}
@@ -52,7 +52,8 @@ class Plan(ctypes.Structure):
                 ("fallback", ctypes.c_int32),
                 ("order", ctypes.c_int32 * MAX_GEMMS), ("group_of", ctypes.c_int32 * MAX_GEMMS),
                 ("stream_of", ctypes.c_int32 * MAX_GEMMS), ("variant_of", ctypes.c_int32 * MAX_GEMMS),
-                ("pred_cd", ctypes.c_int32 * MAX_GEMMS), ("group_size", ctypes.c_int32 * MAX_GEMMS)]
+                ("pred_cd", ctypes.c_int32 * MAX_GEMMS), ("group_size", ctypes.c_int32 * MAX_GEMMS),
+                ("n_dispatches", ctypes.c_int32), ("dispatch_of", ctypes.c_int32 * MAX_GEMMS)]
 
     def as_dict(self) -> dict:
         n = self.n
@@ -60,7 +61,8 @@ class Plan(ctypes.Structure):
                 "order": [x for x in self.order[:n] if x >= 0],
                 "group_of": list(self.group_of[:n]), "stream_of": list(self.stream_of[:n]),
                 "variant_of": list(self.variant_of[:n]), "pred_cd": list(self.pred_cd[:n]),
-                "group_size": list(self.group_size[:self.n_groups])}
+                "group_size": list(self.group_size[:self.n_groups]),
+                "n_dispatches": self.n_dispatches, "dispatch_of": list(self.dispatch_of[:n])}
 
 
 class VariantDesc(ctypes.Structure):

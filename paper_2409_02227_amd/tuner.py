@@ -128,8 +128,8 @@ def operands(torch, dtype, ta, tb, m, n, k, copies, outputs_per_copy):
 
 
 def submission(ops, cd, rounds, vid, ta, tb):
-    """cd copies, each run `rounds` times; entry i belongs to copy i % cd so
-    FORCED mode's round-robin puts a copy's runs back-to-back on one stream."""
+    """cd copies, each run `rounds` times; entry i belongs to copy i % cd, so
+    each run of cd consecutive entries is one group of all cd copies."""
     from paper_2409_02227_amd import gdy
     out = []
     for r in range(rounds):
@@ -187,13 +187,15 @@ def tune_shape(ctx, bench, torch, variants, shape, rounds=3):
                 pool.append(vid)
     rec["pool"] = [variants[v]["name"] for v in pool]
     rec["go"] = {"1": variants[best_iso]["name"]}
-    # step 2: each CD co-runs cd copies, `rounds` runs back-to-back per stream
+    # step 2: each CD co-runs cd copies as one group, launched the way the
+    # library launches a group (one dispatch per kernel); `rounds` groups run
+    # one after another
     for cd in CDS[1:]:
         n_g = cd * rounds
         t_seq = bench.time(submission(ops, cd, rounds, best_iso, ta, tb), "forced", 1) / n_g
         best, best_t = None, None
         for vid in pool:
-            t = bench.time(submission(ops, cd, rounds, vid, ta, tb), "forced", cd) / n_g
+            t = bench.time(submission(ops, cd, rounds, vid, ta, tb), "forced_grouped", cd) / n_g
             if best_t is None or t < best_t:
                 best, best_t = vid, t
         rec["seq"][str(cd)] = t_seq

@@ -35,7 +35,8 @@ def test_struct_layouts_match_header():
     # gdy_gemm: 3 int64, 5 int32, then (ptr, int64) x 3, 2 floats, 2 int32
     assert ctypes.sizeof(gdy.GemmDesc) == 3 * 8 + 5 * 4 + 4 + 6 * 8 + 2 * 4 + 2 * 4
     assert gdy.GemmDesc.a.offset == 48
-    assert ctypes.sizeof(gdy.Plan) == 4 * 4 + 6 * 4 * gdy.MAX_GEMMS
+    assert ctypes.sizeof(gdy.Plan) == 4 * 4 + 6 * 4 * gdy.MAX_GEMMS + 4 + 4 * gdy.MAX_GEMMS
+    assert gdy.Plan.dispatch_of.offset == 4 * 4 + 6 * 4 * gdy.MAX_GEMMS + 4
     assert ctypes.sizeof(gdy.VariantDesc) == 64 + 13 * 4
     text = open(HEADER).read()
     assert "#define GDY_MAX_GEMMS 256" in text and "#define GDY_N_FEATURES 18" in text

@@ -258,3 +258,83 @@ def test_direct_falls_back_when_ineligible(ctx):
     ran = ctx.variant(plan["variant_of"][0])
     assert not ran["direct"] and (ran["bm"], ran["bn"]) == (128, 128)
     check(mat)
+
+
+def _isolated_codes(ctx, mats, vids):
+    out = []
+    for m, vid in zip(mats, vids):
+        _run(ctx, [m], "forced", 1, [vid])
+        out.append(out_codes(m).copy())
+    return out
+
+
+def test_fused_dispatch_mixed_shapes_and_caps(ctx):
+    """GEMMs of different shapes (ragged tails, K = 0, one element) and grid
+    caps of one kernel share a single dispatch; each GEMM's result equals its
+    isolated launch bit for bit and passes the oracle."""
+    name = "bf16_nn_128x128_w2x2_m32"
+    caps = [ctx.find(f"{name}_c{c}") for c in (0, 32, 128, 64)]
+    assert min(caps) >= 0
+    shapes = [(300, 1000, 700), (64, 4096, 1024), (5, 77, 33), (513, 129, 256), (1, 1, 1),
+              (40, 50, 0), (200, 300, 100), (129, 257, 65)]
+    mats = [inputs.materialize(GemmSpec(m, n, k, "bf16", seed=600 + i, name=f"f{i}"))
+            for i, (m, n, k) in enumerate(shapes)]
+    vids = [caps[i % 4] for i in range(len(mats))]
+    iso = _isolated_codes(ctx, mats, vids)
+    plan = _run(ctx, mats, "forced_grouped", 0, vids)
+    assert plan["n_dispatches"] == 1 and set(plan["dispatch_of"]) == {0}
+    assert all(s == -1 for s in plan["stream_of"])
+    for m, ref in zip(mats, iso):
+        assert np.array_equal(out_codes(m), ref), f"{m.spec.name}: fused differs from isolated"
+        check(m, label="fused")
+
+
+def test_fused_dispatch_direct_kernels(ctx):
+    """Direct kernels (global->LDS copies) fused: 16-byte aligned operands,
+    K whole K tiles, ragged M and N."""
+    for dt in ("bf16", "fp8"):
+        vid = ctx.find(f"{dt}_nn_128x128_w2x2_d2_c0")
+        assert vid >= 0
+        bk = ctx.variant(vid)["bk"]
+        es = 1 if dt == "fp8" else 2
+        shapes = [(300, 1000, 4 * bk), (64, 520, bk), (257, 136, 2 * bk), (128, 128, 3 * bk)]
+        mats = []
+        for i, (m, n, k) in enumerate(shapes):
+            mats.append(inputs.materialize(GemmSpec(
+                m, n, k, dt, 0, 0, seed=700 + i, name=f"fd{i}", pad_a=_pad_to(k, 16 // es),
+                pad_b=_pad_to(n, 16 // es), pad_c=3)))
+        vids = [vid] * len(mats)
+        iso = _isolated_codes(ctx, mats, vids)
+        plan = _run(ctx, mats, "forced_grouped", 0, vids)
+        assert plan["n_dispatches"] == 1 and all(v == vid for v in plan["variant_of"])
+        for m, ref in zip(mats, iso):
+            assert np.array_equal(out_codes(m), ref), f"{dt} {m.spec.name}: fused differs"
+            check(m, label=f"fused direct {dt}")
+
+
+def test_fused_dispatch_chunks_and_kernel_split(ctx):
+    """20 GEMMs of one kernel make two dispatches (16 + 4, the second on a
+    pool stream); a group with two kernels makes one dispatch per kernel."""
+    vid = ctx.find("bf16_nn_64x128_w1x4_m32_c0")
+    other = ctx.find("bf16_nn_128x128_w2x2_m32_c0")
+    assert vid >= 0 and other >= 0
+    mats = [inputs.materialize(GemmSpec(100 + 7 * i, 200 + 3 * i, 96, "bf16", seed=800 + i,
+                                        name=f"ch{i}")) for i in range(20)]
+    iso = _isolated_codes(ctx, mats, [vid] * 20)
+    plan = _run(ctx, mats, "forced_grouped", 0, [vid] * 20)
+    assert plan["n_dispatches"] == 2
+    assert plan["dispatch_of"] == [0] * 16 + [1] * 4
+    assert plan["stream_of"] == [-1] * 16 + [0] * 4
+    for m, ref in zip(mats, iso):
+        assert np.array_equal(out_codes(m), ref), f"{m.spec.name}: chunked dispatch differs"
+    check(mats[0])
+    check(mats[19])
+    # two kernels alternating in groups of 4: two dispatches per group
+    vids = [vid if i % 2 == 0 else other for i in range(8)]
+    sub = mats[:8]
+    iso = _isolated_codes(ctx, sub, vids)
+    plan = _run(ctx, sub, "forced_grouped", 4, vids)
+    assert plan["n_groups"] == 2 and plan["n_dispatches"] == 4
+    assert plan["dispatch_of"] == [0, 1, 0, 1, 2, 3, 2, 3]
+    for m, ref in zip(sub, iso):
+        assert np.array_equal(out_codes(m), ref), f"{m.spec.name}: split dispatch differs"

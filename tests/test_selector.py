@@ -157,6 +157,10 @@ def _check_plan(ctx, table, descs, slots=16):
         if len(live) > 1:
             assert p["pred_cd"][i] == want["pred_cd"][i]
     assert p["cd"] == max(len(g) for g in want["groups"])
+    assert p["n_dispatches"] == want["n_dispatches"]
+    for i in live:
+        assert p["dispatch_of"][i] == want["dispatch_of"][i], i
+        assert p["stream_of"][i] == want["stream_of"][i], i
 
 
 def _random_set(rng, n):
