@@ -50,6 +50,7 @@ struct Variant {
 struct TableEntry {
   int dtype, ta, tb, mlog;
   int64_t n, k;
+  double ln, lk;  // log2(n), log2(k)
   int v[GDY_N_CD];
 };
 
@@ -57,6 +58,7 @@ struct Table {
   bool loaded = false;
   bool has_lr = false;
   std::vector<TableEntry> entries;
+  std::vector<int> by_layout[4][2][2];  // entry indices per (dtype, ta, tb), file order
   double xmin[GDY_N_FEATURES], xmax[GDY_N_FEATURES];
   double w[GDY_N_FEATURES][GDY_N_CD];
   double b[GDY_N_CD];
@@ -199,35 +201,35 @@ int heuristic_variant(const gdy_ctx* ctx, const gdy_gemm& g) {
 
 // GO table lookup: nearest tuned shape bucket (same dtype and layout) in
 // log2 space, then the variant stored for CD class ci.
-int table_variant(const gdy_ctx* ctx, const gdy_gemm& g, int ci) {
+int nearest_entry(const gdy_ctx* ctx, const gdy_gemm& g) {
   const Table& t = ctx->table;
+  if (!t.loaded || g.a_type < 1 || g.a_type > 3) return -1;
   const int mlog = ceil_log2(std::max<int64_t>(g.m, 1));
   const double ln = std::log2((double)std::max<int64_t>(g.n, 1));
   const double lk = std::log2((double)std::max<int64_t>(g.k, 1));
   int best = -1;
   double best_d = 0;
-  for (size_t i = 0; i < t.entries.size(); ++i) {
+  for (int i : t.by_layout[g.a_type][g.trans_a & 1][g.trans_b & 1]) {
     const TableEntry& e = t.entries[i];
-    if (e.dtype != g.a_type || e.ta != g.trans_a || e.tb != g.trans_b) continue;
-    const double d = std::fabs((double)(e.mlog - mlog)) + std::fabs(std::log2((double)e.n) - ln) +
-                     std::fabs(std::log2((double)e.k) - lk);
+    const double d = std::fabs((double)(e.mlog - mlog)) + std::fabs(e.ln - ln) + std::fabs(e.lk - lk);
     if (best < 0 || d < best_d) {
-      best = (int)i;
+      best = i;
       best_d = d;
     }
   }
-  if (best < 0) return -1;
-  return t.entries[best].v[ci];
+  return best;
 }
 
-// Variant bound to GEMM g for CD class ci (0 = isolated).
-int bind_variant(const gdy_ctx* ctx, const gdy_gemm& g, int ci, bool* fallback) {
-  if (ctx->table.loaded) {
-    const int v = table_variant(ctx, g, ci);
-    if (v >= 0) return runnable(ctx, v, g);
-  }
+// Variant for CD class ci given the GEMM's nearest tuned entry (-1: none,
+// then the isolated heuristics).
+int bind_entry(const gdy_ctx* ctx, const gdy_gemm& g, int entry, int ci, bool* fallback) {
+  if (entry >= 0) return runnable(ctx, ctx->table.entries[entry].v[ci], g);
   if (fallback) *fallback = true;
   return heuristic_variant(ctx, g);
+}
+
+int bind_variant(const gdy_ctx* ctx, const gdy_gemm& g, int ci, bool* fallback) {
+  return bind_entry(ctx, g, nearest_entry(ctx, g), ci, fallback);
 }
 
 // CD class whose tuned kernel serves a group of s GEMMs: nearest class in
@@ -245,12 +247,12 @@ int class_for_size(int s) {
 
 // Sec. 4.3 features: M, N, K and, per CD class, (#WGs, occupancy, #waves)
 // of the kernel bound for that class; #waves = #WGs / (CUs * occupancy).
-void features(const gdy_ctx* ctx, const gdy_gemm& g, double* x) {
+void features(const gdy_ctx* ctx, const gdy_gemm& g, int entry, double* x) {
   x[0] = (double)g.m;
   x[1] = (double)g.n;
   x[2] = (double)g.k;
   for (int ci = 0; ci < GDY_N_CD; ++ci) {
-    const int vid = bind_variant(ctx, g, ci, nullptr);
+    const int vid = bind_entry(ctx, g, entry, ci, nullptr);
     double wgs = 0, occ = 0, waves = 0;
     if (vid >= 0) {
       const Geometry geo = geometry(ctx, vid, g);
@@ -511,12 +513,14 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
   // size and dispatched with the group's other GEMMs of the same kernel.
   // Without a trained predictor every GEMM keeps CD 1.
   std::vector<int> pred(n, 0);
+  std::vector<int> entry(n, -1);  // nearest tuned shape, looked up once per GEMM
   for (int t = 0; t < L; ++t) {
     const int i = live[t];
+    entry[i] = nearest_entry(ctx, g[i]);
     int cd = 1;
     if (ctx->table.loaded && ctx->table.has_lr) {
       double x[GDY_N_FEATURES];
-      features(ctx, g[i], x);
+      features(ctx, g[i], entry[i], x);
       cd = predict_cd(ctx, x);
     } else {
       fb = true;
@@ -555,7 +559,7 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
       const int i = grp[u];
       p->order[t++] = i;
       p->group_of[i] = q;
-      p->variant_of[i] = bind_variant(ctx, g[i], class_for_size(s), &fb);
+      p->variant_of[i] = bind_entry(ctx, g[i], entry[i], class_for_size(s), &fb);
     }
     form_dispatches(ctx, grp, S, p);
   }
@@ -786,6 +790,11 @@ gdy_status load_table(gdy_ctx* ctx, const char* path) {
           return fail(ctx, GDY_ERR_TABLE, "variant %s does not match its entry", name.c_str());
         e.v[c] = vid;
       }
+      e.ln = std::log2((double)e.n);
+      e.lk = std::log2((double)e.k);
+      if (e.dtype < 1 || e.dtype > 3 || (e.ta & ~1) || (e.tb & ~1))
+        return fail(ctx, GDY_ERR_TABLE, "bad entry line: %s", line.c_str());
+      t.by_layout[e.dtype][e.ta][e.tb].push_back((int)t.entries.size());
       t.entries.push_back(e);
     } else {
       return fail(ctx, GDY_ERR_TABLE, "unknown GO table line: %s", line.c_str());
@@ -1074,7 +1083,7 @@ gdy_status gdy_features(gdy_ctx* ctx, const gdy_gemm* gemm, double* out_features
   if (!ctx || !gemm || !out_features) return GDY_ERR_INVALID_ARG;
   gdy_status s = validate(ctx, gemm, 1, GDY_SELECTOR);
   if (s != GDY_OK) return s;
-  features(ctx, *gemm, out_features);
+  features(ctx, *gemm, nearest_entry(ctx, *gemm), out_features);
   return GDY_OK;
 }
 
