@@ -133,7 +133,17 @@ def dominant_kernel(ctx, mats, plan, steps):
     idx = members[d]
     v = ctx.variant(plan["variant_of"][idx[0]])
     specs = [mats[i].spec for i in idx]
-    return {"variant": v["name"], "shape": [[s.m, s.n, s.k] for s in specs],
+    # workgroups of the dispatch (to find it in a profiler trace): each GEMM
+    # its tiles or cap x occupancy, all but the last rounded up to 8
+    grid = 0
+    for u, i in enumerate(idx):
+        w = ctx.variant(plan["variant_of"][i])
+        s = mats[i].spec
+        wg = -(-s.m // w["bm"]) * -(-s.n // w["bn"])
+        if w["grid_cap_cus"]:
+            wg = min(wg, w["grid_cap_cus"] * max(w["occupancy"], 1))
+        grid += -(-wg // 8) * 8 if u + 1 < len(idx) else wg
+    return {"variant": v["name"], "shape": [[s.m, s.n, s.k] for s in specs], "grid": grid,
             "launches": len(per[d]), "mean_ms": float(np.mean(per[d])),
             "flops": sum(2 * s.m * s.n * s.k for s in specs),
             "bytes": sum(s.compulsory_bytes() for s in specs), "dtype": specs[0].dtype}
@@ -278,7 +288,8 @@ def main():
     roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
             "frac": round(ach / peak, 4),
             "traffic": recorded_traffic(args.workload, dom["variant"], dom["shape"]),
-            "kernel": dom["variant"], "gemms": dom["shape"], "launches": dom["launches"],
+            "kernel": dom["variant"], "gemms": dom["shape"], "workgroups": dom["grid"],
+            "launches": dom["launches"],
             "mean_ms": round(dom["mean_ms"], 4)}
     ai = dom["flops"] / dom["bytes"]
     if ai < peak * 1e12 / (PEAK_HBM_GBS * 1e9):
