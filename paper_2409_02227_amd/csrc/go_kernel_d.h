@@ -34,6 +34,8 @@
 #pragma once
 #include "go_kernel.h"
 
+#include <type_traits>
+
 namespace gdy {
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -242,6 +244,15 @@ struct DCfg {
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must hold whole 32x32 blocks");
   static_assert(LDS <= 160 * 1024, "LDS budget");
   static_assert(STAGES >= 2 && STAGES <= 4, "stages");
+  // Register estimate for the pipelined loop (accumulators plus two
+  // fragment buffers, 56 registers for addresses and the rest) against the
+  // per-wave budget at this kernel's waves per SIMD; kernels over it, and
+  // tiles of a single K step (both buffers then straddle the tile boundary),
+  // keep the simple loop, whose fragment buffers the compiler may share.
+  static constexpr int FRAG_REGS = ES == 2 ? 4 : 8;
+  static constexpr int WAVES_PER_SIMD = (NW / 4 > 1 ? NW / 4 : 1) * (LDS <= 80 * 1024 ? 2 : 1);
+  static constexpr bool PIPE = NKSTEP >= 2 &&
+      FM * FN * 16 + 2 * (FM + FN) * FRAG_REGS <= 512 / WAVES_PER_SIMD - 56;
 };
 
 template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int STAGES, int KB>
@@ -326,63 +337,173 @@ go_gemm_d(KLaunch L) {
 #pragma unroll
         for (int r = 0; r < M::NACC; ++r) acc[j][i][r] = 0.f;
 
-    wait_vmcnt<0>();  // previous tile's stores and copies are done
-#pragma unroll
-    for (int s = 0; s < STAGES - 1; ++s)
-      if (s < nk) issue_tile(s, 0, 1);
-
-    for (int kt = 0; kt < nk; ++kt) {
-      // tile kt has landed once at most (tiles issued after it) copies remain
-      if constexpr (STAGES == 2) {
-        wait_vmcnt<0>();
-      } else {
-        const int ahead = min(STAGES - 2, nk - 1 - kt);
-        if (ahead >= 2) wait_vmcnt<2 * PER_TILE>();
-        else if (ahead == 1) wait_vmcnt<PER_TILE>();
-        else wait_vmcnt<0>();
-      }
-      barrier_nowait();
-      const bool prefetch = kt + STAGES - 1 < nk;
-
-      const lds_u8* As = smem + (kt % STAGES) * C::STAGE_BYTES;
+    // per-step fragment loads (buffer `buf` of af/bf) from the stage at As
+    Frag af[2][C::FM], bf[2][C::FN];
+    auto load_step = [&](const lds_u8* As, int ks, int buf) {
       const lds_u8* Bs = As + C::A_BYTES;
-      // fragments of K step ks+1 are read while the MFMAs of step ks run;
-      // the scheduling fences keep the compiler from hoisting further reads
-      // (which would need registers for every step of the tile at once)
-      Frag af[2][C::FM], bf[2][C::FN];
-      auto load_step = [&](int ks, int buf) {
 #pragma unroll
-        for (int i = 0; i < C::FM; ++i) {
-          if constexpr (TA == 0)
-            af[buf][i] = frag_k<C::ES>(As + (wm * C::WTM + i * 32) * KB, ak0, ak1, ks);
-          else
-            af[buf][i] = frag_t<C::ES, AT>(As, aoff[i], ks);
-        }
+      for (int i = 0; i < C::FM; ++i) {
+        if constexpr (TA == 0)
+          af[buf][i] = frag_k<C::ES>(As + (wm * C::WTM + i * 32) * KB, ak0, ak1, ks);
+        else
+          af[buf][i] = frag_t<C::ES, AT>(As, aoff[i], ks);
+      }
 #pragma unroll
-        for (int j = 0; j < C::FN; ++j) {
-          if constexpr (TB == 1)
-            bf[buf][j] = frag_k<C::ES>(Bs + (wn * C::WTN + j * 32) * KB, bk0, bk1, ks);
-          else
-            bf[buf][j] = frag_t<C::ES, BT>(Bs, boff[j], ks);
+      for (int j = 0; j < C::FN; ++j) {
+        if constexpr (TB == 1)
+          bf[buf][j] = frag_k<C::ES>(Bs + (wn * C::WTN + j * 32) * KB, bk0, bk1, ks);
+        else
+          bf[buf][j] = frag_t<C::ES, BT>(Bs, boff[j], ks);
+      }
+    };
+    constexpr int NMMA = C::FM * C::FN;
+    auto mma_range = [&](int buf, int q0, int q1) {
+#pragma unroll
+      for (int q = 0; q < NMMA; ++q) {
+        if (q < q0 || q >= q1) continue;
+        const int j = q / C::FM, i = q % C::FM;
+        acc[j][i] = M::run(bf[buf][j], af[buf][i], acc[j][i]);
+      }
+    };
+
+    if constexpr (C::PIPE) {
+      // Ring of STAGES K tiles, every stage filled up front.  The wait and
+      // barrier for tile kt+1 sit inside the last K step of tile kt, after
+      // half of its MFMAs: tile kt+1's first fragments are read while the
+      // other half runs, and the stage of tile kt is refilled with tile
+      // kt+STAGES right after the barrier.  Within a K step the next step's
+      // fragment reads are interleaved with the first half of the MFMAs.
+      constexpr int RD_A = TA == 0 ? (C::ES == 2 ? 1 : 2) : (C::ES == 2 ? 2 : 4);
+      constexpr int RD_B = TB == 1 ? (C::ES == 2 ? 1 : 2) : (C::ES == 2 ? 2 : 4);
+      constexpr int NREAD = C::FM * RD_A + C::FN * RD_B;  // LDS reads per K step
+      auto interleave = [&]() {
+        constexpr int H = NMMA / 2 > 0 ? NMMA / 2 : 1;
+#pragma unroll
+        for (int q = 0; q < NMMA; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+          const int r0 = q < H ? q * NREAD / H : NREAD, r1 = q < H ? (q + 1) * NREAD / H : NREAD;
+#pragma unroll
+          for (int r = r0; r < r1; ++r) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one DS read
         }
       };
-      load_step(0, 0);
+      auto interleave_half = [&]() {
+        constexpr int H = NMMA - NMMA / 2;
 #pragma unroll
-      for (int ks = 0; ks < C::NKSTEP; ++ks) {
-        if (ks + 1 < C::NKSTEP) load_step(ks + 1, (ks + 1) & 1);
-        // with two stages the copies must land by the next iteration: issue
-        // them all at once; deeper rings spread them over the K steps
-        if constexpr (STAGES == 2) {
-          if (prefetch && ks == 0) issue_tile(kt + 1, 0, 1);
-        } else {
-          if (prefetch) issue_tile(kt + STAGES - 1, ks, C::NKSTEP);
+        for (int q = 0; q < H; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          const int r0 = q * NREAD / H, r1 = (q + 1) * NREAD / H;
+#pragma unroll
+          for (int r = r0; r < r1; ++r) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
+      };
+      // wait until a tile has landed, `after` tiles having been issued after it
+      auto wait_tile = [&](int after) {
+        if constexpr (STAGES >= 4) {
+          if (after >= 3) { wait_vmcnt<3 * PER_TILE>(); return; }
+        }
+        if constexpr (STAGES >= 3) {
+          if (after >= 2) { wait_vmcnt<2 * PER_TILE>(); return; }
+        }
+        if (after >= 1) wait_vmcnt<PER_TILE>();
+        else wait_vmcnt<0>();
+      };
+
+      wait_vmcnt<0>();  // previous tile's stores and copies are done
 #pragma unroll
-        for (int j = 0; j < C::FN; ++j)
+      for (int s = 0; s < STAGES; ++s)
+        if (s < nk) issue_tile(s, 0, 1);
+      if (nk > 0) {
+        wait_tile(min(STAGES - 1, nk - 1));
+        barrier_nowait();
+        load_step(smem, 0, 0);
+      }
+      // one K tile; P: parity of its first step's fragment buffer; LAST: no
+      // tile follows (both compile-time, so the body has no branch and the
+      // compiler counts outstanding reads exactly)
+      auto tile_body = [&](int kt, auto P, auto LAST) {
+        const lds_u8* As = smem + (kt % STAGES) * C::STAGE_BYTES;
 #pragma unroll
-          for (int i = 0; i < C::FM; ++i)
-            acc[j][i] = M::run(bf[ks & 1][j], af[ks & 1][i], acc[j][i]);
-        __builtin_amdgcn_sched_barrier(0);
+        for (int ks = 0; ks < C::NKSTEP; ++ks) {
+          const int cur = (decltype(P)::value + ks) & 1, nxt = cur ^ 1;
+          if (ks + 1 < C::NKSTEP) {
+            load_step(As, ks + 1, nxt);
+            mma_range(cur, 0, NMMA);
+            interleave();
+          } else if constexpr (!decltype(LAST)::value) {
+            mma_range(cur, 0, NMMA / 2);
+            __builtin_amdgcn_sched_barrier(0);
+            wait_tile(min(STAGES - 2, nk - 2 - kt));
+            __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of the stage are done
+            barrier_nowait();
+            if (kt + STAGES < nk) issue_tile(kt + STAGES, 0, 1);
+            load_step(smem + ((kt + 1) % STAGES) * C::STAGE_BYTES, 0, nxt);
+            mma_range(cur, NMMA / 2, NMMA);
+            interleave_half();
+          } else {
+            mma_range(cur, 0, NMMA);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      };
+      using P0 = std::integral_constant<int, 0>;
+      using P1 = std::integral_constant<int, C::NKSTEP & 1>;
+      // tiles 0 .. nk-2 (in pairs when a tile has an odd number of K steps,
+      // so buffer parity stays compile-time), then the last one
+      int kt = 0;
+      if constexpr (C::NKSTEP & 1) {
+        for (; kt + 2 <= nk - 1; kt += 2) {
+          tile_body(kt, P0{}, std::false_type{});
+          tile_body(kt + 1, P1{}, std::false_type{});
+        }
+        if (kt < nk - 1) {
+          tile_body(kt, P0{}, std::false_type{});
+          ++kt;
+        }
+        if (kt < nk) {
+          if (kt & 1) tile_body(kt, P1{}, std::true_type{});
+          else tile_body(kt, P0{}, std::true_type{});
+        }
+      } else {
+        for (; kt < nk - 1; ++kt) tile_body(kt, P0{}, std::false_type{});
+        if (kt < nk) tile_body(kt, P0{}, std::true_type{});
+      }
+    } else {
+      wait_vmcnt<0>();  // previous tile's stores and copies are done
+  #pragma unroll
+      for (int s = 0; s < STAGES - 1; ++s)
+        if (s < nk) issue_tile(s, 0, 1);
+
+      for (int kt = 0; kt < nk; ++kt) {
+        // tile kt has landed once at most (tiles issued after it) copies remain
+        if constexpr (STAGES == 2) {
+          wait_vmcnt<0>();
+        } else {
+          const int ahead = min(STAGES - 2, nk - 1 - kt);
+          if (ahead >= 2) wait_vmcnt<2 * PER_TILE>();
+          else if (ahead == 1) wait_vmcnt<PER_TILE>();
+          else wait_vmcnt<0>();
+        }
+        barrier_nowait();
+        const bool prefetch = kt + STAGES - 1 < nk;
+
+        const lds_u8* As = smem + (kt % STAGES) * C::STAGE_BYTES;
+        // fragments of K step ks+1 are read while the MFMAs of step ks run;
+        // the scheduling fences keep the compiler from hoisting further reads
+        // (which would need registers for every step of the tile at once)
+        load_step(As, 0, 0);
+  #pragma unroll
+        for (int ks = 0; ks < C::NKSTEP; ++ks) {
+          if (ks + 1 < C::NKSTEP) load_step(As, ks + 1, (ks + 1) & 1);
+          // with two stages the copies must land by the next iteration: issue
+          // them all at once; deeper rings spread them over the K steps
+          if constexpr (STAGES == 2) {
+            if (prefetch && ks == 0) issue_tile(kt + 1, 0, 1);
+          } else {
+            if (prefetch) issue_tile(kt + STAGES - 1, ks, C::NKSTEP);
+          }
+          mma_range(ks & 1, 0, NMMA);
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
     }
     __syncthreads();  // every wave is done with the ring before the next tile refills it

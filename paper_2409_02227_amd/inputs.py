@@ -218,6 +218,22 @@ def _device_tensor(codes: np.ndarray, dtype: str, rows: int, ld: int, cols: int,
     return full[:, :cols]
 
 
+def from_codes(spec: GemmSpec, a_codes: np.ndarray, b_codes: np.ndarray, scale_a: float = 1.0,
+               scale_b: float = 1.0, device="cuda") -> Materialized:
+    """Device operands from given flat codes in the stored layouts of `spec`
+    (for inputs with a chosen structure, e.g. all-subnormal operands)."""
+    import torch
+    ar, ac = spec.stored_shape("a")
+    br, bc = spec.stored_shape("b")
+    assert a_codes.size == ar * spec.ld("a") and b_codes.size == br * spec.ld("b")
+    a = _device_tensor(a_codes, spec.dtype, ar, spec.ld("a"), ac, device)
+    b = _device_tensor(b_codes, spec.dtype, br, spec.ld("b"), bc, device)
+    odt = getattr(torch, _TORCH_CODE[OUT[spec.dtype]])
+    cfull = torch.full((spec.m, spec.ld("c")), float("nan"), dtype=odt, device=device)
+    return Materialized(spec, a, b, cfull[:, :spec.n], cfull, scale_a, scale_b,
+                        {"a": a_codes, "b": b_codes})
+
+
 def materialize(spec: GemmSpec, device="cuda", keep_host=True) -> Materialized:
     import torch
     ar, ac = spec.stored_shape("a")

@@ -338,3 +338,54 @@ def test_fused_dispatch_chunks_and_kernel_split(ctx):
     assert plan["dispatch_of"] == [0, 1, 0, 1, 2, 3, 2, 3]
     for m, ref in zip(sub, iso):
         assert np.array_equal(out_codes(m), ref), f"{m.spec.name}: split dispatch differs"
+
+
+@pytest.mark.parametrize("dt", ["fp8", "f16"])
+def test_subnormal_inputs(ctx, dt):
+    """A holds only positive subnormal codes, B positive normal codes: every
+    product comes from a subnormal input and ref equals the bound, so a
+    kernel that flushed subnormal inputs to zero would fail the bound.  Every
+    uncapped kernel of the dtype and layout (staged and direct)."""
+    m, n, k = 96, 160, 256
+    rng = np.random.default_rng(11)
+    if dt == "fp8":
+        a_codes = rng.integers(0x01, 0x08, size=m * k).astype(np.uint8)   # (j/8) 2^-6
+        b_codes = rng.integers(0x30, 0x48, size=k * n).astype(np.uint8)   # 0.5 .. 3.75
+    else:
+        a_codes = rng.integers(0x0001, 0x0400, size=m * k).astype(np.uint16)  # < 2^-14
+        b_codes = rng.integers(0x3800, 0x4400, size=k * n).astype(np.uint16)  # 0.5 .. 4
+    spec = GemmSpec(m, n, k, dt, 0, 0, seed=0, name=f"subnormal_{dt}")
+    mat = inputs.from_codes(spec, a_codes, b_codes)
+    ran = 0
+    for vid, v in _kernels(ctx):
+        if DT_NAME[v["dtype"]] != dt or v["trans_a"] or v["trans_b"]:
+            continue
+        plan = _run(ctx, [mat], "forced", 1, [vid])
+        assert plan["variant_of"][0] == vid, f"{v['name']}: a different kernel ran"
+        check(mat, label=f"subnormal {v['name']}")
+        ran += 1
+    assert ran > 0
+
+
+def test_direct_kernels_k_depths(ctx):
+    """Each direct kernel at K-tile counts 1, 2, S-1, S, S+1 and 2S+1 for its
+    ring of S stages (prologue, ring wrap and last-tile paths of the main
+    loop), ragged M and N, 16-byte aligned rows."""
+    for vid, v in _kernels(ctx):
+        if not v["direct"]:
+            continue
+        dt = DT_NAME[v["dtype"]]
+        es = 1 if dt == "fp8" else 2
+        stages = int(v["name"].split("_d")[-1].split("_")[0].rstrip("h"))
+        m, n = v["bm"] + 5, v["bn"] + 3
+        for nk in sorted({1, 2, max(stages - 1, 1), stages, stages + 1, 2 * stages + 1}):
+            k = nk * v["bk"]
+            ta, tb = v["trans_a"], v["trans_b"]
+            a_cols = m if ta else k
+            b_cols = k if tb else n
+            spec = GemmSpec(m, n, k, dt, ta, tb, seed=5000 + 7 * vid + nk, name=f"{v['name']}_nk{nk}",
+                            pad_a=_pad_to(a_cols, 16 // es), pad_b=_pad_to(b_cols, 16 // es))
+            mat = inputs.materialize(spec)
+            plan = _run(ctx, [mat], "forced", 1, [vid])
+            assert plan["variant_of"][0] == vid, f"{v['name']}: direct path not taken"
+            check(mat, label=f"{v['name']} nk={nk}")
