@@ -118,7 +118,7 @@ def dominant_kernel(ctx, mats, plan, steps):
     per-dispatch HIP events (recorded on the stream the dispatch runs on)."""
     n = len(mats)
     members = {}
-    for i in range(n):
+    for i in plan["order"]:  # launch order: a dispatch lays its GEMMs out in this order
         d = plan["dispatch_of"][i]
         if d >= 0:
             members.setdefault(d, []).append(i)
