@@ -221,7 +221,7 @@ def het_bench(args, desc):
             gemms.append(gdy.Gemm(a, b, c))
         arrs.append((gdy.descs(gemms), len(gemms), gemms))
         flops.append(sum(g.flops for g, _, _ in sub))
-    steps = max(1, args.steps // 4)
+    steps = args.steps
     t_sel, t_seq = [], []
     for arr, n, _ in arrs:
         t_seq.append(time_steps(ctx, arr, n, "sequential", steps, 2, handle, torch))

@@ -338,6 +338,16 @@ def test_fused_dispatch_chunks_and_kernel_split(ctx):
     assert plan["dispatch_of"] == [0, 1, 0, 1, 2, 3, 2, 3]
     for m, ref in zip(sub, iso):
         assert np.array_equal(out_codes(m), ref), f"{m.spec.name}: split dispatch differs"
+    # two GEMMs on two kernels: the second dispatch forks to a pool stream
+    big = [inputs.materialize(GemmSpec(4096, 4096, 1024, "bf16", seed=900 + i, name=f"big{i}"))
+           for i in range(2)]
+    vids = [vid, other]
+    iso = _isolated_codes(ctx, big, vids)
+    plan = _run(ctx, big, "forced_grouped", 0, vids)
+    assert plan["dispatch_of"] == [0, 1] and plan["stream_of"] == [-1, 0]
+    for m, ref in zip(big, iso):
+        assert np.array_equal(out_codes(m), ref), f"{m.spec.name}: forked dispatch differs"
+        check(m, samples=4, label="forked")
 
 
 @pytest.mark.parametrize("dt", ["fp8", "f16"])

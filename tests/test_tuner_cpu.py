@@ -11,7 +11,9 @@ from paper_2409_02227_amd import gdy, tuner
 def test_label_rule():
     assert tuner.label_of({2: 1.30, 4: 1.50, 8: 1.40, 16: 1.10}) == 4
     assert tuner.label_of({2: 1.04, 4: 1.01, 8: 0.90, 16: 0.80}) == 1     # no CD gains 5%
-    assert tuner.label_of({2: 1.20, 4: 1.20, 8: 1.0, 16: 1.0}) == 2       # ties: smaller CD
+    assert tuner.label_of({2: 1.20, 4: 1.20, 8: 1.0, 16: 1.0}) == 4       # ties: larger CD
+    assert tuner.label_of({2: 1.06, 4: 1.03, 8: 1.01, 16: 1.0}) == 4      # within 3% of the best
+    assert tuner.label_of({2: 1.50, 4: 1.44, 8: 1.46, 16: 1.40}) == 8
     assert tuner.label_of({2: 1.05, 4: 1.0, 8: 1.0, 16: 1.0}) == 2
 
 
