@@ -27,8 +27,10 @@
  * (C is overwritten) and round-to-nearest-even into the output type.
  *
  * Supported (a_type, b_type, c_type): (F16, F16, F16), (BF16, BF16, BF16),
- * (FP8_E4M3, FP8_E4M3, BF16).  FP8_E4M3 is the OCP "E4M3FN" encoding
- * (bias 7, largest finite 448, no infinities).
+ * (FP8_E4M3, FP8_E4M3, BF16), (F32, F32, F32).  FP8_E4M3 is the OCP "E4M3FN"
+ * encoding (bias 7, largest finite 448, no infinities).  F32 runs on the
+ * fp32 MFMAs (the full-precision GEMMs of Sec. 5.2 and 6.8) and stores C
+ * unrounded.
  *
  * Ownership: all matrices are device buffers owned by the caller, who keeps
  * them alive until the origin stream passes the work.  The library owns its
@@ -69,7 +71,7 @@ typedef enum {
   GDY_ERR_NOMEM = 7        /* host allocation failed                                 */
 } gdy_status;
 
-typedef enum { GDY_F16 = 1, GDY_BF16 = 2, GDY_FP8_E4M3 = 3 } gdy_dtype;
+typedef enum { GDY_F16 = 1, GDY_BF16 = 2, GDY_FP8_E4M3 = 3, GDY_F32 = 4 } gdy_dtype;
 
 /* Execution configurations (Sec. 5.5). */
 typedef enum {
@@ -106,7 +108,7 @@ typedef struct {
   const void* a; int64_t lda;       /* device pointers; leading dimensions in elements      */
   const void* b; int64_t ldb;
   void* c;       int64_t ldc;       /* ldc >= n                                             */
-  float scale_a, scale_b;           /* fp8 per-tensor scales; must be 1.0f for 16-bit types */
+  float scale_a, scale_b;           /* fp8 per-tensor scales; must be 1.0f for other types  */
   int32_t tenant;                   /* caller's tag, reported back in per-kernel timings    */
   int32_t variant;                  /* GDY_FORCED: variant id to use; otherwise ignored     */
 } gdy_gemm;

@@ -90,7 +90,7 @@ def n_waves(wgs: int, cus: int, occupancy: int) -> float:
 
 
 def elem_bytes(dtype: int) -> int:
-    return 1 if dtype == 3 else 2
+    return {1: 2, 2: 2, 3: 1, 4: 4}[dtype]
 
 
 def direct_ok(v: dict, g: dict) -> bool:

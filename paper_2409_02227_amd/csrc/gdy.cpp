@@ -58,13 +58,15 @@ struct Table {
   bool loaded = false;
   bool has_lr = false;
   std::vector<TableEntry> entries;
-  std::vector<int> by_layout[4][2][2];  // entry indices per (dtype, ta, tb), file order
+  std::vector<int> by_layout[5][2][2];  // entry indices per (dtype, ta, tb), file order
   double xmin[GDY_N_FEATURES], xmax[GDY_N_FEATURES];
   double w[GDY_N_FEATURES][GDY_N_CD];
   double b[GDY_N_CD];
 };
 
-int elem_size(int dt) { return dt == DT_FP8 ? 1 : 2; }
+int elem_size(int dt) { return dt == DT_FP8 ? 1 : dt == DT_F32 ? 4 : 2; }
+// bytes of one element of C: fp32 for fp32 inputs, else a 16-bit type
+int out_size(const gdy_gemm& g) { return g.c_type == GDY_F32 ? 4 : 2; }
 
 int ceil_log2(int64_t x) {
   int l = 0;
@@ -163,7 +165,7 @@ bool variant_fits(const gdy_ctx* ctx, int vid, const gdy_gemm& g) {
 bool direct_ok(const gdy_ctx* ctx, int vid, const gdy_gemm& g) {
   const KernelDesc* d = ctx->kernels[ctx->variants[vid].kernel].d;
   if (!d->direct) return true;
-  const int es = g.a_type == GDY_FP8_E4M3 ? 1 : 2;
+  const int es = elem_size(g.a_type);
   return g.k % d->bk == 0 && (uintptr_t)g.a % 16 == 0 && (uintptr_t)g.b % 16 == 0 &&
          (g.lda * es) % 16 == 0 && (g.ldb * es) % 16 == 0;
 }
@@ -203,7 +205,7 @@ int heuristic_variant(const gdy_ctx* ctx, const gdy_gemm& g) {
 // log2 space, then the variant stored for CD class ci.
 int nearest_entry(const gdy_ctx* ctx, const gdy_gemm& g) {
   const Table& t = ctx->table;
-  if (!t.loaded || g.a_type < 1 || g.a_type > 3) return -1;
+  if (!t.loaded || g.a_type < 1 || g.a_type > 4) return -1;
   const int mlog = ceil_log2(std::max<int64_t>(g.m, 1));
   const double ln = std::log2((double)std::max<int64_t>(g.n, 1));
   const double lk = std::log2((double)std::max<int64_t>(g.k, 1));
@@ -315,22 +317,25 @@ gdy_status validate_one(gdy_ctx* ctx, const gdy_gemm& g, int i, Extent* ea, Exte
   const bool t16 = (g.a_type == GDY_F16 && g.b_type == GDY_F16 && g.c_type == GDY_F16) ||
                    (g.a_type == GDY_BF16 && g.b_type == GDY_BF16 && g.c_type == GDY_BF16);
   const bool t8 = g.a_type == GDY_FP8_E4M3 && g.b_type == GDY_FP8_E4M3 && g.c_type == GDY_BF16;
-  if (!t16 && !t8)
+  const bool t32 = g.a_type == GDY_F32 && g.b_type == GDY_F32 && g.c_type == GDY_F32;
+  if (!t16 && !t8 && !t32)
     return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: unsupported dtype triple (%d,%d,%d)", i,
                 g.a_type, g.b_type, g.c_type);
   if ((g.trans_a != 0 && g.trans_a != 1) || (g.trans_b != 0 && g.trans_b != 1))
     return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: trans flags must be 0 or 1", i);
   if (!std::isfinite(g.scale_a) || !std::isfinite(g.scale_b))
     return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: non-finite scale", i);
-  if (t16 && (g.scale_a != 1.0f || g.scale_b != 1.0f))
-    return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: scales must be 1 for 16-bit inputs", i);
+  if ((t16 || t32) && (g.scale_a != 1.0f || g.scale_b != 1.0f))
+    return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: scales must be 1 for 16- and 32-bit inputs", i);
   if (g.m == 0 || g.n == 0) return GDY_OK;  // no-op
   const int es = elem_size(g.a_type);
   if (!g.c) return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: null C", i);
   if (g.ldc < g.n) return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: ldc < n", i);
-  if ((uintptr_t)g.c % 2) return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: C not 2-byte aligned", i);
+  const int os = out_size(g);
+  if ((uintptr_t)g.c % os)
+    return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: C not %d-byte aligned", i, os);
   int64_t cb;
-  if (!stored_extent(g.m, g.n, g.ldc, 2, &cb))
+  if (!stored_extent(g.m, g.n, g.ldc, os, &cb))
     return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: C extent too large", i);
   ec->lo = (uintptr_t)g.c;
   ec->hi = ec->lo + (uintptr_t)cb;
@@ -338,7 +343,7 @@ gdy_status validate_one(gdy_ctx* ctx, const gdy_gemm& g, int i, Extent* ea, Exte
   if (!g.a || !g.b) return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: null A or B", i);
   if (g.lda < (g.trans_a ? g.m : g.k)) return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: lda too small", i);
   if (g.ldb < (g.trans_b ? g.k : g.n)) return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: ldb too small", i);
-  if (es == 2 && (((uintptr_t)g.a | (uintptr_t)g.b) % 2))
+  if (es > 1 && (((uintptr_t)g.a | (uintptr_t)g.b) % es))
     return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: A or B not element aligned", i);
   int64_t ab, bb;
   const bool oka = g.trans_a ? stored_extent(g.k, g.m, g.lda, es, &ab) : stored_extent(g.m, g.k, g.lda, es, &ab);
@@ -571,7 +576,7 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
 // ---------------------------------------------------------------------------
 bool vec_ok(const void* ptr, int64_t ld, int es, bool kcontiguous) {
   const uintptr_t a = (uintptr_t)ptr;
-  if (kcontiguous || es == 2) return a % 16 == 0 && (ld * es) % 16 == 0;
+  if (kcontiguous || es >= 2) return a % 16 == 0 && (ld * es) % 16 == 0;
   return a % 8 == 0 && (ld * es) % 8 == 0;  // fp8 k-major operand: 8-byte row vectors
 }
 
@@ -606,7 +611,7 @@ KArgs make_args(const gdy_ctx* ctx, int vid, const gdy_gemm& g, Geometry* geo_ou
     if (g.trans_a) stored_extent(g.k, g.m, g.lda, es, &ab); else stored_extent(g.m, g.k, g.lda, es, &ab);
     if (g.trans_b) stored_extent(g.n, g.k, g.ldb, es, &bb); else stored_extent(g.k, g.n, g.ldb, es, &bb);
   }
-  stored_extent(g.m, g.n, g.ldc, 2, &cb);
+  stored_extent(g.m, g.n, g.ldc, out_size(g), &cb);
   a.a_bytes = read_records(g.a, ab);
   a.b_bytes = read_records(g.b, bb);
   a.c_bytes = (int32_t)cb;  // stores are element-wise: exact extent
@@ -614,7 +619,7 @@ KArgs make_args(const gdy_ctx* ctx, int vid, const gdy_gemm& g, Geometry* geo_ou
   a.tiles_n = geo.tiles_n;
   a.a_vec = g.k > 0 && vec_ok(g.a, g.lda, es, g.trans_a == 0);
   a.b_vec = g.k > 0 && vec_ok(g.b, g.ldb, es, g.trans_b == 1);
-  a.c_vec = (uintptr_t)g.c % 8 == 0 && (g.ldc * 2) % 8 == 0;
+  a.c_vec = (uintptr_t)g.c % 8 == 0 && (g.ldc * out_size(g)) % 8 == 0;
   a.group_m = 8;
   a.xcd_remap = 1;
   (void)k;
@@ -792,7 +797,7 @@ gdy_status load_table(gdy_ctx* ctx, const char* path) {
       }
       e.ln = std::log2((double)e.n);
       e.lk = std::log2((double)e.k);
-      if (e.dtype < 1 || e.dtype > 3 || (e.ta & ~1) || (e.tb & ~1))
+      if (e.dtype < 1 || e.dtype > 4 || (e.ta & ~1) || (e.tb & ~1))
         return fail(ctx, GDY_ERR_TABLE, "bad entry line: %s", line.c_str());
       t.by_layout[e.dtype][e.ta][e.tb].push_back((int)t.entries.size());
       t.entries.push_back(e);
@@ -875,16 +880,18 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
     ctx->arch = ctx->arch.substr(0, ctx->arch.find(':'));
   }
 
-  const KernelDesc* tabs[6];
-  int counts[6];
+  const int kTables = 7;
+  const KernelDesc* tabs[kTables];
+  int counts[kTables];
   counts[0] = kernels_bf16(&tabs[0]);
   counts[1] = kernels_f16(&tabs[1]);
   counts[2] = kernels_fp8(&tabs[2]);
   counts[3] = kernels_d_bf16(&tabs[3]);
   counts[4] = kernels_d_f16(&tabs[4]);
   counts[5] = kernels_d_fp8(&tabs[5]);
+  counts[6] = kernels_f32(&tabs[6]);
   uint64_t h = 1469598103934665603ull;
-  for (int t = 0; t < 6; ++t) {
+  for (int t = 0; t < kTables; ++t) {
     for (int i = 0; i < counts[t]; ++i) {
       Kernel k;
       k.d = &tabs[t][i];

@@ -6,7 +6,7 @@
 namespace gdy {
 
 // Element types, numerically equal to the public gdy_dtype values.
-enum : int { DT_F16 = 1, DT_BF16 = 2, DT_FP8 = 3 };
+enum : int { DT_F16 = 1, DT_BF16 = 2, DT_FP8 = 3, DT_F32 = 4 };
 
 // Kernel arguments, passed by value.  Sizes and leading dimensions are in
 // elements; the storage reading is row-major with op(A)(i,k) = A[i*lda+k]
@@ -61,6 +61,7 @@ struct KernelDesc {
 int kernels_bf16(const KernelDesc** out);
 int kernels_f16(const KernelDesc** out);
 int kernels_fp8(const KernelDesc** out);
+int kernels_f32(const KernelDesc** out);
 int kernels_d_bf16(const KernelDesc** out);
 int kernels_d_f16(const KernelDesc** out);
 int kernels_d_fp8(const KernelDesc** out);

@@ -49,6 +49,12 @@ template <int DT> struct ElemSize;
 template <> struct ElemSize<DT_BF16> { static constexpr int v = 2; };
 template <> struct ElemSize<DT_F16> { static constexpr int v = 2; };
 template <> struct ElemSize<DT_FP8> { static constexpr int v = 1; };
+template <> struct ElemSize<DT_F32> { static constexpr int v = 4; };
+
+// Bytes of one output element: fp32 inputs give fp32 results, the others
+// round to a 16-bit type.
+template <int DT> struct OutSize { static constexpr int v = 2; };
+template <> struct OutSize<DT_F32> { static constexpr int v = 4; };
 
 // ---------------------------------------------------------------------------
 // MFMA wrappers.  Frag is one lane's operand fragment (FB bytes of K for one
@@ -116,7 +122,30 @@ template <> struct Mma<DT_FP8, 16> {
   }
 };
 
+// fp32: 32x32x2 and 16x16x4 MFMAs, one element of K per lane.
+template <> struct Mma<DT_F32, 32> {
+  typedef float Frag;
+  typedef f32x16 Acc;
+  static constexpr int FB = 4, NACC = 16;
+  static __device__ __forceinline__ Acc run(Frag a, Frag b, Acc c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct Mma<DT_F32, 16> {
+  typedef float Frag;
+  typedef f32x4 Acc;
+  static constexpr int FB = 4, NACC = 4;
+  static __device__ __forceinline__ Acc run(Frag a, Frag b, Acc c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+};
+
 template <class Frag> struct FragLoad;
+template <> struct FragLoad<float> {
+  static __device__ __forceinline__ float run(const uint8_t* p) {
+    return *reinterpret_cast<const float*>(p);
+  }
+};
 template <> struct FragLoad<u32x4> {
   static __device__ __forceinline__ u32x4 run(const uint8_t* p) {
     return *reinterpret_cast<const u32x4*>(p);
@@ -153,8 +182,14 @@ __device__ __forceinline__ Rsrc make_rsrc(const void* base, int bytes) {
 
 template <int ES>
 __device__ __forceinline__ unsigned load_elem(Rsrc r, int off) {
+  if (ES == 4) return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
   if (ES == 2) return (unsigned)__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
   return (unsigned)__builtin_amdgcn_raw_buffer_load_b8(r, off, 0, 0);
+}
+
+// All-ones mask of one element's bits within its 32-bit word.
+template <int ES> __device__ __forceinline__ unsigned elem_field(int bit) {
+  return ES == 4 ? 0xffffffffu : ((ES == 2 ? 0xffffu : 0xffu) << (bit & 31));
 }
 
 // Operand that is K-contiguous in global memory: row r, k at byte
@@ -190,8 +225,7 @@ struct StageK {
           for (int e = 0; e < KPACK; ++e) {
             const int bit = e * ES * 8;
             const unsigned keep = (gk + e < K) ? 0xffffffffu : 0u;
-            const unsigned field = (ES == 2 ? 0xffffu : 0xffu) << (bit & 31);
-            v[bit >> 5] &= ~field | keep;
+            v[bit >> 5] &= ~elem_field<ES>(bit) | keep;
           }
         }
       }
@@ -211,8 +245,8 @@ struct StageK {
 
 // Operand stored k-major in global memory: row r, k at byte
 // k*ld_bytes + r*ES.  A block is KPACK consecutive k by 8 consecutive rows;
-// it is loaded as KPACK row-vectors of 8 elements and transposed in
-// registers into 8 K-vectors of 16 bytes.  Block b: k-block b%8, row-block
+// it is loaded as KPACK row-vectors of 8 elements (8, 16 or 32 bytes) and
+// transposed in registers into 8 K-vectors of 16 bytes.  Block b: k-block b%8, row-block
 // b/8, so the 8 lanes sharing a row-block fill one 128-byte LDS row.
 // k-rows past the K edge are never loaded (zeros); elements past the row
 // edge only feed outputs that are never stored.
@@ -239,7 +273,15 @@ struct StageT {
         if (!live || gk0 + r >= K) continue;  // k-rows past the K edge stay zero
         const int off = base + r * ld_bytes;
         if (vec) {
-          if (W == 4) {
+          if (W == 8) {
+            u32x4 v0 = __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0);
+            u32x4 v1 = __builtin_amdgcn_raw_buffer_load_b128(src, off + 16, 0, 0);
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+              in[i][r][w] = v0[w];
+              in[i][r][w + 4] = v1[w];
+            }
+          } else if (W == 4) {
             u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0);
 #pragma unroll
             for (int w = 0; w < W; ++w) in[i][r][w] = v[w];
@@ -270,7 +312,9 @@ struct StageT {
         u32x4 o;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          if (ES == 2) {
+          if (ES == 4) {
+            o[j] = in[i][j][c];  // k = j of row c
+          } else if (ES == 2) {
             // k pairs (2j, 2j+1) of row c
             const unsigned lo = (in[i][2 * j][c >> 1] >> ((c & 1) * 16)) & 0xffffu;
             const unsigned hi = (in[i][2 * j + 1][c >> 1] >> ((c & 1) * 16)) & 0xffffu;
@@ -308,6 +352,14 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
 }
 template <> __device__ __forceinline__ uint16_t to_out<DT_BF16>(float x) { return f32_to_bf16_rne(x); }
 template <> __device__ __forceinline__ uint16_t to_out<DT_FP8>(float x) { return f32_to_bf16_rne(x); }
+
+// One output element at byte offset `off` of C (fp32 results are stored as is).
+template <int DT> __device__ __forceinline__ void store_out(float x, Rsrc rc, int off) {
+  if constexpr (DT == DT_F32)
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, x), rc, off, 0, 0);
+  else
+    __builtin_amdgcn_raw_buffer_store_b16(to_out<DT>(x), rc, off, 0, 0);
+}
 
 // ---------------------------------------------------------------------------
 // Tile order: logical tile ids are laid out so that the first
@@ -392,7 +444,8 @@ go_gemm(KLaunch L) {
   const Rsrc rc = make_rsrc(p.c, p.c_bytes);
   const int lda_b = (int)p.lda * C::ES;
   const int ldb_b = (int)p.ldb * C::ES;
-  const int ldc_b = (int)p.ldc * 2;
+  constexpr int OS = OutSize<DT>::v;
+  const int ldc_b = (int)p.ldc * OS;
   const int Mrows = (int)p.m, Ncols = (int)p.n;
 
   for (int t = (int)blockIdx.x - wg0; t < ntiles; t += nwg) {
@@ -469,8 +522,7 @@ go_gemm(KLaunch L) {
             rr = 4 * (lane >> 4) + r;
           const int row = m0 + wm * C::WTM + i * MM + rr;
           if (row < Mrows && col < Ncols)
-            __builtin_amdgcn_raw_buffer_store_b16(to_out<DT>(acc[i][j][r] * s), rc,
-                                                  row * ldc_b + col * 2, 0, 0);
+            store_out<DT>(acc[i][j][r] * s, rc, row * ldc_b + col * OS);
         }
       }
     }

@@ -20,7 +20,7 @@ N_FEATURES = 18
 CD_CLASSES = (1, 2, 4, 8, 16)
 
 # gdy_dtype
-F16, BF16, FP8_E4M3 = 1, 2, 3
+F16, BF16, FP8_E4M3, F32 = 1, 2, 3, 4
 # gdy_mode
 SEQUENTIAL, DEFAULT, GO, SELECTOR, FORCED, FORCED_GROUPED = 0, 1, 2, 3, 4, 5
 MODES = {"sequential": SEQUENTIAL, "default": DEFAULT, "go": GO,
@@ -134,7 +134,7 @@ def _dtype_code(t) -> int:
     if _TORCH_DTYPE is None:
         import torch
         _TORCH_DTYPE = {torch.float16: F16, torch.bfloat16: BF16, torch.float8_e4m3fn: FP8_E4M3,
-                        torch.uint8: FP8_E4M3}
+                        torch.uint8: FP8_E4M3, torch.float32: F32}
     return _TORCH_DTYPE[t.dtype]
 
 

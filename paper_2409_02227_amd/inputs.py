@@ -31,8 +31,9 @@ from dataclasses import dataclass, field, replace
 
 import numpy as np
 
-ELEM = {"bf16": 2, "f16": 2, "fp8": 1}
-OUT = {"bf16": "bf16", "f16": "f16", "fp8": "bf16"}
+ELEM = {"bf16": 2, "f16": 2, "fp8": 1, "f32": 4}
+OUT = {"bf16": "bf16", "f16": "f16", "fp8": "bf16", "f32": "f32"}
+OUT_ELEM = {"bf16": 2, "f16": 2, "f32": 4}
 
 
 @dataclass
@@ -40,7 +41,7 @@ class GemmSpec:
     m: int
     n: int
     k: int
-    dtype: str = "bf16"          # input type: bf16 | f16 | fp8
+    dtype: str = "bf16"          # input type: bf16 | f16 | fp8 | f32
     trans_a: int = 0
     trans_b: int = 0
     a_dist: tuple = ("uniform", -1.0, 1.0)
@@ -69,7 +70,7 @@ class GemmSpec:
 
     def compulsory_bytes(self) -> int:
         es = ELEM[self.dtype]
-        return (self.m * self.k + self.k * self.n) * es + self.m * self.n * 2
+        return (self.m * self.k + self.k * self.n) * es + self.m * self.n * OUT_ELEM[OUT[self.dtype]]
 
 
 # ---------------------------------------------------------------------------
@@ -99,6 +100,8 @@ def encode(values: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "fp8":
         t = torch.clamp(t, -448.0, 448.0)
         return t.to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    if dtype == "f32":
+        return t.numpy().view(np.uint32).copy()
     raise ValueError(dtype)
 
 
@@ -194,7 +197,8 @@ CONFIGS = {1: config1, 2: config2, 3: config3, 5: config5}
 # ---------------------------------------------------------------------------
 # device materialisation (torch is used for memory only)
 # ---------------------------------------------------------------------------
-_TORCH_CODE = {"bf16": "bfloat16", "f16": "float16", "fp8": "float8_e4m3fn"}
+_TORCH_CODE = {"bf16": "bfloat16", "f16": "float16", "fp8": "float8_e4m3fn", "f32": "float32"}
+_RAW_VIEW = {1: np.uint8, 2: np.int16, 4: np.int32}
 
 
 @dataclass
@@ -212,7 +216,7 @@ class Materialized:
 def _device_tensor(codes: np.ndarray, dtype: str, rows: int, ld: int, cols: int, device):
     import torch
     tdt = getattr(torch, _TORCH_CODE[dtype])
-    raw = torch.from_numpy(codes.view(np.uint8) if dtype == "fp8" else codes.view(np.int16))
+    raw = torch.from_numpy(codes.view(_RAW_VIEW[ELEM[dtype]]))
     full = raw.to(device).view(tdt).reshape(rows, ld) if rows > 0 else \
         torch.empty((0, ld), dtype=tdt, device=device)
     return full[:, :cols]

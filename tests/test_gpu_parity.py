@@ -1,9 +1,10 @@
 """GPU parity: every GO-Kernel and every execution mode against the CPU
 oracle, through the C-ABI (libgdy.so via the ctypes binding).
 
-Bar (spec contract): |gpu - ref| <= tau * sum_k |a(i,k) b(k,j)| + 1e-6
-with tau = 2^-7 for bf16/fp16 inputs and 2^-3 for fp8; results of one
-variant are bit-identical between isolated and concurrent execution.
+Bar: |gpu - ref| <= tau * sum_k |a(i,k) b(k,j)| + 1e-6 with tau = 2^-7 for
+bf16/fp16 inputs and 2^-3 for fp8 (the stated contract) and 2^-10 for fp32
+(derived from K * 2^-24 at K <= 16384); results of one variant are
+bit-identical between isolated and concurrent execution.
 """
 import itertools
 import os
@@ -21,7 +22,7 @@ from tests.gpu_helpers import check, gemm_of, out_codes, reset_outputs  # noqa: 
 
 pytestmark = pytest.mark.gpu
 
-DT_NAME = {1: "f16", 2: "bf16", 3: "fp8"}
+DT_NAME = {1: "f16", 2: "bf16", 3: "fp8", 4: "f32"}
 
 
 @pytest.fixture(scope="module")
@@ -52,7 +53,7 @@ def test_every_kernel_ragged_tiles(ctx):
     for vid, v in _kernels(ctx):
         bm, bn, bk = v["bm"], v["bn"], v["bk"]
         dt = DT_NAME[v["dtype"]]
-        spec = GemmSpec(2 * bm - 5, bn + 3, 2 * bk + 37 if dt != "fp8" else bk + 53, dt,
+        spec = GemmSpec(2 * bm - 5, bn + 3, {"fp8": bk + 53, "f32": 2 * bk + 7}.get(dt, 2 * bk + 37), dt,
                         v["trans_a"], v["trans_b"], seed=vid, name=v["name"])
         mat = inputs.materialize(spec)
         _run(ctx, [mat], "forced", 1, [vid])
@@ -70,7 +71,7 @@ def test_every_kernel_aligned_multi_tile(ctx):
         check(mat, label=v["name"])
 
 
-@pytest.mark.parametrize("dt,ta,tb", [(d, a, b) for d in ("bf16", "f16", "fp8")
+@pytest.mark.parametrize("dt,ta,tb", [(d, a, b) for d in ("bf16", "f16", "fp8", "f32")
                                       for a, b in itertools.product([0, 1], [0, 1])])
 def test_odd_leading_dims_and_tiny_shapes(ctx, dt, ta, tb):
     """ld > minimal and unaligned (element-wise load path), M = 1, K = 1,
@@ -399,3 +400,24 @@ def test_direct_kernels_k_depths(ctx):
             plan = _run(ctx, [mat], "forced", 1, [vid])
             assert plan["variant_of"][0] == vid, f"{v['name']}: direct path not taken"
             check(mat, label=f"{v['name']} nk={nk}")
+
+
+def test_f32_concurrent_and_selector_modes(ctx):
+    """fp32 GEMMs (the paper's full-precision case) in every execution mode:
+    the fused and stream launches of one variant give the isolated bits."""
+    specs = [GemmSpec(300 + 37 * i, 520 - 41 * i, 384 + 64 * i, "f32", i % 2, (i // 2) % 2,
+                      seed=950 + i, name=f"f32_{i}") for i in range(4)]
+    mats = [inputs.materialize(s) for s in specs]
+    for mode in ("sequential", "default", "go", "selector"):
+        _run(ctx, mats, mode)
+        for m in mats:
+            check(m, label=f"f32 {mode}")
+    vid = ctx.find("f32_nn_128x128_w2x2_m32_c0")
+    assert vid >= 0
+    same = [inputs.materialize(GemmSpec(200, 300, 100 + 50 * i, "f32", seed=960 + i, name=f"f32s{i}"))
+            for i in range(4)]
+    iso = _isolated_codes(ctx, same, [vid] * 4)
+    for mode, cd in (("forced", 4), ("forced_grouped", 4)):
+        _run(ctx, same, mode, cd, [vid] * 4)
+        for m, ref in zip(same, iso):
+            assert np.array_equal(out_codes(m), ref), f"{mode}: {m.spec.name} differs"

@@ -255,3 +255,14 @@ def test_accept_rule():
     assert not ok
     ok, _ = oracle.accept([np.nan, -2.0], ref, bound, 2.0 ** -7)
     assert not ok
+
+
+def test_f32_codes_decode_as_numpy_float32():
+    """fp32 storage decodes to the float64 value of the same float32 (numpy
+    conversion), subnormals and signed zeros included."""
+    rng = np.random.default_rng(12)
+    codes = rng.integers(0, 2 ** 32, size=4096, dtype=np.uint64).astype(np.uint32)
+    codes = codes[(codes & 0x7f800000) != 0x7f800000]  # finite codes only
+    codes = np.concatenate([codes, np.array([0, 0x80000000, 1, 0x807fffff, 0x7f7fffff], np.uint32)])
+    got = oracle.decode(codes, "f32")
+    np.testing.assert_array_equal(got, codes.view(np.float32).astype(np.float64))

@@ -104,7 +104,7 @@ def _desc(m, n, k, dtype, ta, tb, base, pad=0):
     d = gdy.GemmDesc()
     d.m, d.n, d.k = m, n, k
     d.a_type = d.b_type = dtype
-    d.c_type = 1 if dtype == 1 else 2
+    d.c_type = {1: 1, 2: 2, 3: 2, 4: 4}[dtype]
     d.trans_a, d.trans_b = ta, tb
     d.lda = (m if ta else k) + pad
     d.ldb = (k if tb else n) + pad
@@ -130,7 +130,7 @@ def _synthetic_table(path, ctx, rng):
     lines.append("lr_max " + " ".join(map(repr, xmax.tolist())))
     lines.append("lr_w " + " ".join(map(repr, rng.normal(0, 2, sel.N_FEATURES * 5).tolist())))
     lines.append("lr_b " + " ".join(map(repr, rng.normal(0, 1, 5).tolist())))
-    for dtype in (1, 2, 3):
+    for dtype in (1, 2, 3, 4):
         for ta, tb in ((0, 0), (0, 1), (1, 1)):
             pool = [v["name"] for v in V if (v["dtype"], v["trans_a"], v["trans_b"]) == (dtype, ta, tb)]
             for mlog in (4, 7, 10, 12):
@@ -166,7 +166,7 @@ def _check_plan(ctx, table, descs, slots=16):
 def _random_set(rng, n):
     out = []
     for i in range(n):
-        dtype = int(rng.choice([1, 2, 3]))
+        dtype = int(rng.choice([1, 2, 3, 4]))
         ta, tb = [(0, 0), (0, 1), (1, 1)][int(rng.integers(3))]
         m = int(rng.integers(1, 5000))
         nn = int(rng.choice([512, 1000, 2048, 4096, 8192]))
@@ -207,7 +207,7 @@ def test_planner_matches_oracle_on_the_tuned_table():
     for specs in sets:
         descs = []
         for i, s in enumerate(specs):
-            d = _desc(s.m, s.n, s.k, {"f16": 1, "bf16": 2, "fp8": 3}[s.dtype], s.trans_a,
+            d = _desc(s.m, s.n, s.k, {"f16": 1, "bf16": 2, "fp8": 3, "f32": 4}[s.dtype], s.trans_a,
                       s.trans_b, (i + 1) << 36)
             descs.append(d)
         _check_plan(ctx, table, descs)
