@@ -24,7 +24,7 @@ sys.path.insert(0, ROOT)
 
 import numpy as np  # noqa: E402
 
-PEAK_TFLOPS = {"bf16": 2516.6, "f16": 2516.6, "fp8": 5033.2}  # MI355X dense MFMA
+PEAK_TFLOPS = {"bf16": 2516.6, "f16": 2516.6, "fp8": 5033.2, "f32": 157.3}  # MI355X dense MFMA
 PEAK_HBM_GBS = 8000.0
 METRIC = "aggregate TFLOP/s of concurrent GEMM sets; speedup vs sequential; % MFMA peak"
 DEFAULT_TABLE = os.path.join(ROOT, "paper_2409_02227_amd", "tables", "gfx950.table")
@@ -37,6 +37,9 @@ WORKLOADS = {
     "two_tenant_fp8": (5, "2 tenants x 16 fp8 e4m3 GEMMs, M in {1,32,256,2048}, N=K in {4096,8192}"),
     "het_submissions": (4, "seeded submissions of 2-16 bf16 GEMMs, M log-uniform in [16,4096], "
                            "N,K in {1024,2048,4096,8192}, operands windows of device pools"),
+    "tp8_layer_share_nt": ("3nt", "the 8 bf16 GEMMs of tp8_layer_share with each weight stored N x K "
+                                  "(linear-layer layout) and used transposed"),
+    "tp8_layer_share_f32": ("3f32", "the 8 GEMMs of tp8_layer_share in fp32 (full precision)"),
 }
 TRAFFIC = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2409_02227_amd", "csrc", f)
@@ -168,7 +171,7 @@ def cpu_baseline(mats, target_s):
     """The oracle on full rows of every GEMM: calibrate rows per GEMM with a
     one-row pass, then time a sample of about target_s seconds."""
     import oracle
-    dt = {"bf16": "bf16", "f16": "f16", "fp8": "e4m3fn"}
+    dt = {"bf16": "bf16", "f16": "f16", "fp8": "e4m3fn", "f32": "f32"}
 
     def run(rows):
         fl, t0 = 0, time.perf_counter()
@@ -257,7 +260,12 @@ def main():
     cfg_id, desc = WORKLOADS[args.workload]
     if cfg_id == 4:
         return het_bench(args, desc)
-    specs = inputs.CONFIGS[cfg_id]()
+    if cfg_id == "3nt":
+        specs = inputs.config3(trans_b=1)
+    elif cfg_id == "3f32":
+        specs = inputs.config3(dtype="f32")
+    else:
+        specs = inputs.CONFIGS[cfg_id]()
     mats = [inputs.materialize(s, "cuda:0", keep_host=True) for s in specs]
     table = args.table if args.table and os.path.exists(args.table) else None
     ctx = gdy.Context(0, table=table, max_streams=16)

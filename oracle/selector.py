@@ -15,6 +15,9 @@ Definitions followed:
   * Sec. 4.3, Eq. 1: P = exp(X W) / sum_i exp(X W_i) over the CD classes
     1, 2, 4, 8, 16, on min-max normalised features; the predicted CD is the
     most probable class; the executed CD is min(predicted, available GEMMs).
+    A table may hold one predictor per input type (precision changes how
+    GEMMs share the GPU, Sec. 6.8; the features do not describe it); a
+    GEMM uses its type's predictor when present, else the shared one.
   * Sec. 4.4: a single GEMM keeps its isolated kernel.
   * Sec. 6.7: GEMMs of a heterogeneous set run together only if all of them
     prefer that CD; otherwise they are split into smaller sets.  Reading
@@ -49,8 +52,12 @@ N_FEATURES = 3 + 3 * len(CD_CLASSES)
 # ---------------------------------------------------------------------------
 
 def parse_table(path: str) -> dict:
-    t = {"entries": [], "lr": None}
-    lr = {}
+    """Entries and predictors: t["lr"] is the predictor shared by all input
+    types, t["lr_by_type"][d] one trained on input type d alone (its lines
+    follow an "lr_dtype d" line)."""
+    t = {"entries": [], "lr": None, "lr_by_type": {}}
+    blocks = {0: {}}
+    cur = 0
     with open(path) as f:
         for raw in f:
             line = raw.strip()
@@ -61,17 +68,31 @@ def parse_table(path: str) -> dict:
                 t["arch"], t["cus"] = tok[1], int(tok[3])
             elif tok[0] == "catalogue":
                 t["catalogue"] = int(tok[1], 16)
+            elif tok[0] == "lr_dtype":
+                cur = int(tok[1])
+                blocks.setdefault(cur, {})
             elif tok[0] in ("lr_min", "lr_max", "lr_b"):
-                lr[tok[0]] = np.array([float(x) for x in tok[1:]])
+                blocks[cur][tok[0]] = np.array([float(x) for x in tok[1:]])
             elif tok[0] == "lr_w":
-                lr["lr_w"] = np.array([float(x) for x in tok[1:]]).reshape(N_FEATURES, len(CD_CLASSES))
+                blocks[cur]["lr_w"] = np.array([float(x) for x in tok[1:]]).reshape(
+                    N_FEATURES, len(CD_CLASSES))
             elif tok[0] == "entry":
                 t["entries"].append({"dtype": int(tok[1]), "ta": int(tok[2]), "tb": int(tok[3]),
                                      "mlog": int(tok[4]), "n": int(tok[5]), "k": int(tok[6]),
                                      "variants": tok[7:12]})
-    if len(lr) == 4:
-        t["lr"] = {"xmin": lr["lr_min"], "xmax": lr["lr_max"], "w": lr["lr_w"], "b": lr["lr_b"]}
+    for d, lr in blocks.items():
+        if len(lr) == 4:
+            model = {"xmin": lr["lr_min"], "xmax": lr["lr_max"], "w": lr["lr_w"], "b": lr["lr_b"]}
+            if d == 0:
+                t["lr"] = model
+            else:
+                t["lr_by_type"][d] = model
     return t
+
+
+def predictor_for(table: dict, dtype: int):
+    """The input type's own predictor when the table has one, else the shared one."""
+    return table["lr_by_type"].get(dtype, table["lr"])
 
 
 # ---------------------------------------------------------------------------
@@ -249,17 +270,26 @@ def plan_selector(gemms: list, table: dict, variants: list, cus: int, slots: int
             out["groups"], out["variant_of"], variants, slots)
         return out
     for i in live:
+        lr = predictor_for(table, gemms[i]["a_type"])
+        if lr is None:
+            out["pred_cd"][i] = clamp(1, n)
+            continue
         x = features(gemms[i], table, variants, by_name, cus)
-        out["pred_cd"][i] = clamp(predict_cd(x, table["lr"]), n)
+        out["pred_cd"][i] = clamp(predict_cd(x, lr), n)
     order = sorted(live, key=lambda i: -out["pred_cd"][i])  # stable: submission order on ties
-    groups = group(order, out["pred_cd"], slots)
-    # within a group, longest (2MNK) first; stable
-    out["groups"] = [sorted(grp, key=lambda i: -(gemms[i]["m"] * gemms[i]["n"] * gemms[i]["k"]))
-                     for grp in groups]
-    for grp in out["groups"]:
+    out["groups"] = []
+    for grp in group(order, out["pred_cd"], slots):
         ci = class_for_size(len(grp))
+        parts = {}  # kernel -> GEMMs, in order of first appearance
         for i in grp:
             out["variant_of"][i] = bind(gemms[i], ci, table, variants, by_name)
+            parts.setdefault(kernel_of(variants[out["variant_of"][i]]["name"]), []).append(i)
+        # inside a dispatch: K descending, then M*N; dispatches: total 2MNK descending
+        parts = [sorted(v, key=lambda i: (-gemms[i]["k"], -gemms[i]["m"] * gemms[i]["n"]))
+                 for v in parts.values()]
+        work = [sum(2.0 * gemms[i]["m"] * gemms[i]["n"] * gemms[i]["k"] for i in v) for v in parts]
+        ranked = sorted(range(len(parts)), key=lambda u: -work[u])
+        out["groups"].append([i for u in ranked for i in parts[u]])
     out["dispatch_of"], out["stream_of"], out["n_dispatches"] = dispatches(
         out["groups"], out["variant_of"], variants, slots)
     return out

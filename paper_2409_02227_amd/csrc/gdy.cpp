@@ -54,14 +54,25 @@ struct TableEntry {
   int v[GDY_N_CD];
 };
 
-struct Table {
-  bool loaded = false;
-  bool has_lr = false;
-  std::vector<TableEntry> entries;
-  std::vector<int> by_layout[5][2][2];  // entry indices per (dtype, ta, tb), file order
+// One CD predictor (Eq. 1): min-max bounds of the features, weights, biases.
+struct Predictor {
+  bool has = false;
   double xmin[GDY_N_FEATURES], xmax[GDY_N_FEATURES];
   double w[GDY_N_FEATURES][GDY_N_CD];
   double b[GDY_N_CD];
+};
+
+struct Table {
+  bool loaded = false;
+  std::vector<TableEntry> entries;
+  std::vector<int> by_layout[5][2][2];  // entry indices per (dtype, ta, tb), file order
+  // lr[0]: the predictor for every input type; lr[d]: one trained on input
+  // type d alone, used for GEMMs of that type when present
+  Predictor lr[5];
+  const Predictor* for_type(int dtype) const {
+    if (dtype >= 1 && dtype <= 4 && lr[dtype].has) return &lr[dtype];
+    return lr[0].has ? &lr[0] : nullptr;
+  }
 };
 
 int elem_size(int dt) { return dt == DT_FP8 ? 1 : dt == DT_F32 ? 4 : 2; }
@@ -272,8 +283,7 @@ void features(const gdy_ctx* ctx, const gdy_gemm& g, int entry, double* x) {
 // the argmax of the linear scores (softmax is monotone).  Features are
 // min-max normalised with the training minima and maxima.  Ties go to the
 // smaller CD.  Returns the CD value (1..16).
-int predict_cd(const gdy_ctx* ctx, const double* x) {
-  const Table& t = ctx->table;
+int predict_cd(const Predictor& t, const double* x) {
   double xn[GDY_N_FEATURES];
   for (int i = 0; i < GDY_N_FEATURES; ++i) {
     const double span = t.xmax[i] - t.xmin[i];
@@ -513,9 +523,9 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
 
   // GDY_SELECTOR (Sec. 4.3, Sec. 6.7): per-GEMM CD = min(predicted, n);
   // sort by it (descending, stable); greedily form groups whose size never
-  // exceeds any member's CD; groups run one after another, longest GEMM
-  // first within a group, each bound to the GO-Kernel tuned for the group's
-  // size and dispatched with the group's other GEMMs of the same kernel.
+  // exceeds any member's CD; groups run one after another, each GEMM bound
+  // to the GO-Kernel tuned for the group's size and dispatched with the
+  // group's other GEMMs of the same kernel.
   // Without a trained predictor every GEMM keeps CD 1.
   std::vector<int> pred(n, 0);
   std::vector<int> entry(n, -1);  // nearest tuned shape, looked up once per GEMM
@@ -523,10 +533,11 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
     const int i = live[t];
     entry[i] = nearest_entry(ctx, g[i]);
     int cd = 1;
-    if (ctx->table.loaded && ctx->table.has_lr) {
+    const Predictor* lr = ctx->table.loaded ? ctx->table.for_type(g[i].a_type) : nullptr;
+    if (lr) {
       double x[GDY_N_FEATURES];
       features(ctx, g[i], entry[i], x);
-      cd = predict_cd(ctx, x);
+      cd = predict_cd(*lr, x);
     } else {
       fb = true;
     }
@@ -547,26 +558,51 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
     gcap = std::min(gcap, cap);
     groups.back().push_back(i);
   }
-  // within a group, longest first (estimated by 2MNK): the GEMMs whose
-  // tiles take longest are dispatched first
+  // launch order within a group: the GEMMs bound to one kernel form one
+  // dispatch (a group holds at most 16); inside it the longest workgroups
+  // go first (tiles of one size take time in proportion to K: K
+  // descending, then M*N), and the dispatches go in order of their total
+  // work (sum of 2MNK, descending), so the largest one starts first on the
+  // origin stream.  Ties keep the grouping order.
   int t = 0;
   p->n_groups = (int)groups.size();
   p->cd = 0;
   for (int q = 0; q < p->n_groups; ++q) {
-    std::vector<int>& grp = groups[q];
-    std::stable_sort(grp.begin(), grp.end(), [&](int a, int b) {
-      return g[a].m * g[a].n * g[a].k > g[b].m * g[b].n * g[b].k;
-    });
+    const std::vector<int>& grp = groups[q];
     const int s = (int)grp.size();
+    std::vector<int> kern;                // kernels in order of first appearance
+    std::vector<std::vector<int>> parts;  // their GEMMs
+    for (int i : grp) {
+      p->variant_of[i] = bind_entry(ctx, g[i], entry[i], class_for_size(s), &fb);
+      const int k = ctx->variants[p->variant_of[i]].kernel;
+      size_t u = 0;
+      while (u < kern.size() && kern[u] != k) ++u;
+      if (u == kern.size()) {
+        kern.push_back(k);
+        parts.emplace_back();
+      }
+      parts[u].push_back(i);
+    }
+    std::vector<double> work(parts.size(), 0.0);
+    for (size_t u = 0; u < parts.size(); ++u) {
+      std::stable_sort(parts[u].begin(), parts[u].end(), [&](int a, int b) {
+        if (g[a].k != g[b].k) return g[a].k > g[b].k;
+        return g[a].m * g[a].n > g[b].m * g[b].n;
+      });
+      for (int i : parts[u]) work[u] += 2.0 * (double)g[i].m * (double)g[i].n * (double)g[i].k;
+    }
+    std::vector<int> pord(parts.size());
+    for (size_t u = 0; u < pord.size(); ++u) pord[u] = (int)u;
+    std::stable_sort(pord.begin(), pord.end(), [&](int a, int b) { return work[a] > work[b]; });
+    std::vector<int> ordered;
+    for (int u : pord) ordered.insert(ordered.end(), parts[u].begin(), parts[u].end());
     p->group_size[q] = s;
     p->cd = std::max(p->cd, s);
-    for (int u = 0; u < s; ++u) {
-      const int i = grp[u];
+    for (int i : ordered) {
       p->order[t++] = i;
       p->group_of[i] = q;
-      p->variant_of[i] = bind_entry(ctx, g[i], entry[i], class_for_size(s), &fb);
     }
-    form_dispatches(ctx, grp, S, p);
+    form_dispatches(ctx, ordered, S, p);
   }
   p->fallback = fb ? 1 : 0;
 }
@@ -740,7 +776,10 @@ gdy_status load_table(gdy_ctx* ctx, const char* path) {
   if (!f) return fail(ctx, GDY_ERR_TABLE, "cannot open GO table %s", path);
   Table t;
   std::string line, tag;
-  int have_min = 0, have_max = 0, have_w = 0, have_b = 0;
+  // predictor blocks: lr_min / lr_max / lr_w / lr_b lines belong to the
+  // input type of the last lr_dtype line (none yet: the shared predictor)
+  int cur = 0;
+  int have[5][4] = {};  // min, max, w, b seen per block
   bool header = false;
   while (std::getline(f, line)) {
     if (line.empty() || line[0] == '#') continue;
@@ -768,17 +807,21 @@ gdy_status load_table(gdy_ctx* ctx, const char* path) {
       // grows; a name the library does not know is rejected below.
       std::string hex;
       in >> hex;
+    } else if (tag == "lr_dtype") {
+      if (!(in >> cur) || cur < 1 || cur > 4) return fail(ctx, GDY_ERR_TABLE, "bad lr_dtype line");
     } else if (tag == "lr_min" || tag == "lr_max" || tag == "lr_b") {
-      double* dst = tag == "lr_min" ? t.xmin : tag == "lr_max" ? t.xmax : t.b;
+      Predictor& P = t.lr[cur];
+      double* dst = tag == "lr_min" ? P.xmin : tag == "lr_max" ? P.xmax : P.b;
       const int cnt = tag == "lr_b" ? GDY_N_CD : GDY_N_FEATURES;
       for (int i = 0; i < cnt; ++i)
         if (!(in >> dst[i])) return fail(ctx, GDY_ERR_TABLE, "short %s row", tag.c_str());
-      (tag == "lr_min" ? have_min : tag == "lr_max" ? have_max : have_b) = 1;
+      have[cur][tag == "lr_min" ? 0 : tag == "lr_max" ? 1 : 3] = 1;
     } else if (tag == "lr_w") {
+      Predictor& P = t.lr[cur];
       for (int i = 0; i < GDY_N_FEATURES; ++i)
         for (int c = 0; c < GDY_N_CD; ++c)
-          if (!(in >> t.w[i][c])) return fail(ctx, GDY_ERR_TABLE, "short lr_w row");
-      have_w = 1;
+          if (!(in >> P.w[i][c])) return fail(ctx, GDY_ERR_TABLE, "short lr_w row");
+      have[cur][2] = 1;
     } else if (tag == "entry") {
       TableEntry e;
       in >> e.dtype >> e.ta >> e.tb >> e.mlog >> e.n >> e.k;
@@ -806,7 +849,11 @@ gdy_status load_table(gdy_ctx* ctx, const char* path) {
     }
   }
   if (!header) return fail(ctx, GDY_ERR_TABLE, "%s is not a GO table", path);
-  t.has_lr = have_min && have_max && have_w && have_b;
+  for (int d = 0; d < 5; ++d) {
+    const int seen = have[d][0] + have[d][1] + have[d][2] + have[d][3];
+    if (seen != 0 && seen != 4) return fail(ctx, GDY_ERR_TABLE, "incomplete predictor block %d", d);
+    t.lr[d].has = seen == 4;
+  }
   t.loaded = true;
   ctx->table = t;
   return GDY_OK;

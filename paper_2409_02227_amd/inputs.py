@@ -146,11 +146,15 @@ CONFIG3_SHAPES = (("qkv", 512, 4608, 12288), ("out", 512, 12288, 1536),
                   ("up", 512, 6144, 12288), ("down", 512, 12288, 6144))
 
 
-def config3(seed: int = 3) -> list:
+def config3(seed: int = 3, dtype: str = "bf16", trans_b: int = 0) -> list:
+    """The tensor-sliced layer share; `dtype` f32 gives its full-precision
+    form, `trans_b` 1 stores each weight N x K (the layout of a linear
+    layer's weight) and uses it transposed."""
     out = []
     for mb in range(2):
         for j, (nm, m, n, k) in enumerate(CONFIG3_SHAPES):
-            out.append(GemmSpec(m, n, k, "bf16", seed=seed * 1000 + 10 * mb + j, name=f"{nm}_mb{mb}"))
+            out.append(GemmSpec(m, n, k, dtype, 0, trans_b, seed=seed * 1000 + 10 * mb + j,
+                                name=f"{nm}_mb{mb}"))
     return out
 
 

@@ -39,9 +39,10 @@ import paper_2409_02227_amd  # noqa: F401,E402  (GPU_MAX_HW_QUEUES before HIP st
 
 CDS = (1, 2, 4, 8, 16)
 RCS = (0, 128, 64, 32)  # whole GPU, then CU-masked budgets
-DT_CODE = {"f16": 1, "bf16": 2, "fp8": 3}
+DT_CODE = {"f16": 1, "bf16": 2, "fp8": 3, "f32": 4}
 BEST_CD_GAIN = 1.05     # Sec. 5.5: sequential unless a CD gives >= 5%
 LABEL_TOL = 0.03        # CDs within 3% of the best speedup count as equally good
+MIN_TYPE_RECORDS = 20   # an input type gets its own predictor from this many tuned shapes
 
 
 # ---------------------------------------------------------------------------
@@ -64,6 +65,18 @@ def shape_set(kind: str) -> list:
         ms = (16, 32, 64, 128, 256, 512, 1024, 2048, 4096)
         nks = (1024, 2048, 4096, 8192)
     shapes += [("bf16", 0, 0, m, n, k) for m in ms for n in nks for k in nks]
+    if kind == "full":
+        # transposed layouts (Sec. 2.5, 3.2: transposes change how GEMMs share the
+        # GPU) and full precision (Sec. 5.2), on a coarser grid, plus the
+        # layer share in both forms
+        ms2, nks2 = (16, 64, 256, 1024, 4096), (1024, 4096)
+        for ta, tb in ((0, 1), (1, 0), (1, 1)):
+            shapes += [("bf16", ta, tb, m, n, k) for m in ms2 for n in nks2 for k in nks2]
+        shapes += [("f32", 0, 0, m, n, k) for m in ms2 for n in nks2 for k in nks2]
+        shapes += [("f16", 0, 0, m, n, k) for m in ms2 for n in nks2 for k in nks2]
+        for nm, m, n, k in (("qkv", 512, 4608, 12288), ("out", 512, 12288, 1536),
+                            ("up", 512, 6144, 12288), ("down", 512, 12288, 6144)):
+            shapes += [("bf16", 0, 1, m, n, k), ("f32", 0, 0, m, n, k)]
     seen, out = set(), []
     for s in shapes:
         if s not in seen:
@@ -117,8 +130,9 @@ def operands(torch, dtype, ta, tb, m, n, k, copies, outputs_per_copy):
     """`copies` independent operand sets with random values (timing only);
     each copy gets `outputs_per_copy` distinct C buffers so that repeated
     runs of one copy are separate GEMMs of the submission."""
-    tdt = {"bf16": torch.bfloat16, "f16": torch.float16, "fp8": torch.float8_e4m3fn}[dtype]
-    odt = torch.float16 if dtype == "f16" else torch.bfloat16
+    tdt = {"bf16": torch.bfloat16, "f16": torch.float16, "fp8": torch.float8_e4m3fn,
+           "f32": torch.float32}[dtype]
+    odt = {"f16": torch.float16, "f32": torch.float32}.get(dtype, torch.bfloat16)
     out = []
     for _ in range(copies):
         a = torch.randn((k, m) if ta else (m, k), device="cuda").to(tdt)
@@ -214,17 +228,25 @@ def tune_shape(ctx, bench, torch, variants, shape, rounds=3):
 # table writing and predictor training
 # ---------------------------------------------------------------------------
 
-def write_table(path, ctx, records, lr=None):
-    import socket  # noqa: F401  (hostnames are not recorded)
+def _lr_lines(lr) -> list:
+    return ["lr_min " + " ".join(repr(float(x)) for x in lr["xmin"]),
+            "lr_max " + " ".join(repr(float(x)) for x in lr["xmax"]),
+            "lr_w " + " ".join(repr(float(x)) for x in np.asarray(lr["w"]).ravel()),
+            "lr_b " + " ".join(repr(float(x)) for x in lr["b"])]
+
+
+def write_table(path, ctx, records, lr=None, lr_by_type=None):
+    """GO table: header, the shared predictor, one predictor block per input
+    type that has its own ("lr_dtype <code>" then its four lines), entries."""
     lines = ["gdy-go-table 1",
              f"# written by paper_2409_02227_amd.tuner on {time.strftime('%Y-%m-%d %H:%M:%S')}",
              f"device gfx950 cus {ctx.cus()}",
              f"catalogue {ctx.catalogue_hash():016x}"]
     if lr is not None:
-        lines.append("lr_min " + " ".join(repr(float(x)) for x in lr["xmin"]))
-        lines.append("lr_max " + " ".join(repr(float(x)) for x in lr["xmax"]))
-        lines.append("lr_w " + " ".join(repr(float(x)) for x in np.asarray(lr["w"]).ravel()))
-        lines.append("lr_b " + " ".join(repr(float(x)) for x in lr["b"]))
+        lines += _lr_lines(lr)
+    for code, model in sorted((lr_by_type or {}).items()):
+        lines.append(f"lr_dtype {int(code)}")
+        lines += _lr_lines(model)
     for r in records:
         dtype, ta, tb, m, n, k = r["shape"]
         mlog = max(0, math.ceil(math.log2(max(m, 1))))
@@ -244,7 +266,7 @@ def feature_rows(ctx, records):
         d = gdy.GemmDesc()
         d.m, d.n, d.k = m, n, k
         d.a_type = d.b_type = DT_CODE[dtype]
-        d.c_type = 1 if dtype == "f16" else 2
+        d.c_type = {"f16": 1, "f32": 4}.get(dtype, 2)
         d.trans_a, d.trans_b = ta, tb
         d.a, d.b, d.c = 1 << 20, 1 << 32, 1 << 40  # never dereferenced
         d.lda = m if ta else k
@@ -305,12 +327,13 @@ def predict_rows(X, lr):
     return np.array(CDS)[np.argmax(Xn @ lr["w"] + lr["b"], axis=1)]
 
 
-def evaluate(records, X, lr, idx):
+def evaluate(records, X, lr, idx, lr_by_type=None):
     """Sec. 6.6 style: with a GEMMs available (2, 4, 8, 16), the executed CD is
     min(predicted, a); it is correct when it equals the best-CD choice among
     CDs <= a (sequential unless a CD gains 5%); also the geomean of the
     speedup obtained over the best-CD speedup."""
-    pred = predict_rows(X[idx], lr)
+    pred = [predict_rows(X[i][None, :], (lr_by_type or {}).get(DT_CODE[records[i]["shape"][0]], lr))[0]
+            for i in idx]
     out = {}
     for a in CDS[1:]:
         ok, ratio = 0, []
@@ -372,11 +395,27 @@ def main(argv=None):
     ctx2 = gdy.Context(0, table=args.out, max_streams=16)
     X, y = feature_rows(ctx2, records)
     lr = train_lr(X, y)
-    write_table(args.out, ctx, records, lr)
+    # one predictor per input type with enough records of its own (precision
+    # changes how GEMMs share the GPU, Sec. 6.8, and no feature describes it)
+    codes = np.array([DT_CODE[r["shape"][0]] for r in records])
+    per = {}
+    for code in sorted(set(codes.tolist())):
+        idx = np.where(codes == code)[0]
+        if len(idx) >= MIN_TYPE_RECORDS and len(set(y[idx].tolist())) > 1:
+            m = train_lr(X[idx], y[idx])
+            m["test"], m["train"] = idx[m["test"]], idx[m["train"]]
+            per[code] = m
+    write_table(args.out, ctx, records, lr, per)
+    test = np.concatenate([per[c]["test"] if c in per else
+                           np.intersect1d(lr["test"], np.where(codes == c)[0])
+                           for c in sorted(set(codes.tolist()))])
     summary = {"shapes": len(records), "labels": {int(c): int((y == c).sum()) for c in CDS},
                "acc_train": lr["acc_train"], "acc_test": lr["acc_test"],
-               "by_available_test": evaluate(records, X, lr, lr["test"]),
-               "by_available_all": evaluate(records, X, lr, np.arange(len(records)))}
+               "per_type": {int(c): {"records": int((codes == c).sum()), "own_predictor": c in per,
+                                     "acc_test": per[c]["acc_test"] if c in per else None}
+                            for c in sorted(set(codes.tolist()))},
+               "by_available_test": evaluate(records, X, lr, test, per),
+               "by_available_all": evaluate(records, X, lr, np.arange(len(records)), per)}
     print(json.dumps(summary), flush=True)
     with open(os.path.splitext(args.out)[0] + "_summary.json", "w") as f:
         json.dump(summary, f, indent=1)

@@ -54,11 +54,15 @@ def test_written_table_reads_back(tmp_path):
     rng = np.random.default_rng(2)
     lr = {"xmin": np.zeros(18), "xmax": np.ones(18), "w": rng.normal(size=(18, 5)),
           "b": rng.normal(size=5)}
+    lr8 = {"xmin": np.zeros(18), "xmax": np.full(18, 2.0), "w": rng.normal(size=(18, 5)),
+           "b": rng.normal(size=5)}
     path = str(tmp_path / "t.table")
-    tuner.write_table(path, ctx, recs, lr)
+    tuner.write_table(path, ctx, recs, lr, {3: lr8})
     t = sel.parse_table(path)
     assert t["entries"][0]["variants"] == names and t["entries"][0]["mlog"] == 9
     np.testing.assert_array_equal(t["lr"]["w"], lr["w"])
+    np.testing.assert_array_equal(t["lr_by_type"][3]["w"], lr8["w"])
+    assert sel.predictor_for(t, 3) is t["lr_by_type"][3] and sel.predictor_for(t, 2) is t["lr"]
     c2 = gdy.Context(-1, table=path)       # the library accepts it
     d = gdy.GemmDesc(m=512, n=4096, k=1024, a_type=2, b_type=2, c_type=2, a=1 << 36,
                      b=2 << 36, c=3 << 36, lda=1024, ldb=4096, ldc=4096, scale_a=1.0,
