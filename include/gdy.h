@@ -111,6 +111,15 @@ typedef struct {
   float scale_a, scale_b;           /* fp8 per-tensor scales; must be 1.0f for other types  */
   int32_t tenant;                   /* caller's tag, reported back in per-kernel timings    */
   int32_t variant;                  /* GDY_FORCED: variant id to use; otherwise ignored     */
+  /* Strided batch (B-GEMM, Sec. 6.7): `batch` independent GEMMs of this
+   * shape; item b reads A + b*stride_a, B + b*stride_b and writes
+   * C + b*stride_c (strides in elements).  batch 0 or 1: a single GEMM and
+   * the strides are ignored.  C items must not overlap each other; A and B
+   * items may (stride 0 broadcasts one operand).  Every item obeys the
+   * single-GEMM extent limits. */
+  int32_t batch;
+  int32_t reserved;                 /* must be 0                                            */
+  int64_t stride_a, stride_b, stride_c;
 } gdy_gemm;
 
 /* A plan: how a submission is grouped, streamed and bound to variants. */

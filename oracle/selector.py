@@ -34,8 +34,9 @@ Definitions followed:
     nearest to s in log2 (ties toward the larger class).
 The library's documented substitution of a direct kernel by the staged
 kernel of the same tile (when K is not a whole number of K tiles or an
-operand is not 16-byte aligned) is reproduced so that the kernels compared
-are the ones that run.
+operand, row pitch or batch stride is not 16-byte aligned) is reproduced so
+that the kernels compared are the ones that run.  A strided batch (B-GEMM,
+Sec. 6.7) is one member of a submission whose workgroups cover every item.
 """
 from __future__ import annotations
 
@@ -99,9 +100,11 @@ def predictor_for(table: dict, dtype: int):
 # features (Sec. 4.3)
 # ---------------------------------------------------------------------------
 
-def n_workgroups(m: int, n: int, bm: int, bn: int, cap_cus: int, occupancy: int) -> int:
-    """Workgroups launched: one per output tile, or capped at cap x occupancy."""
-    tiles = math.ceil(m / bm) * math.ceil(n / bn)
+def n_workgroups(m: int, n: int, bm: int, bn: int, cap_cus: int, occupancy: int,
+                 batch: int = 1) -> int:
+    """Workgroups launched: one per output tile (of every item of a strided
+    batch), or capped at cap x occupancy."""
+    tiles = math.ceil(m / bm) * math.ceil(n / bn) * max(batch, 1)
     return tiles if cap_cus == 0 else min(tiles, cap_cus * max(occupancy, 1))
 
 
@@ -118,8 +121,10 @@ def direct_ok(v: dict, g: dict) -> bool:
     if not v["direct"]:
         return True
     es = elem_bytes(g["a_type"])
+    items = g.get("batch", 0) <= 1 or (
+        (g.get("stride_a", 0) * es) % 16 == 0 and (g.get("stride_b", 0) * es) % 16 == 0)
     return (g["k"] % v["bk"] == 0 and g["a"] % 16 == 0 and g["b"] % 16 == 0
-            and (g["lda"] * es) % 16 == 0 and (g["ldb"] * es) % 16 == 0)
+            and (g["lda"] * es) % 16 == 0 and (g["ldb"] * es) % 16 == 0 and items)
 
 
 def runnable(vid: int, g: dict, variants: list) -> int:
@@ -162,7 +167,8 @@ def features(g: dict, table: dict, variants: list, by_name: dict, cus: int) -> n
     for ci in range(len(CD_CLASSES)):
         v = variants[bind(g, ci, table, variants, by_name)]
         occ = v["occupancy"]
-        wgs = n_workgroups(g["m"], g["n"], v["bm"], v["bn"], v["grid_cap_cus"], occ)
+        wgs = n_workgroups(g["m"], g["n"], v["bm"], v["bn"], v["grid_cap_cus"], occ,
+                           g.get("batch", 0))
         x += [float(wgs), float(occ), n_waves(wgs, cus, occ)]
     return np.array(x)
 

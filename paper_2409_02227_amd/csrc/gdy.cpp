@@ -159,7 +159,7 @@ Geometry geometry(const gdy_ctx* ctx, int vid, const gdy_gemm& g) {
   Geometry geo;
   geo.tiles_m = (int)((g.m + k.d->bm - 1) / k.d->bm);
   geo.tiles_n = (int)((g.n + k.d->bn - 1) / k.d->bn);
-  geo.tiles = geo.tiles_m * geo.tiles_n;
+  geo.tiles = geo.tiles_m * geo.tiles_n * std::max(g.batch, 1);  // every item of a batch
   geo.grid = geo.tiles;
   if (v.cap > 0) geo.grid = std::min(geo.tiles, v.cap * std::max(k.occupancy, 1));
   return geo;
@@ -177,8 +177,9 @@ bool direct_ok(const gdy_ctx* ctx, int vid, const gdy_gemm& g) {
   const KernelDesc* d = ctx->kernels[ctx->variants[vid].kernel].d;
   if (!d->direct) return true;
   const int es = elem_size(g.a_type);
+  const bool items = g.batch <= 1 || ((g.stride_a * es) % 16 == 0 && (g.stride_b * es) % 16 == 0);
   return g.k % d->bk == 0 && (uintptr_t)g.a % 16 == 0 && (uintptr_t)g.b % 16 == 0 &&
-         (g.lda * es) % 16 == 0 && (g.ldb * es) % 16 == 0;
+         (g.lda * es) % 16 == 0 && (g.ldb * es) % 16 == 0 && items;
 }
 
 // The variant that actually runs for g: a direct variant whose requirements
@@ -333,6 +334,11 @@ gdy_status validate_one(gdy_ctx* ctx, const gdy_gemm& g, int i, Extent* ea, Exte
                 g.a_type, g.b_type, g.c_type);
   if ((g.trans_a != 0 && g.trans_a != 1) || (g.trans_b != 0 && g.trans_b != 1))
     return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: trans flags must be 0 or 1", i);
+  if (g.batch < 0 || g.reserved != 0)
+    return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: negative batch or nonzero reserved field", i);
+  const int64_t nb = std::max(g.batch, 1);
+  if (nb > 1 && (g.stride_a < 0 || g.stride_b < 0 || g.stride_c < 0))
+    return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: negative batch stride", i);
   if (!std::isfinite(g.scale_a) || !std::isfinite(g.scale_b))
     return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: non-finite scale", i);
   if ((t16 || t32) && (g.scale_a != 1.0f || g.scale_b != 1.0f))
@@ -347,8 +353,15 @@ gdy_status validate_one(gdy_ctx* ctx, const gdy_gemm& g, int i, Extent* ea, Exte
   int64_t cb;
   if (!stored_extent(g.m, g.n, g.ldc, os, &cb))
     return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: C extent too large", i);
+  if (nb > 1 && g.stride_c * os < cb)
+    return fail(ctx, GDY_ERR_ALIAS, "gemm %d: batch items of C overlap (stride_c too small)", i);
+  {
+    const int64_t bm = (g.m + 15) / 16, bn = (g.n + 15) / 16;  // tiles of the smallest kernel
+    if (bm * bn * nb >= (int64_t)INT32_MAX)
+      return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: batch x tiles too large", i);
+  }
   ec->lo = (uintptr_t)g.c;
-  ec->hi = ec->lo + (uintptr_t)cb;
+  ec->hi = ec->lo + (uintptr_t)((nb - 1) * g.stride_c * os + cb);
   if (g.k == 0) return GDY_OK;
   if (!g.a || !g.b) return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: null A or B", i);
   if (g.lda < (g.trans_a ? g.m : g.k)) return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: lda too small", i);
@@ -360,9 +373,9 @@ gdy_status validate_one(gdy_ctx* ctx, const gdy_gemm& g, int i, Extent* ea, Exte
   const bool okb = g.trans_b ? stored_extent(g.n, g.k, g.ldb, es, &bb) : stored_extent(g.k, g.n, g.ldb, es, &bb);
   if (!oka || !okb) return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: A or B extent too large", i);
   ea->lo = (uintptr_t)g.a;
-  ea->hi = ea->lo + (uintptr_t)ab;
+  ea->hi = ea->lo + (uintptr_t)((nb - 1) * g.stride_a * es + ab);
   eb->lo = (uintptr_t)g.b;
-  eb->hi = eb->lo + (uintptr_t)bb;
+  eb->hi = eb->lo + (uintptr_t)((nb - 1) * g.stride_b * es + bb);
   return GDY_OK;
 }
 
@@ -610,10 +623,12 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
 // ---------------------------------------------------------------------------
 // Launching
 // ---------------------------------------------------------------------------
-bool vec_ok(const void* ptr, int64_t ld, int es, bool kcontiguous) {
+// Vector loads need the base, the row pitch and (in a batch) the item
+// stride, all in bytes, aligned to the vector size.
+bool vec_ok(const void* ptr, int64_t ld, int es, bool kcontiguous, int64_t item_stride_bytes) {
   const uintptr_t a = (uintptr_t)ptr;
-  if (kcontiguous || es >= 2) return a % 16 == 0 && (ld * es) % 16 == 0;
-  return a % 8 == 0 && (ld * es) % 8 == 0;  // fp8 k-major operand: 8-byte row vectors
+  const int64_t v = (kcontiguous || es >= 2) ? 16 : 8;  // fp8 k-major operand: 8-byte row vectors
+  return a % v == 0 && (ld * es) % v == 0 && item_stride_bytes % v == 0;
 }
 
 // Buffer size for reads: the extent rounded up to the end of the dword that
@@ -653,11 +668,17 @@ KArgs make_args(const gdy_ctx* ctx, int vid, const gdy_gemm& g, Geometry* geo_ou
   a.c_bytes = (int32_t)cb;  // stores are element-wise: exact extent
   a.tiles_m = geo.tiles_m;
   a.tiles_n = geo.tiles_n;
-  a.a_vec = g.k > 0 && vec_ok(g.a, g.lda, es, g.trans_a == 0);
-  a.b_vec = g.k > 0 && vec_ok(g.b, g.ldb, es, g.trans_b == 1);
-  a.c_vec = (uintptr_t)g.c % 8 == 0 && (g.ldc * out_size(g)) % 8 == 0;
+  const bool batched = g.batch > 1;
+  a.a_vec = g.k > 0 && vec_ok(g.a, g.lda, es, g.trans_a == 0, batched ? g.stride_a * es : 0);
+  a.b_vec = g.k > 0 && vec_ok(g.b, g.ldb, es, g.trans_b == 1, batched ? g.stride_b * es : 0);
+  a.c_vec = (uintptr_t)g.c % 8 == 0 && (g.ldc * out_size(g)) % 8 == 0 &&
+            (!batched || (g.stride_c * out_size(g)) % 8 == 0);
   a.group_m = 8;
   a.xcd_remap = 1;
+  a.batch = (int32_t)std::max(g.batch, 1);
+  a.stride_a = a.batch > 1 ? g.stride_a * es : 0;
+  a.stride_b = a.batch > 1 ? g.stride_b * es : 0;
+  a.stride_c = a.batch > 1 ? g.stride_c * out_size(g) : 0;
   (void)k;
   if (geo_out) *geo_out = geo;
   return a;

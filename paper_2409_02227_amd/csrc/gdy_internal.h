@@ -29,6 +29,10 @@ struct KArgs {
   int32_t c_vec;      // 1: C base and rows allow 8-byte stores
   int32_t group_m;    // tile-order swizzle: tile rows per group
   int32_t xcd_remap;  // 1: keep consecutive tiles on one XCD
+  int32_t batch;      // items of a strided batch (>= 1); the extents above are per item
+  int64_t stride_a;   // bytes between consecutive items of A, B and C
+  int64_t stride_b;
+  int64_t stride_c;
 };
 
 // One kernel dispatch: up to kMaxFused GEMMs that use the same kernel share

@@ -439,16 +439,25 @@ go_gemm(KLaunch L) {
   const int ntiles = p.tiles_m * p.tiles_n;
   const int K = (int)p.k;
   const int nk = (K + C::BK - 1) / C::BK;
-  const Rsrc ra = make_rsrc(p.a, p.a_bytes);
-  const Rsrc rb = make_rsrc(p.b, p.b_bytes);
-  const Rsrc rc = make_rsrc(p.c, p.c_bytes);
+  Rsrc ra = make_rsrc(p.a, p.a_bytes);
+  Rsrc rb = make_rsrc(p.b, p.b_bytes);
+  Rsrc rc = make_rsrc(p.c, p.c_bytes);
   const int lda_b = (int)p.lda * C::ES;
   const int ldb_b = (int)p.ldb * C::ES;
   constexpr int OS = OutSize<DT>::v;
   const int ldc_b = (int)p.ldc * OS;
   const int Mrows = (int)p.m, Ncols = (int)p.n;
 
-  for (int t = (int)blockIdx.x - wg0; t < ntiles; t += nwg) {
+  const int total = ntiles * p.batch;  // tiles of every item of a strided batch
+  for (int tb = (int)blockIdx.x - wg0; tb < total; tb += nwg) {
+    int t = tb;
+    if (p.batch > 1) {  // item-major: the item's operands get buffer resources of their own
+      const int item = tb / ntiles;
+      t = tb - item * ntiles;
+      ra = make_rsrc(p.a + item * p.stride_a, p.a_bytes);
+      rb = make_rsrc(p.b + item * p.stride_b, p.b_bytes);
+      rc = make_rsrc(p.c + item * p.stride_c, p.c_bytes);
+    }
     int tm, tn;
     tile_coords(t, p, tm, tn);
     const int m0 = tm * BM;

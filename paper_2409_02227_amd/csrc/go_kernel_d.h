@@ -285,9 +285,9 @@ go_gemm_d(KLaunch L) {
   const int wn = wave % WN;
   const int ntiles = p.tiles_m * p.tiles_n;
   const int nk = (int)p.k / C::BK;  // host guarantees K % BK == 0
-  const sdesc ra = make_sdesc(p.a, p.a_bytes);
-  const sdesc rb = make_sdesc(p.b, p.b_bytes);
-  const Rsrc rc = make_rsrc(p.c, p.c_bytes);
+  sdesc ra = make_sdesc(p.a, p.a_bytes);
+  sdesc rb = make_sdesc(p.b, p.b_bytes);
+  Rsrc rc = make_rsrc(p.c, p.c_bytes);
   const int lda_b = (int)p.lda * C::ES;
   const int ldb_b = (int)p.ldb * C::ES;
   const int ldc_b = (int)p.ldc * 2;
@@ -311,7 +311,16 @@ go_gemm_d(KLaunch L) {
       for (int hh = 0; hh < NHH; ++hh) boff[j][hh] = kt_lane<C::ES, BT>(lane, wn * C::WTN + j * 32, hh);
   }
 
-  for (int t = (int)blockIdx.x - wg0; t < ntiles; t += nwg) {
+  const int total = ntiles * p.batch;  // tiles of every item of a strided batch
+  for (int tb = (int)blockIdx.x - wg0; tb < total; tb += nwg) {
+    int t = tb;
+    if (p.batch > 1) {  // item-major: the item's operands get buffer resources of their own
+      const int item = tb / ntiles;
+      t = tb - item * ntiles;
+      ra = make_sdesc(p.a + item * p.stride_a, p.a_bytes);
+      rb = make_sdesc(p.b + item * p.stride_b, p.b_bytes);
+      rc = make_rsrc(p.c + item * p.stride_c, p.c_bytes);
+    }
     int tm, tn;
     tile_coords(t, p, tm, tn);
     const int m0 = tm * BM;

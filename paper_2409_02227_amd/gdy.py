@@ -44,7 +44,10 @@ class GemmDesc(ctypes.Structure):
                 ("b", ctypes.c_void_p), ("ldb", ctypes.c_int64),
                 ("c", ctypes.c_void_p), ("ldc", ctypes.c_int64),
                 ("scale_a", ctypes.c_float), ("scale_b", ctypes.c_float),
-                ("tenant", ctypes.c_int32), ("variant", ctypes.c_int32)]
+                ("tenant", ctypes.c_int32), ("variant", ctypes.c_int32),
+                ("batch", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("stride_a", ctypes.c_int64), ("stride_b", ctypes.c_int64),
+                ("stride_c", ctypes.c_int64)]
 
 
 class Plan(ctypes.Structure):
@@ -144,7 +147,9 @@ class Gemm:
 
     a: M x K (or K x M when trans_a) row-major; b: K x N (or N x K when
     trans_b); c: M x N output.  Strided 2-D views are allowed as long as the
-    last dimension is contiguous (ld = stride(0))."""
+    last dimension is contiguous (ld = stride(0)).  A strided batch
+    (B-GEMM) passes 3-D tensors whose first dimension is the batch: C must
+    be 3-D; A or B may stay 2-D to be shared by every item (stride 0)."""
     a: object
     b: object
     c: object
@@ -157,20 +162,33 @@ class Gemm:
 
     def desc(self) -> GemmDesc:
         a, b, c = self.a, self.b, self.c
-        m, n = c.shape
-        k = a.shape[0] if self.trans_a else a.shape[1]
-        for t in (a, b, c):
+        batch = c.shape[0] if c.dim() == 3 else 0
+        if batch and any(t.dim() == 3 and t.shape[0] != batch for t in (a, b)):
+            raise ValueError("batched operands disagree on the batch size")
+        if not batch and (a.dim() == 3 or b.dim() == 3):
+            raise ValueError("a batched A or B needs a batched C")
+
+        def mat(t):  # the 2-D item view and the item stride in elements
+            if t.dim() == 3:
+                return t[0], t.stride(0)
+            return t, 0
+        (a2, sa), (b2, sb), (c2, sc) = mat(a), mat(b), mat(c)
+        m, n = c2.shape
+        k = a2.shape[0] if self.trans_a else a2.shape[1]
+        for t in (a2, b2, c2):
             if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1):
-                raise ValueError("operands must be 2-D with a contiguous last dimension")
+                raise ValueError("operands must be 2-D (or 3-D batches) with a contiguous last dimension")
         d = GemmDesc()
         d.m, d.n, d.k = m, n, k
         d.a_type, d.b_type, d.c_type = _dtype_code(a), _dtype_code(b), _dtype_code(c)
         d.trans_a, d.trans_b = int(self.trans_a), int(self.trans_b)
-        d.a, d.lda = a.data_ptr(), max(a.stride(0), 1)
-        d.b, d.ldb = b.data_ptr(), max(b.stride(0), 1)
-        d.c, d.ldc = c.data_ptr(), max(c.stride(0), 1)
+        d.a, d.lda = a.data_ptr(), max(a2.stride(0), 1)
+        d.b, d.ldb = b.data_ptr(), max(b2.stride(0), 1)
+        d.c, d.ldc = c.data_ptr(), max(c2.stride(0), 1)
         d.scale_a, d.scale_b = float(self.scale_a), float(self.scale_b)
         d.tenant, d.variant = int(self.tenant), int(self.variant)
+        d.batch = batch
+        d.stride_a, d.stride_b, d.stride_c = sa, sb, sc
         return d
 
 

@@ -52,10 +52,21 @@ class GemmSpec:
     pad_c: int = 0
     tenant: int = 0
     name: str = ""
+    batch: int = 0               # > 0: a strided batch (B-GEMM) of that many items
+    pad_item: int = 0            # extra elements between consecutive A and B items
+
+    @property
+    def items(self) -> int:
+        return max(self.batch, 1)
 
     @property
     def flops(self) -> int:
-        return 2 * self.m * self.n * self.k
+        return 2 * self.m * self.n * self.k * self.items
+
+    def item_stride(self, which: str) -> int:
+        """Elements between consecutive items of an operand (C items are packed)."""
+        r, c = self.stored_shape(which)
+        return r * self.ld(which) + (self.pad_item if which in ("a", "b") else 0)
 
     def stored_shape(self, which: str) -> tuple:
         if which == "a":
@@ -70,7 +81,8 @@ class GemmSpec:
 
     def compulsory_bytes(self) -> int:
         es = ELEM[self.dtype]
-        return (self.m * self.k + self.k * self.n) * es + self.m * self.n * OUT_ELEM[OUT[self.dtype]]
+        return self.items * ((self.m * self.k + self.k * self.n) * es
+                             + self.m * self.n * OUT_ELEM[OUT[self.dtype]])
 
 
 # ---------------------------------------------------------------------------
@@ -120,6 +132,8 @@ def operand_codes(spec: GemmSpec, which: str) -> tuple:
     ld = spec.ld(which)
     rng = np.random.default_rng([spec.seed, {"a": 1, "b": 2}[which]])
     size = r * ld if r > 0 else 0
+    if spec.batch > 0 and size > 0:  # every item, padding between items included
+        size = spec.item_stride(which) * (spec.batch - 1) + size
     if spec.dtype == "fp8":
         codes, s = fp8_scaled(rng, size)
         return codes, s
@@ -226,6 +240,11 @@ def _device_tensor(codes: np.ndarray, dtype: str, rows: int, ld: int, cols: int,
     return full[:, :cols]
 
 
+def _batched(flat, spec: GemmSpec, which: str, rows: int, cols: int):
+    """3-D (batch, rows, cols) view of a flat device buffer of batch items."""
+    return flat.as_strided((spec.batch, rows, cols), (spec.item_stride(which), spec.ld(which), 1))
+
+
 def from_codes(spec: GemmSpec, a_codes: np.ndarray, b_codes: np.ndarray, scale_a: float = 1.0,
                scale_b: float = 1.0, device="cuda") -> Materialized:
     """Device operands from given flat codes in the stored layouts of `spec`
@@ -248,9 +267,19 @@ def materialize(spec: GemmSpec, device="cuda", keep_host=True) -> Materialized:
     br, bc = spec.stored_shape("b")
     a_codes, sa = operand_codes(spec, "a")
     b_codes, sb = operand_codes(spec, "b")
+    odt = getattr(torch, _TORCH_CODE[OUT[spec.dtype]])
+    if spec.batch > 0:
+        tdt = getattr(torch, _TORCH_CODE[spec.dtype])
+        flat_a = torch.from_numpy(a_codes.view(_RAW_VIEW[ELEM[spec.dtype]])).to(device).view(tdt)
+        flat_b = torch.from_numpy(b_codes.view(_RAW_VIEW[ELEM[spec.dtype]])).to(device).view(tdt)
+        a = _batched(flat_a, spec, "a", ar, ac)
+        b = _batched(flat_b, spec, "b", br, bc)
+        cfull = torch.full((spec.batch, spec.m, spec.ld("c")), float("nan"), dtype=odt, device=device)
+        c = cfull[:, :, :spec.n]
+        host = {"a": a_codes, "b": b_codes} if keep_host else {}
+        return Materialized(spec, a, b, c, cfull, sa, sb, host)
     a = _device_tensor(a_codes, spec.dtype, ar, spec.ld("a"), ac, device)
     b = _device_tensor(b_codes, spec.dtype, br, spec.ld("b"), bc, device)
-    odt = getattr(torch, _TORCH_CODE[OUT[spec.dtype]])
     cfull = torch.full((spec.m, spec.ld("c")), float("nan"), dtype=odt, device=device)
     c = cfull[:, :spec.n]
     host = {"a": a_codes, "b": b_codes} if keep_host else {}

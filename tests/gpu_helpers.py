@@ -28,8 +28,15 @@ def decode_out(mat) -> np.ndarray:
 
 
 def check(mat, rng=None, samples=8, label=""):
-    """Compare one materialised GEMM with the oracle; returns worst ratio."""
+    """Compare one materialised GEMM with the oracle (each item of a strided
+    batch against the oracle on that item's operands); returns worst ratio."""
     s = mat.spec
+    if s.batch > 0:
+        worst = 0.0
+        for i in range(s.batch):
+            item = _item(mat, i)
+            worst = max(worst, check(item, rng, samples, f"{label} item {i}"))
+        return worst
     dt = ORC[s.dtype]
     got = decode_out(mat)
     if s.m * s.n * s.k <= FULL_LIMIT:
@@ -55,6 +62,20 @@ def check(mat, rng=None, samples=8, label=""):
         pad = mat.c_full[:, s.n:].float()
         assert torch.isnan(pad).all().item(), f"{label} {s.name}: wrote into C padding"
     return worst
+
+
+def _item(mat, i):
+    """Item i of a batched GEMM as a single-GEMM Materialized (host codes sliced)."""
+    from dataclasses import replace
+    s = mat.spec
+    single = replace(s, batch=0, pad_item=0, name=f"{s.name}[{i}]")
+    host = {}
+    for w in ("a", "b"):
+        r, _ = s.stored_shape(w)
+        off = i * s.item_stride(w)
+        host[w] = mat.host[w][off:off + r * s.ld(w)]
+    return inputs.Materialized(single, mat.a[i], mat.b[i], mat.c[i], mat.c_full[i], mat.scale_a,
+                               mat.scale_b, host)
 
 
 def gemm_of(mat, variant=-1):

@@ -32,8 +32,9 @@ def test_library_loads_and_exports_every_declared_symbol():
 
 
 def test_struct_layouts_match_header():
-    # gdy_gemm: 3 int64, 5 int32, then (ptr, int64) x 3, 2 floats, 2 int32
-    assert ctypes.sizeof(gdy.GemmDesc) == 3 * 8 + 5 * 4 + 4 + 6 * 8 + 2 * 4 + 2 * 4
+    # gdy_gemm: 3 int64, 5 int32, then (ptr, int64) x 3, 2 floats, 2 int32, 2 int32, 3 int64
+    assert ctypes.sizeof(gdy.GemmDesc) == 3 * 8 + 5 * 4 + 4 + 6 * 8 + 2 * 4 + 2 * 4 + 2 * 4 + 3 * 8
+    assert gdy.GemmDesc.batch.offset == 112 and gdy.GemmDesc.stride_a.offset == 120
     assert gdy.GemmDesc.a.offset == 48
     assert ctypes.sizeof(gdy.Plan) == 4 * 4 + 6 * 4 * gdy.MAX_GEMMS + 4 + 4 * gdy.MAX_GEMMS
     assert gdy.Plan.dispatch_of.offset == 4 * 4 + 6 * 4 * gdy.MAX_GEMMS + 4
@@ -48,3 +49,30 @@ def test_status_strings_without_device():
     assert lib.gdy_status_string(3).startswith(b"output aliases")
     assert lib.gdy_last_error(None) == b"null context"
     assert lib.gdy_variant_count(None) == 0
+
+
+def test_binding_layouts_equal_the_c_compilers(tmp_path):
+    """Every field offset and struct size of the ctypes binding equals what
+    a C compiler makes of include/gdy.h."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    structs = {"gdy_gemm": gdy.GemmDesc, "gdy_plan_t": gdy.Plan, "gdy_variant_desc": gdy.VariantDesc}
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "gdy.h"', "int main(void) {"]
+    for cname, py in structs.items():
+        lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
+        for f, _ in py._fields_:
+            lines.append(f'  printf("{cname} {f} %zu\\n", offsetof({cname}, {f}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    got = {(a, b): int(c) for a, b, c in (l.split() for l in out if l)}
+    for cname, py in structs.items():
+        assert got[(cname, "size")] == ctypes.sizeof(py), cname
+        for f, _ in py._fields_:
+            assert got[(cname, f)] == getattr(py, f).offset, (cname, f)

@@ -421,3 +421,88 @@ def test_f32_concurrent_and_selector_modes(ctx):
         _run(ctx, same, mode, cd, [vid] * 4)
         for m, ref in zip(same, iso):
             assert np.array_equal(out_codes(m), ref), f"{mode}: {m.spec.name} differs"
+
+
+# --------------------------------------------------------------------------
+# strided batched GEMMs (B-GEMMs, Sec. 6.7)
+# --------------------------------------------------------------------------
+
+def test_bgemm_every_dtype_layout_and_family(ctx):
+    """Ragged batched GEMMs in every dtype and layout on one staged and one
+    direct kernel, item strides 16-byte aligned (direct path taken) and not
+    (vector loads off, staged kernel bound); each item against the oracle."""
+    for vid, v in _kernels(ctx):
+        if (v["bm"], v["bn"]) != (128, 128) or v["name"].endswith(("_d4_c0",)):
+            continue
+        dt = DT_NAME[v["dtype"]]
+        es = {"fp8": 1, "f32": 4}.get(dt, 2)
+        ta, tb = v["trans_a"], v["trans_b"]
+        m, n, k = 150, 133, 2 * v["bk"]
+        a_cols, b_cols = (m if ta else k), (k if tb else n)
+        for pad_item in (16 // es * 3, 1):
+            spec = GemmSpec(m, n, k, dt, ta, tb, seed=7000 + vid + pad_item, batch=5,
+                            pad_item=pad_item, pad_a=_pad_to(a_cols, 16 // es),
+                            pad_b=_pad_to(b_cols, 16 // es), name=f"{v['name']}_b5p{pad_item}")
+            mat = inputs.materialize(spec)
+            plan = _run(ctx, [mat], "forced", 1, [vid])
+            ran = ctx.variant(plan["variant_of"][0])
+            if v["direct"]:
+                assert ran["direct"] == (pad_item != 1), f"{v['name']} pad {pad_item}: {ran['name']}"
+            check(mat, label=f"bgemm {v['name']} pad {pad_item}")
+
+
+def test_bgemm_items_equal_single_gemms_bitwise(ctx):
+    """Each item of a batch gives the bits of the same GEMM run alone."""
+    vid = ctx.find("bf16_nn_128x128_w2x2_d2_c0")
+    assert vid >= 0
+    spec = GemmSpec(200, 264, 128, "bf16", seed=7100, batch=6, pad_item=64, name="bits")
+    mat = inputs.materialize(spec)
+    _run(ctx, [mat], "forced", 1, [vid])
+    batched = out_codes(mat).copy()
+    from tests.gpu_helpers import _item
+    for i in range(spec.batch):
+        single = _item(mat, i)
+        # copies so that the single GEMM owns its operands
+        alone = inputs.from_codes(single.spec, single.host["a"], single.host["b"])
+        _run(ctx, [alone], "forced", 1, [vid])
+        assert np.array_equal(out_codes(alone), batched[i]), f"item {i} differs"
+
+
+def test_bgemm_heterogeneous_concurrent_modes(ctx):
+    """Four attention-score B-GEMMs of different sequence lengths (Q K^T per
+    head, K stored SL x 64 and used transposed) in every execution mode."""
+    specs = [GemmSpec(sl, sl, 64, "bf16", 0, 1, seed=7200 + sl, batch=8, name=f"attn{sl}")
+             for sl in (128, 200, 384, 512)]
+    mats = [inputs.materialize(s) for s in specs]
+    for mode in ("sequential", "default", "go", "selector"):
+        plan = _run(ctx, mats, mode)
+        assert sorted(plan["order"]) == [0, 1, 2, 3]
+        for m in mats:
+            check(m, label=f"bgemm {mode}")
+
+
+def test_bgemm_shared_operand_and_validation(ctx):
+    """A B operand shared by every item (stride 0); overlapping C items and
+    a negative batch are rejected before anything runs."""
+    batch, m, n, k = 4, 96, 160, 128
+    spec = GemmSpec(m, n, k, "bf16", seed=7300, batch=batch, name="shared")
+    mat = inputs.materialize(spec)
+    b2 = mat.b[0]  # every item uses item 0's B
+    reset_outputs([mat])
+    ctx.execute([gdy.Gemm(mat.a, b2, mat.c)], mode="sequential")
+    torch.cuda.synchronize()
+    from tests.gpu_helpers import _item
+    for i in range(batch):
+        it = _item(mat, i)
+        it.host["b"] = mat.host["b"][:k * n]
+        check(it, label=f"shared B item {i}")
+    d = gdy.Gemm(mat.a, mat.b, mat.c).desc()
+    d.stride_c = m * n - 1  # items of C would overlap
+    with pytest.raises(gdy.GdyError) as e:
+        ctx.execute([d])
+    assert e.value.status == 3
+    d = gdy.Gemm(mat.a, mat.b, mat.c).desc()
+    d.batch = -2
+    with pytest.raises(gdy.GdyError) as e:
+        ctx.execute([d])
+    assert e.value.status == 1

@@ -84,6 +84,8 @@ def test_workgroups_and_waves_hand_values():
     assert math.isclose(sel.n_waves(64, 256, 1), 0.25)
     # a grid cap of 64 CUs at occupancy 2 launches 128 workgroups
     assert sel.n_workgroups(4096, 4096, 128, 128, 64, 2) == 128
+    # a strided batch of 12 attention-score products (256 x 256 x 64), 128 x 128 tiles
+    assert sel.n_workgroups(256, 256, 128, 128, 0, 2, batch=12) == 48
 
 
 def test_nearest_entry_by_log2_distance():
@@ -117,7 +119,8 @@ def _desc(m, n, k, dtype, ta, tb, base, pad=0):
 
 def _as_dict(d):
     return {"m": d.m, "n": d.n, "k": d.k, "a_type": d.a_type, "trans_a": d.trans_a,
-            "trans_b": d.trans_b, "a": d.a, "b": d.b, "lda": d.lda, "ldb": d.ldb}
+            "trans_b": d.trans_b, "a": d.a, "b": d.b, "lda": d.lda, "ldb": d.ldb,
+            "batch": d.batch, "stride_a": d.stride_a, "stride_b": d.stride_b}
 
 
 def _synthetic_table(path, ctx, rng):
@@ -178,7 +181,13 @@ def _random_set(rng, n):
         m = int(rng.integers(1, 5000))
         nn = int(rng.choice([512, 1000, 2048, 4096, 8192]))
         k = int(rng.choice([64, 100, 1024, 3000, 8192]))
-        out.append(_desc(m, nn, k, dtype, ta, tb, (i + 1) << 36, pad=int(rng.choice([0, 0, 3]))))
+        d = _desc(m, nn, k, dtype, ta, tb, (i + 1) << 36, pad=int(rng.choice([0, 0, 3])))
+        if rng.random() < 0.3:  # a strided batch: item strides aligned or not
+            d.batch = int(rng.integers(2, 40))
+            d.stride_a = (d.lda * (k if ta else m)) + int(rng.choice([0, 8, 3]))
+            d.stride_b = (d.ldb * (nn if tb else k)) + int(rng.choice([0, 8, 5]))
+            d.stride_c = d.ldc * m
+        out.append(d)
     return out
 
 
