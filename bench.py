@@ -40,6 +40,8 @@ WORKLOADS = {
     "tp8_layer_share_nt": ("3nt", "the 8 bf16 GEMMs of tp8_layer_share with each weight stored N x K "
                                   "(linear-layer layout) and used transposed"),
     "tp8_layer_share_f32": ("3f32", "the 8 GEMMs of tp8_layer_share in fp32 (full precision)"),
+    "attn_bgemm_4p": ("attn", "4 heterogeneous strided batched bf16 GEMMs: attention scores Q K^T "
+                              "(SL x SL x 64, K transposed) for SL 128/256/384/512, 64 items each"),
 }
 TRAFFIC = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2409_02227_amd", "csrc", f)
@@ -142,13 +144,13 @@ def dominant_kernel(ctx, mats, plan, steps):
     for u, i in enumerate(idx):
         w = ctx.variant(plan["variant_of"][i])
         s = mats[i].spec
-        wg = -(-s.m // w["bm"]) * -(-s.n // w["bn"])
+        wg = -(-s.m // w["bm"]) * -(-s.n // w["bn"]) * s.items
         if w["grid_cap_cus"]:
             wg = min(wg, w["grid_cap_cus"] * max(w["occupancy"], 1))
         grid += -(-wg // 8) * 8 if u + 1 < len(idx) else wg
-    return {"variant": v["name"], "shape": [[s.m, s.n, s.k] for s in specs], "grid": grid,
+    return {"variant": v["name"], "shape": [[s.m, s.n, s.k] + ([s.batch] if s.batch else []) for s in specs], "grid": grid,
             "launches": len(per[d]), "mean_ms": float(np.mean(per[d])),
-            "flops": sum(2 * s.m * s.n * s.k for s in specs),
+            "flops": sum(s.flops for s in specs),
             "bytes": sum(s.compulsory_bytes() for s in specs), "dtype": specs[0].dtype}
 
 
@@ -264,6 +266,8 @@ def main():
         specs = inputs.config3(trans_b=1)
     elif cfg_id == "3f32":
         specs = inputs.config3(dtype="f32")
+    elif cfg_id == "attn":
+        specs = inputs.config_attn()
     else:
         specs = inputs.CONFIGS[cfg_id]()
     mats = [inputs.materialize(s, "cuda:0", keep_host=True) for s in specs]

@@ -209,6 +209,16 @@ def config5(seed: int = 5) -> list:
     return out
 
 
+def config_attn(seed: int = 6, items: int = 64) -> list:
+    """Heterogeneous strided batched GEMMs (B-GEMMs, Sec. 6.7): the attention
+    scores Q K^T of four sequence-length buckets (128, 256, 384, 512 tokens),
+    each a batch of 16 heads x 4 sequences with head dimension 64; K is
+    stored SL x 64 and used transposed.  Activations ~ U[-1, 1]."""
+    u = ("uniform", -1.0, 1.0)
+    return [GemmSpec(sl, sl, 64, "bf16", 0, 1, a_dist=u, b_dist=u, seed=seed * 1000 + sl,
+                     batch=items, name=f"scores_sl{sl}") for sl in (128, 256, 384, 512)]
+
+
 CONFIGS = {1: config1, 2: config2, 3: config3, 5: config5}
 
 

@@ -77,6 +77,10 @@ def shape_set(kind: str) -> list:
         for nm, m, n, k in (("qkv", 512, 4608, 12288), ("out", 512, 12288, 1536),
                             ("up", 512, 6144, 12288), ("down", 512, 12288, 6144)):
             shapes += [("bf16", 0, 1, m, n, k), ("f32", 0, 0, m, n, k)]
+        # strided batched attention GEMMs (Sec. 6.7): scores Q K^T (SL x SL x 64,
+        # K used transposed) and context P V (SL x 64 x SL), 64 items
+        for sl in (128, 256, 512):
+            shapes += [("bf16", 0, 1, sl, sl, 64, 64), ("bf16", 0, 0, sl, 64, sl, 64)]
     seen, out = set(), []
     for s in shapes:
         if s not in seen:
@@ -126,18 +130,20 @@ def gdy_stream_handle(torch):
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
-def operands(torch, dtype, ta, tb, m, n, k, copies, outputs_per_copy):
+def operands(torch, dtype, ta, tb, m, n, k, copies, outputs_per_copy, batch=0):
     """`copies` independent operand sets with random values (timing only);
     each copy gets `outputs_per_copy` distinct C buffers so that repeated
-    runs of one copy are separate GEMMs of the submission."""
+    runs of one copy are separate GEMMs of the submission.  batch > 0: each
+    operand is a strided batch of that many items (a B-GEMM)."""
     tdt = {"bf16": torch.bfloat16, "f16": torch.float16, "fp8": torch.float8_e4m3fn,
            "f32": torch.float32}[dtype]
     odt = {"f16": torch.float16, "f32": torch.float32}.get(dtype, torch.bfloat16)
     out = []
+    lead = (batch,) if batch > 0 else ()
     for _ in range(copies):
-        a = torch.randn((k, m) if ta else (m, k), device="cuda").to(tdt)
-        b = (torch.randn((n, k) if tb else (k, n), device="cuda") * 0.02).to(tdt)
-        cs = [torch.empty((m, n), device="cuda", dtype=odt) for _ in range(outputs_per_copy)]
+        a = torch.randn(lead + ((k, m) if ta else (m, k)), device="cuda").to(tdt)
+        b = (torch.randn(lead + ((n, k) if tb else (k, n)), device="cuda") * 0.02).to(tdt)
+        cs = [torch.empty(lead + (m, n), device="cuda", dtype=odt) for _ in range(outputs_per_copy)]
         out.append((a, b, cs))
     return out
 
@@ -168,12 +174,13 @@ def candidates(variants, code, ta, tb, m):
 
 def tune_shape(ctx, bench, torch, variants, shape, rounds=3):
     """Steps 1 and 2 for one shape; returns a JSON-able record."""
-    dtype, ta, tb, m, n, k = shape
+    dtype, ta, tb, m, n, k = shape[:6]
+    batch = shape[6] if len(shape) > 6 else 0  # B-GEMM items
     code = DT_CODE[dtype]
     cands = candidates(variants, code, ta, tb, m)
     uncapped = [v for v in cands if variants[v]["grid_cap_cus"] == 0]
     by_name = {v["name"]: i for i, v in enumerate(variants)}
-    ops = operands(torch, dtype, ta, tb, m, n, k, 16, rounds)
+    ops = operands(torch, dtype, ta, tb, m, n, k, 16, rounds, batch)
     rec = {"shape": list(shape), "iso": {}, "rc_best": {}, "conc": {}, "seq": {}, "pool": []}
     # step 1: isolated timings on the whole GPU (every variant, grid caps
     # included) and on each CU-masked pool (uncapped tiles)
@@ -248,7 +255,7 @@ def write_table(path, ctx, records, lr=None, lr_by_type=None):
         lines.append(f"lr_dtype {int(code)}")
         lines += _lr_lines(model)
     for r in records:
-        dtype, ta, tb, m, n, k = r["shape"]
+        dtype, ta, tb, m, n, k = r["shape"][:6]
         mlog = max(0, math.ceil(math.log2(max(m, 1))))
         names = [r["go"][str(cd)] for cd in CDS]
         lines.append(f"entry {DT_CODE[dtype]} {ta} {tb} {mlog} {n} {k} " + " ".join(names))
@@ -262,8 +269,11 @@ def feature_rows(ctx, records):
     from paper_2409_02227_amd import gdy
     X, y = [], []
     for r in records:
-        dtype, ta, tb, m, n, k = r["shape"]
+        dtype, ta, tb, m, n, k = r["shape"][:6]
         d = gdy.GemmDesc()
+        if len(r["shape"]) > 6:  # a B-GEMM: its features count every item's workgroups
+            d.batch = r["shape"][6]
+            d.stride_a, d.stride_b, d.stride_c = m * k, k * n, m * n
         d.m, d.n, d.k = m, n, k
         d.a_type = d.b_type = DT_CODE[dtype]
         d.c_type = {"f16": 1, "f32": 4}.get(dtype, 2)
