@@ -100,7 +100,15 @@ typedef enum {
  */
 #define GDY_MAX_FUSED 16
 
-/* One GEMM of a submission. */
+/* What an entry of a submission computes.  GDY_OP_ADD is the non-GEMM
+ * co-runner of Sec. 7.1: C[i][j] = A[i][j] + B[i][j] over an M x N region
+ * (A and B M x N with lda, ldb >= N; k must be 0; trans flags 0; a_type ==
+ * b_type == c_type in {F16, BF16, F32}; the sum is formed in fp32 and
+ * rounded once).  The selector lets an add join any group (it restricts
+ * no concurrency); the GEMMs' predicted degrees decide whether it co-runs. */
+typedef enum { GDY_OP_GEMM = 0, GDY_OP_ADD = 1 } gdy_op;
+
+/* One GEMM (or element-wise add) of a submission. */
 typedef struct {
   int64_t m, n, k;                  /* sizes; m or n == 0 is a no-op, k == 0 writes zeros   */
   int32_t a_type, b_type, c_type;   /* gdy_dtype values                                     */
@@ -118,7 +126,7 @@ typedef struct {
    * items may (stride 0 broadcasts one operand).  Every item obeys the
    * single-GEMM extent limits. */
   int32_t batch;
-  int32_t reserved;                 /* must be 0                                            */
+  int32_t op;                       /* gdy_op: what this entry computes (0: a GEMM)         */
   int64_t stride_a, stride_b, stride_c;
 } gdy_gemm;
 
@@ -153,6 +161,8 @@ typedef struct {
   int32_t direct;           /* 1: global->LDS copies; needs K % bk == 0 and 16-byte
                                aligned A/B bases and row pitches, else the staged
                                variant of the same tile and cap runs instead     */
+  int32_t kind;             /* 0: a GEMM kernel; 1: the element-wise add (GDY_OP_ADD),
+                               bm x bn is then its workgroup tile of elements    */
 } gdy_variant_desc;
 
 typedef struct gdy_ctx gdy_ctx;

@@ -136,6 +136,21 @@ def gemm_entries(m, n, k, a, a_type, lda, b, b_type, ldb, rows, cols,
     return ref, bound
 
 
+def add(m, n, a, a_type, lda, b, b_type, ldb):
+    """Element-wise A + B over an M x N region (the non-GEMM co-runner of
+    Sec. 7.1), in fp64 on the decoded operands; returns (ref, bound) with
+    bound = |a| + |b|, the scale a correctly rounded result is judged on."""
+    a = _as_codes(a, a_type).reshape(-1)
+    b = _as_codes(b, b_type).reshape(-1)
+    _check_extent(m, n, lda, 0, a.size, "A")
+    _check_extent(m, n, ldb, 0, b.size, "B")
+    rows = np.arange(m)[:, None]
+    cols = np.arange(n)[None, :]
+    va = decode(a[rows * lda + cols], a_type)
+    vb = decode(b[rows * ldb + cols], b_type)
+    return va + vb, np.abs(va) + np.abs(vb)
+
+
 def _check_extent(rows, cols, ld, trans, size, name):
     """The flat buffer must hold every element op() touches."""
     if rows == 0 or cols == 0:

@@ -127,6 +127,14 @@ def direct_ok(v: dict, g: dict) -> bool:
             and (g["lda"] * es) % 16 == 0 and (g["ldb"] * es) % 16 == 0 and items)
 
 
+def add_variant(g: dict, variants: list) -> int:
+    """An element-wise add (the non-GEMM of Sec. 7.1) runs the add kernel of its type."""
+    for w, u in enumerate(variants):
+        if u.get("kind", 0) == 1 and u["dtype"] == g["a_type"]:
+            return w
+    raise LookupError("no add kernel for this type")
+
+
 def runnable(vid: int, g: dict, variants: list) -> int:
     """The variant that runs: a direct one the GEMM cannot take is replaced
     by the staged variant of the same dtype, layout, tile and cap."""
@@ -134,7 +142,8 @@ def runnable(vid: int, g: dict, variants: list) -> int:
     if direct_ok(v, g):
         return vid
     for w, u in enumerate(variants):
-        if (not u["direct"] and u["dtype"] == v["dtype"] and u["trans_a"] == v["trans_a"]
+        if (not u["direct"] and u.get("kind", 0) == 0 and u["dtype"] == v["dtype"]
+                and u["trans_a"] == v["trans_a"]
                 and u["trans_b"] == v["trans_b"] and u["bm"] == v["bm"] and u["bn"] == v["bn"]
                 and u["grid_cap_cus"] == v["grid_cap_cus"]):
             return w
@@ -156,6 +165,8 @@ def nearest_entry(entries: list, g: dict):
 
 
 def bind(g: dict, class_index: int, table: dict, variants: list, by_name: dict) -> int:
+    if g.get("op", 0) == 1:
+        return add_variant(g, variants)
     e = nearest_entry(table["entries"], g)
     if e is None:
         raise LookupError("no tuned shape for this dtype/layout")
@@ -276,6 +287,9 @@ def plan_selector(gemms: list, table: dict, variants: list, cus: int, slots: int
             out["groups"], out["variant_of"], variants, slots)
         return out
     for i in live:
+        if gemms[i].get("op", 0) == 1:  # a non-GEMM restricts no group (Sec. 7.1)
+            out["pred_cd"][i] = clamp(CD_CLASSES[-1], n)
+            continue
         lr = predictor_for(table, gemms[i]["a_type"])
         if lr is None:
             out["pred_cd"][i] = clamp(1, n)

@@ -15,7 +15,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libgdy.so")
 
 SOURCES = ["kernels_d_bf16.hip", "kernels_d_f16.hip", "kernels_d_fp8.hip",
-           "kernels_bf16.hip", "kernels_f16.hip", "kernels_fp8.hip", "kernels_f32.hip", "gdy.cpp"]
+           "kernels_bf16.hip", "kernels_f16.hip", "kernels_fp8.hip", "kernels_f32.hip", "kernels_ew.hip", "gdy.cpp"]
 ARCH = "gfx950"
 # -packed-fp32-ops: keep hipcc from forming packed fp32 ALU ops by itself.
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

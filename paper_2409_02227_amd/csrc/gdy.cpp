@@ -168,6 +168,7 @@ Geometry geometry(const gdy_ctx* ctx, int vid, const gdy_gemm& g) {
 bool variant_fits(const gdy_ctx* ctx, int vid, const gdy_gemm& g) {
   if (vid < 0 || vid >= (int)ctx->variants.size()) return false;
   const KernelDesc* d = ctx->kernels[ctx->variants[vid].kernel].d;
+  if ((d->ew != 0) != (g.op == GDY_OP_ADD)) return false;  // GEMM kernels for GEMMs, the add for adds
   return d->dtype == g.a_type && d->ta == g.trans_a && d->tb == g.trans_b;
 }
 
@@ -217,7 +218,7 @@ int heuristic_variant(const gdy_ctx* ctx, const gdy_gemm& g) {
 // log2 space, then the variant stored for CD class ci.
 int nearest_entry(const gdy_ctx* ctx, const gdy_gemm& g) {
   const Table& t = ctx->table;
-  if (!t.loaded || g.a_type < 1 || g.a_type > 4) return -1;
+  if (!t.loaded || g.op != GDY_OP_GEMM || g.a_type < 1 || g.a_type > 4) return -1;
   const int mlog = ceil_log2(std::max<int64_t>(g.m, 1));
   const double ln = std::log2((double)std::max<int64_t>(g.n, 1));
   const double lk = std::log2((double)std::max<int64_t>(g.k, 1));
@@ -237,6 +238,7 @@ int nearest_entry(const gdy_ctx* ctx, const gdy_gemm& g) {
 // Variant for CD class ci given the GEMM's nearest tuned entry (-1: none,
 // then the isolated heuristics).
 int bind_entry(const gdy_ctx* ctx, const gdy_gemm& g, int entry, int ci, bool* fallback) {
+  if (g.op == GDY_OP_ADD) return heuristic_variant(ctx, g);  // the add kernel of its type
   if (entry >= 0) return runnable(ctx, ctx->table.entries[entry].v[ci], g);
   if (fallback) *fallback = true;
   return heuristic_variant(ctx, g);
@@ -320,11 +322,48 @@ bool stored_extent(int64_t rows, int64_t cols, int64_t ld, int es, int64_t* byte
   return (rows + 256) * ld * es + 1024 < (int64_t)INT32_MAX;
 }
 
+// The element-wise add: A, B and C are M x N regions of one type.
+gdy_status validate_add(gdy_ctx* ctx, const gdy_gemm& g, int i, Extent* ea, Extent* eb, Extent* ec) {
+  const bool t = g.a_type == g.b_type && g.a_type == g.c_type &&
+                 (g.a_type == GDY_F16 || g.a_type == GDY_BF16 || g.a_type == GDY_F32);
+  if (!t) return fail(ctx, GDY_ERR_UNSUPPORTED, "add %d: unsupported type triple (%d,%d,%d)", i,
+                      g.a_type, g.b_type, g.c_type);
+  if (g.k != 0 || g.trans_a || g.trans_b || g.scale_a != 1.0f || g.scale_b != 1.0f)
+    return fail(ctx, GDY_ERR_INVALID_ARG, "add %d: k, trans flags and scales must be 0, 0, 1", i);
+  if (g.m == 0 || g.n == 0) return GDY_OK;
+  const int es = elem_size(g.a_type);
+  const int64_t nb = std::max(g.batch, 1);
+  if (!g.a || !g.b || !g.c) return fail(ctx, GDY_ERR_INVALID_ARG, "add %d: null operand", i);
+  if (g.lda < g.n || g.ldb < g.n || g.ldc < g.n)
+    return fail(ctx, GDY_ERR_INVALID_ARG, "add %d: leading dimension < n", i);
+  if ((((uintptr_t)g.a | (uintptr_t)g.b | (uintptr_t)g.c) % es))
+    return fail(ctx, GDY_ERR_UNSUPPORTED, "add %d: operands not element aligned", i);
+  int64_t ab, bb, cb;
+  if (!stored_extent(g.m, g.n, g.lda, es, &ab) || !stored_extent(g.m, g.n, g.ldb, es, &bb) ||
+      !stored_extent(g.m, g.n, g.ldc, es, &cb))
+    return fail(ctx, GDY_ERR_UNSUPPORTED, "add %d: extent too large", i);
+  if (nb > 1 && g.stride_c * es < cb)
+    return fail(ctx, GDY_ERR_ALIAS, "add %d: batch items of C overlap (stride_c too small)", i);
+  ea->lo = (uintptr_t)g.a;
+  ea->hi = ea->lo + (uintptr_t)((nb - 1) * g.stride_a * es + ab);
+  eb->lo = (uintptr_t)g.b;
+  eb->hi = eb->lo + (uintptr_t)((nb - 1) * g.stride_b * es + bb);
+  ec->lo = (uintptr_t)g.c;
+  ec->hi = ec->lo + (uintptr_t)((nb - 1) * g.stride_c * es + cb);
+  return GDY_OK;
+}
+
 gdy_status validate_one(gdy_ctx* ctx, const gdy_gemm& g, int i, Extent* ea, Extent* eb,
                         Extent* ec) {
   *ea = *eb = *ec = Extent{0, 0};
   if (g.m < 0 || g.n < 0 || g.k < 0)
     return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: negative size", i);
+  if (g.op != GDY_OP_GEMM && g.op != GDY_OP_ADD)
+    return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: unknown op %d", i, g.op);
+  if (g.batch < 0) return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: negative batch", i);
+  if (g.batch > 1 && (g.stride_a < 0 || g.stride_b < 0 || g.stride_c < 0))
+    return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: negative batch stride", i);
+  if (g.op == GDY_OP_ADD) return validate_add(ctx, g, i, ea, eb, ec);
   const bool t16 = (g.a_type == GDY_F16 && g.b_type == GDY_F16 && g.c_type == GDY_F16) ||
                    (g.a_type == GDY_BF16 && g.b_type == GDY_BF16 && g.c_type == GDY_BF16);
   const bool t8 = g.a_type == GDY_FP8_E4M3 && g.b_type == GDY_FP8_E4M3 && g.c_type == GDY_BF16;
@@ -334,11 +373,7 @@ gdy_status validate_one(gdy_ctx* ctx, const gdy_gemm& g, int i, Extent* ea, Exte
                 g.a_type, g.b_type, g.c_type);
   if ((g.trans_a != 0 && g.trans_a != 1) || (g.trans_b != 0 && g.trans_b != 1))
     return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: trans flags must be 0 or 1", i);
-  if (g.batch < 0 || g.reserved != 0)
-    return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: negative batch or nonzero reserved field", i);
   const int64_t nb = std::max(g.batch, 1);
-  if (nb > 1 && (g.stride_a < 0 || g.stride_b < 0 || g.stride_c < 0))
-    return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: negative batch stride", i);
   if (!std::isfinite(g.scale_a) || !std::isfinite(g.scale_b))
     return fail(ctx, GDY_ERR_INVALID_ARG, "gemm %d: non-finite scale", i);
   if ((t16 || t32) && (g.scale_a != 1.0f || g.scale_b != 1.0f))
@@ -547,7 +582,9 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
     entry[i] = nearest_entry(ctx, g[i]);
     int cd = 1;
     const Predictor* lr = ctx->table.loaded ? ctx->table.for_type(g[i].a_type) : nullptr;
-    if (lr) {
+    if (g[i].op == GDY_OP_ADD) {
+      cd = kCD[GDY_N_CD - 1];  // a non-GEMM restricts no group: the GEMMs' degrees decide (Sec. 7.1)
+    } else if (lr) {
       double x[GDY_N_FEATURES];
       features(ctx, g[i], entry[i], x);
       cd = predict_cd(*lr, x);
@@ -658,7 +695,11 @@ KArgs make_args(const gdy_ctx* ctx, int vid, const gdy_gemm& g, Geometry* geo_ou
   a.ldc = g.ldc;
   a.scale = g.scale_a * g.scale_b;  // one fp32 rounding
   int64_t ab = 0, bb = 0, cb = 0;
-  if (g.k > 0) {
+  const bool add = g.op == GDY_OP_ADD;
+  if (add) {  // the element-wise add reads M x N regions of A and B
+    stored_extent(g.m, g.n, g.lda, es, &ab);
+    stored_extent(g.m, g.n, g.ldb, es, &bb);
+  } else if (g.k > 0) {
     if (g.trans_a) stored_extent(g.k, g.m, g.lda, es, &ab); else stored_extent(g.m, g.k, g.lda, es, &ab);
     if (g.trans_b) stored_extent(g.n, g.k, g.ldb, es, &bb); else stored_extent(g.k, g.n, g.ldb, es, &bb);
   }
@@ -669,8 +710,8 @@ KArgs make_args(const gdy_ctx* ctx, int vid, const gdy_gemm& g, Geometry* geo_ou
   a.tiles_m = geo.tiles_m;
   a.tiles_n = geo.tiles_n;
   const bool batched = g.batch > 1;
-  a.a_vec = g.k > 0 && vec_ok(g.a, g.lda, es, g.trans_a == 0, batched ? g.stride_a * es : 0);
-  a.b_vec = g.k > 0 && vec_ok(g.b, g.ldb, es, g.trans_b == 1, batched ? g.stride_b * es : 0);
+  a.a_vec = (g.k > 0 || add) && vec_ok(g.a, g.lda, es, g.trans_a == 0, batched ? g.stride_a * es : 0);
+  a.b_vec = (g.k > 0 || add) && vec_ok(g.b, g.ldb, es, add || g.trans_b == 1, batched ? g.stride_b * es : 0);
   a.c_vec = (uintptr_t)g.c % 8 == 0 && (g.ldc * out_size(g)) % 8 == 0 &&
             (!batched || (g.stride_c * out_size(g)) % 8 == 0);
   a.group_m = 8;
@@ -855,7 +896,7 @@ gdy_status load_table(gdy_ctx* ctx, const char* path) {
           if (ctx->variants[v].name == name) vid = (int)v;
         if (vid < 0) return fail(ctx, GDY_ERR_TABLE, "GO table names unknown variant %s", name.c_str());
         const KernelDesc* d = ctx->kernels[ctx->variants[vid].kernel].d;
-        if (d->dtype != e.dtype || d->ta != e.ta || d->tb != e.tb)
+        if (d->ew || d->dtype != e.dtype || d->ta != e.ta || d->tb != e.tb)
           return fail(ctx, GDY_ERR_TABLE, "variant %s does not match its entry", name.c_str());
         e.v[c] = vid;
       }
@@ -948,7 +989,7 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
     ctx->arch = ctx->arch.substr(0, ctx->arch.find(':'));
   }
 
-  const int kTables = 7;
+  const int kTables = 8;
   const KernelDesc* tabs[kTables];
   int counts[kTables];
   counts[0] = kernels_bf16(&tabs[0]);
@@ -958,6 +999,7 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
   counts[4] = kernels_d_f16(&tabs[4]);
   counts[5] = kernels_d_fp8(&tabs[5]);
   counts[6] = kernels_f32(&tabs[6]);
+  counts[7] = kernels_ew(&tabs[7]);
   uint64_t h = 1469598103934665603ull;
   for (int t = 0; t < kTables; ++t) {
     for (int i = 0; i < counts[t]; ++i) {
@@ -977,6 +1019,7 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
       const int kid = (int)ctx->kernels.size();
       ctx->kernels.push_back(k);
       for (int c = 0; c < kNumCaps; ++c) {
+        if (k.d->ew && kCaps[c] != 0) continue;  // the element-wise add has no grid caps
         Variant v;
         v.kernel = kid;
         v.cap = kCaps[c];
@@ -994,7 +1037,7 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
     if (!d->direct) continue;
     for (size_t w = 0; w < ctx->variants.size(); ++w) {
       const KernelDesc* e = ctx->kernels[ctx->variants[w].kernel].d;
-      if (!e->direct && e->dtype == d->dtype && e->ta == d->ta && e->tb == d->tb && e->bm == d->bm &&
+      if (!e->direct && !e->ew && e->dtype == d->dtype && e->ta == d->ta && e->tb == d->tb && e->bm == d->bm &&
           e->bn == d->bn && ctx->variants[w].cap == v.cap) {
         v.staged = (int)w;
         break;
@@ -1158,6 +1201,7 @@ gdy_status gdy_features(gdy_ctx* ctx, const gdy_gemm* gemm, double* out_features
   if (!ctx || !gemm || !out_features) return GDY_ERR_INVALID_ARG;
   gdy_status s = validate(ctx, gemm, 1, GDY_SELECTOR);
   if (s != GDY_OK) return s;
+  if (gemm->op != GDY_OP_GEMM) return fail(ctx, GDY_ERR_INVALID_ARG, "features are defined for GEMMs only");
   features(ctx, *gemm, nearest_entry(ctx, *gemm), out_features);
   return GDY_OK;
 }
@@ -1183,6 +1227,7 @@ gdy_status gdy_variant_info(gdy_ctx* ctx, int32_t id, gdy_variant_desc* out) {
   out->occupancy = k.occupancy;
   out->grid_cap_cus = v.cap;
   out->direct = k.d->direct;
+  out->kind = k.d->ew ? 1 : 0;
   return GDY_OK;
 }
 

@@ -59,6 +59,7 @@ struct KernelDesc {
   int lds_bytes;      // static LDS per workgroup
   const void* func;   // __global__ entry, launched with hipExtLaunchKernel
   int direct;         // 1: global->LDS copies; needs K % bk == 0 and 16-byte alignment
+  int ew;             // 1: the element-wise add (a non-GEMM op), not a GEMM kernel
 };
 
 // Each instantiation unit exports its table.
@@ -66,6 +67,7 @@ int kernels_bf16(const KernelDesc** out);
 int kernels_f16(const KernelDesc** out);
 int kernels_fp8(const KernelDesc** out);
 int kernels_f32(const KernelDesc** out);
+int kernels_ew(const KernelDesc** out);
 int kernels_d_bf16(const KernelDesc** out);
 int kernels_d_f16(const KernelDesc** out);
 int kernels_d_fp8(const KernelDesc** out);

@@ -23,6 +23,7 @@ CD_CLASSES = (1, 2, 4, 8, 16)
 F16, BF16, FP8_E4M3, F32 = 1, 2, 3, 4
 # gdy_mode
 SEQUENTIAL, DEFAULT, GO, SELECTOR, FORCED, FORCED_GROUPED = 0, 1, 2, 3, 4, 5
+GEMM, ADD = 0, 1  # gdy_op
 MODES = {"sequential": SEQUENTIAL, "default": DEFAULT, "go": GO,
          "selector": SELECTOR, "forced": FORCED, "forced_grouped": FORCED_GROUPED}
 
@@ -45,7 +46,7 @@ class GemmDesc(ctypes.Structure):
                 ("c", ctypes.c_void_p), ("ldc", ctypes.c_int64),
                 ("scale_a", ctypes.c_float), ("scale_b", ctypes.c_float),
                 ("tenant", ctypes.c_int32), ("variant", ctypes.c_int32),
-                ("batch", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("batch", ctypes.c_int32), ("op", ctypes.c_int32),
                 ("stride_a", ctypes.c_int64), ("stride_b", ctypes.c_int64),
                 ("stride_c", ctypes.c_int64)]
 
@@ -74,7 +75,7 @@ class VariantDesc(ctypes.Structure):
                 ("bk", ctypes.c_int32), ("waves", ctypes.c_int32), ("mfma", ctypes.c_int32),
                 ("lds_bytes", ctypes.c_int32), ("vgprs", ctypes.c_int32),
                 ("occupancy", ctypes.c_int32), ("grid_cap_cus", ctypes.c_int32),
-                ("direct", ctypes.c_int32)]
+                ("direct", ctypes.c_int32), ("kind", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
         d = {f: getattr(self, f) for f, _ in self._fields_}
@@ -139,6 +140,40 @@ def _dtype_code(t) -> int:
         _TORCH_DTYPE = {torch.float16: F16, torch.bfloat16: BF16, torch.float8_e4m3fn: FP8_E4M3,
                         torch.uint8: FP8_E4M3, torch.float32: F32}
     return _TORCH_DTYPE[t.dtype]
+
+
+@dataclass
+class Add:
+    """Element-wise C = A + B over an M x N region: the non-GEMM that co-runs
+    with GEMMs (Sec. 7.1).  2-D tensors of one type (bf16, fp16, fp32), or
+    3-D strided batches; the last dimension contiguous."""
+    a: object
+    b: object
+    c: object
+    tenant: int = 0
+    variant: int = -1
+
+    def desc(self) -> GemmDesc:
+        a, b, c = self.a, self.b, self.c
+        batch = c.shape[0] if c.dim() == 3 else 0
+
+        def mat(t):
+            return (t[0], t.stride(0)) if t.dim() == 3 else (t, 0)
+        (a2, sa), (b2, sb), (c2, sc) = mat(a), mat(b), mat(c)
+        m, n = c2.shape
+        if tuple(a2.shape) != (m, n) or tuple(b2.shape) != (m, n):
+            raise ValueError("add operands must have C's shape")
+        d = GemmDesc()
+        d.m, d.n, d.k = m, n, 0
+        d.a_type, d.b_type, d.c_type = _dtype_code(a), _dtype_code(b), _dtype_code(c)
+        d.a, d.lda = a.data_ptr(), max(a2.stride(0), 1)
+        d.b, d.ldb = b.data_ptr(), max(b2.stride(0), 1)
+        d.c, d.ldc = c.data_ptr(), max(c2.stride(0), 1)
+        d.scale_a = d.scale_b = 1.0
+        d.tenant, d.variant = int(self.tenant), int(self.variant)
+        d.batch, d.op = batch, ADD
+        d.stride_a, d.stride_b, d.stride_c = sa, sb, sc
+        return d
 
 
 @dataclass

@@ -219,6 +219,46 @@ def config_attn(seed: int = 6, items: int = 64) -> list:
                      batch=items, name=f"scores_sl{sl}") for sl in (128, 256, 384, 512)]
 
 
+@dataclass
+class AddInputs:
+    """Operands of one element-wise add C = A + B over M x N (Sec. 7.1)."""
+    m: int
+    n: int
+    dtype: str
+    ld: int
+    a: object
+    b: object
+    c: object
+    c_full: object
+    host: dict
+
+
+def materialize_add(m: int, n: int, dtype: str = "bf16", seed: int = 0, pad: int = 0,
+                    device="cuda") -> AddInputs:
+    """A, B ~ U[-1, 1] of the given type with leading dimension n + pad;
+    C (same type) prefilled with NaN, its padding columns included."""
+    import torch
+    ld = n + pad
+    rng = np.random.default_rng([seed, 7])
+    u = ("uniform", -1.0, 1.0)
+    a_codes = encode(_draw(rng, u, m * ld), dtype)
+    b_codes = encode(_draw(rng, u, m * ld), dtype)
+    a = _device_tensor(a_codes, dtype, m, ld, n, device)
+    b = _device_tensor(b_codes, dtype, m, ld, n, device)
+    cfull = torch.full((m, ld), float("nan"), dtype=getattr(torch, _TORCH_CODE[dtype]), device=device)
+    return AddInputs(m, n, dtype, ld, a, b, cfull[:, :n], cfull, {"a": a_codes, "b": b_codes})
+
+
+def gemm_add_pairs(seed: int = 7) -> list:
+    """GEMM + non-GEMM co-runs (Sec. 7.1): each bf16 GEMM paired with an
+    element-wise add sized like its output; memory-bound GEMMs (small N and
+    K) and compute-bound ones."""
+    shapes = ((4096, 1024, 1024), (8192, 1024, 512), (16384, 512, 512), (2048, 2048, 2048),
+              (4096, 4096, 1024), (1024, 4096, 4096), (512, 8192, 8192), (2048, 8192, 2048))
+    return [(GemmSpec(m, n, k, "bf16", seed=seed * 1000 + i, name=f"pair{i}"), (m, n))
+            for i, (m, n, k) in enumerate(shapes)]
+
+
 CONFIGS = {1: config1, 2: config2, 3: config3, 5: config5}
 
 

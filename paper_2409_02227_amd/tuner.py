@@ -164,11 +164,12 @@ def candidates(variants, code, ta, tb, m):
     """Catalogue variants for this dtype/layout, without tiles more than 4x
     taller than M (they only burn MFMA work on padding)."""
     mp2 = 1 << max(0, math.ceil(math.log2(max(m, 1))))
-    out = [i for i, v in enumerate(variants)
-           if v["dtype"] == code and v["trans_a"] == ta and v["trans_b"] == tb and v["bm"] <= 4 * mp2]
+    gemm = [i for i, v in enumerate(variants) if v.get("kind", 0) == 0]  # not the element-wise add
+    out = [i for i in gemm if variants[i]["dtype"] == code and variants[i]["trans_a"] == ta
+           and variants[i]["trans_b"] == tb and variants[i]["bm"] <= 4 * mp2]
     if not out:
-        out = [i for i, v in enumerate(variants)
-               if v["dtype"] == code and v["trans_a"] == ta and v["trans_b"] == tb]
+        out = [i for i in gemm if variants[i]["dtype"] == code and variants[i]["trans_a"] == ta
+               and variants[i]["trans_b"] == tb]
     return out
 
 

@@ -11,6 +11,8 @@ from paper_2409_02227_amd import inputs
 
 TAU = {"bf16": 2.0 ** -7, "f16": 2.0 ** -7, "fp8": 2.0 ** -3, "f32": 2.0 ** -10}
 ORC = {"bf16": "bf16", "f16": "f16", "fp8": "e4m3fn", "f32": "f32"}
+# element-wise add: half an ulp of the output type, relative to |a| + |b|
+TAU_ADD = {"bf16": 2.0 ** -8, "f16": 2.0 ** -11, "f32": 2.0 ** -24}
 FULL_LIMIT = 3e8  # multiply-adds the oracle does in full; above: sampled
 
 
@@ -87,3 +89,19 @@ def gemm_of(mat, variant=-1):
 def reset_outputs(mats):
     for m in mats:
         m.c_full.fill_(float("nan"))
+
+
+def check_add(x, label=""):
+    """An element-wise add (inputs.AddInputs) against the oracle: within half
+    an output ulp of the exact sum, measured on |a| + |b|; C's padding columns
+    untouched."""
+    ref, bound = oracle.add(x.m, x.n, x.host["a"], ORC[x.dtype], x.ld, x.host["b"], ORC[x.dtype], x.ld)
+    c = x.c.cpu().contiguous()
+    codes = c.view(torch.int32).numpy().view(np.uint32) if c.dtype == torch.float32 else \
+        c.view(torch.int16).numpy().view(np.uint16)
+    got = oracle.decode(codes, ORC[x.dtype])
+    ok, worst = oracle.accept(got, ref, bound, TAU_ADD[x.dtype], abs_term=1e-30)
+    assert ok, f"{label} add ({x.m},{x.n},{x.dtype}): outside bound, worst ratio {worst:.3g}"
+    if x.ld > x.n:
+        assert torch.isnan(x.c_full[:, x.n:].float()).all().item(), f"{label}: wrote into C padding"
+    return worst

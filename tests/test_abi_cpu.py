@@ -38,7 +38,7 @@ def test_struct_layouts_match_header():
     assert gdy.GemmDesc.a.offset == 48
     assert ctypes.sizeof(gdy.Plan) == 4 * 4 + 6 * 4 * gdy.MAX_GEMMS + 4 + 4 * gdy.MAX_GEMMS
     assert gdy.Plan.dispatch_of.offset == 4 * 4 + 6 * 4 * gdy.MAX_GEMMS + 4
-    assert ctypes.sizeof(gdy.VariantDesc) == 64 + 13 * 4
+    assert ctypes.sizeof(gdy.VariantDesc) == 64 + 14 * 4
     text = open(HEADER).read()
     assert "#define GDY_MAX_GEMMS 256" in text and "#define GDY_N_FEATURES 18" in text
 

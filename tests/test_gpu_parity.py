@@ -43,8 +43,8 @@ def _run(ctx, mats, mode, forced_cd=0, variants=None):
 
 
 def _kernels(ctx):
-    """Uncapped variant of every kernel in the catalogue."""
-    return [(i, v) for i, v in enumerate(ctx.variants()) if v["grid_cap_cus"] == 0]
+    """Uncapped variant of every GEMM kernel in the catalogue."""
+    return [(i, v) for i, v in enumerate(ctx.variants()) if v["grid_cap_cus"] == 0 and v["kind"] == 0]
 
 
 def test_every_kernel_ragged_tiles(ctx):
@@ -99,7 +99,7 @@ def test_grid_caps_are_bit_identical(ctx):
     mat = inputs.materialize(spec)
     by_kernel = {}
     for vid, v in enumerate(ctx.variants()):
-        if v["dtype"] == 2 and v["trans_a"] == 0 and v["trans_b"] == 0:
+        if v["dtype"] == 2 and v["trans_a"] == 0 and v["trans_b"] == 0 and v["kind"] == 0:
             by_kernel.setdefault(v["name"].rsplit("_c", 1)[0], []).append(vid)
     for name, vids in by_kernel.items():
         ref = None
@@ -503,6 +503,66 @@ def test_bgemm_shared_operand_and_validation(ctx):
     assert e.value.status == 3
     d = gdy.Gemm(mat.a, mat.b, mat.c).desc()
     d.batch = -2
+    with pytest.raises(gdy.GdyError) as e:
+        ctx.execute([d])
+    assert e.value.status == 1
+
+
+# --------------------------------------------------------------------------
+# GEMM + non-GEMM co-runs (Sec. 7.1): the element-wise add
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dt", ["bf16", "f16", "f32"])
+def test_add_every_type_and_edge(ctx, dt):
+    """Element-wise adds of every supported type: one element, ragged rows
+    and columns with padded leading dimensions (element-wise loads), and
+    aligned ones (vector loads)."""
+    from tests.gpu_helpers import check_add
+    for i, (m, n, pad) in enumerate(((1, 1, 0), (37, 300, 3), (64, 4096, 0), (257, 1030, 8))):
+        x = inputs.materialize_add(m, n, dt, seed=8000 + i, pad=pad)
+        ctx.execute([gdy.Add(x.a, x.b, x.c)], mode="sequential")
+        torch.cuda.synchronize()
+        check_add(x, label=f"{dt} {m}x{n}+{pad}")
+
+
+def test_gemm_add_corun_every_mode(ctx):
+    """A GEMM and an add of its output size (plus a second add, fused with the
+    first) in every execution mode; every output against the oracle."""
+    from tests.gpu_helpers import check_add
+    g = inputs.materialize(GemmSpec(512, 1024, 768, "bf16", seed=8100, name="corun"))
+    adds = [inputs.materialize_add(512, 1024, "bf16", seed=8101 + i) for i in range(2)]
+    for mode in ("sequential", "default", "go", "selector"):
+        reset_outputs([g])
+        for x in adds:
+            x.c_full.fill_(float("nan"))
+        plan = ctx.execute([gemm_of(g)] + [gdy.Add(x.a, x.b, x.c) for x in adds], mode=mode,
+                           want_plan=True)
+        torch.cuda.synchronize()
+        assert sorted(plan["order"]) == [0, 1, 2]
+        ew = [ctx.variant(plan["variant_of"][i])["kind"] for i in range(3)]
+        assert ew == [0, 1, 1], (mode, ew)
+        check(g, label=f"corun {mode}")
+        for x in adds:
+            check_add(x, label=f"corun {mode}")
+    # the two adds share one dispatch when they run in one group
+    plan = ctx.plan([gemm_of(g)] + [gdy.Add(x.a, x.b, x.c) for x in adds], mode="go")
+    assert plan["dispatch_of"][1] == plan["dispatch_of"][2] != plan["dispatch_of"][0]
+
+
+def test_add_validation(ctx):
+    x = inputs.materialize_add(32, 64, "bf16", seed=8200)
+    d = gdy.Add(x.a, x.b, x.c).desc()
+    d.k = 5
+    with pytest.raises(gdy.GdyError) as e:
+        ctx.execute([d])
+    assert e.value.status == 1
+    d = gdy.Add(x.a, x.b, x.c).desc()
+    d.c_type = 1  # mixed types
+    with pytest.raises(gdy.GdyError) as e:
+        ctx.execute([d])
+    assert e.value.status == 2
+    d = gdy.Add(x.a, x.b, x.c).desc()
+    d.op = 7
     with pytest.raises(gdy.GdyError) as e:
         ctx.execute([d])
     assert e.value.status == 1

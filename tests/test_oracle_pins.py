@@ -266,3 +266,21 @@ def test_f32_codes_decode_as_numpy_float32():
     codes = np.concatenate([codes, np.array([0, 0x80000000, 1, 0x807fffff, 0x7f7fffff], np.uint32)])
     got = oracle.decode(codes, "f32")
     np.testing.assert_array_equal(got, codes.view(np.float32).astype(np.float64))
+
+
+def test_add_closed_forms():
+    """The element-wise add oracle: dyadic values sum exactly, x + (-x) is 0,
+    the bound is |a| + |b|; strided rows are read through lda / ldb."""
+    m, n, lda, ldb = 3, 4, 6, 5
+    va = np.arange(m * lda, dtype=np.float32).reshape(m, lda) * 0.25 - 2.0
+    vb = -np.arange(m * ldb, dtype=np.float32).reshape(m, ldb) * 0.5 + 1.0
+    a = va.astype(np.float32).view(np.uint32)
+    b = vb.astype(np.float32).view(np.uint32)
+    ref, bound = oracle.add(m, n, a, "f32", lda, b, "f32", ldb)
+    np.testing.assert_array_equal(ref, va[:, :n].astype(np.float64) + vb[:, :n].astype(np.float64))
+    np.testing.assert_array_equal(bound, np.abs(va[:, :n]) + np.abs(vb[:, :n]))
+    x = np.array([0x3fc0, 0xc040, 0x4110], np.uint16)   # bf16 1.5, -3.0, 9.0
+    y = np.array([0x4010, 0x4040, 0xc110], np.uint16)   # bf16 2.25, 3.0, -9.0
+    ref, bound = oracle.add(1, 3, x, "bf16", 3, y, "bf16", 3)
+    np.testing.assert_array_equal(ref, [[3.75, 0.0, 0.0]])
+    np.testing.assert_array_equal(bound, [[3.75, 6.0, 18.0]])

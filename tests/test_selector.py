@@ -111,7 +111,7 @@ def _desc(m, n, k, dtype, ta, tb, base, pad=0):
     d.lda = (m if ta else k) + pad
     d.ldb = (k if tb else n) + pad
     d.ldc = n
-    d.a, d.b, d.c = base, base + (1 << 32), base + (2 << 32)
+    d.a, d.b, d.c = base, base + (1 << 34), base + (2 << 34)  # 16 GiB apart: room for batches
     d.scale_a = d.scale_b = 1.0
     d.variant = -1
     return d
@@ -120,7 +120,7 @@ def _desc(m, n, k, dtype, ta, tb, base, pad=0):
 def _as_dict(d):
     return {"m": d.m, "n": d.n, "k": d.k, "a_type": d.a_type, "trans_a": d.trans_a,
             "trans_b": d.trans_b, "a": d.a, "b": d.b, "lda": d.lda, "ldb": d.ldb,
-            "batch": d.batch, "stride_a": d.stride_a, "stride_b": d.stride_b}
+            "batch": d.batch, "stride_a": d.stride_a, "stride_b": d.stride_b, "op": d.op}
 
 
 def _synthetic_table(path, ctx, rng):
@@ -142,7 +142,8 @@ def _synthetic_table(path, ctx, rng):
         lines.append("lr_b " + " ".join(map(repr, rng.normal(0, 1, 5).tolist())))
     for dtype in (1, 2, 3, 4):
         for ta, tb in ((0, 0), (0, 1), (1, 1)):
-            pool = [v["name"] for v in V if (v["dtype"], v["trans_a"], v["trans_b"]) == (dtype, ta, tb)]
+            pool = [v["name"] for v in V if (v["dtype"], v["trans_a"], v["trans_b"]) == (dtype, ta, tb)
+                    and v["kind"] == 0]
             for mlog in (4, 7, 10, 12):
                 for n in (1024, 8192):
                     for k in (1024, 8192):
@@ -181,7 +182,13 @@ def _random_set(rng, n):
         m = int(rng.integers(1, 5000))
         nn = int(rng.choice([512, 1000, 2048, 4096, 8192]))
         k = int(rng.choice([64, 100, 1024, 3000, 8192]))
-        d = _desc(m, nn, k, dtype, ta, tb, (i + 1) << 36, pad=int(rng.choice([0, 0, 3])))
+        d = _desc(m, nn, k, dtype, ta, tb, (i + 1) << 37, pad=int(rng.choice([0, 0, 3])))
+        if rng.random() < 0.15 and dtype != 3:  # an element-wise add (the non-GEMM of Sec. 7.1)
+            d = _desc(m, nn, 0, dtype, 0, 0, (i + 1) << 37)
+            d.lda = d.ldb = d.ldc = nn
+            d.op = 1
+            out.append(d)
+            continue
         if rng.random() < 0.3:  # a strided batch: item strides aligned or not
             d.batch = int(rng.integers(2, 40))
             d.stride_a = (d.lda * (k if ta else m)) + int(rng.choice([0, 8, 3]))
@@ -202,8 +209,11 @@ def test_planner_matches_oracle_on_synthetic_tables(tmp_path):
         for _ in range(40):
             descs = _random_set(rng, int(rng.integers(1, 17)))
             _check_plan(ctx, table, descs)
-            # features, bit for bit
-            d = descs[0]
+            # features (of the first GEMM member), bit for bit
+            gemm_members = [d for d in descs if d.op == 0]
+            if not gemm_members:
+                continue
+            d = gemm_members[0]
             np.testing.assert_array_equal(
                 ctx.features(d),
                 sel.features(_as_dict(d), table, ctx.variants(),

@@ -48,7 +48,8 @@ def test_training_and_evaluation_shapes():
 def test_written_table_reads_back(tmp_path):
     ctx = gdy.Context(-1)
     V = ctx.variants()
-    names = [v["name"] for v in V if (v["dtype"], v["trans_a"], v["trans_b"]) == (2, 0, 0)][:5]
+    names = [v["name"] for v in V if (v["dtype"], v["trans_a"], v["trans_b"]) == (2, 0, 0)
+             and v["kind"] == 0][:5]
     recs = [{"shape": ["bf16", 0, 0, 512, 4096, 1024], "go": {str(c): names[i] for i, c in
                                                               enumerate(tuner.CDS)}}]
     rng = np.random.default_rng(2)
@@ -80,3 +81,13 @@ def test_library_rejects_table_naming_unknown_variants(tmp_path):
     open(path, "w").write("not a table\n")
     with pytest.raises(gdy.GdyError):
         gdy.Context(-1, table=path)
+
+
+def test_library_rejects_the_add_kernel_in_a_gemm_entry(tmp_path):
+    """A GO table entry naming the element-wise add for a GEMM shape is refused."""
+    path = str(tmp_path / "ew.table")
+    open(path, "w").write("gdy-go-table 1\ndevice host cus 256\ncatalogue 0123456789abcdef\n"
+                          "entry 2 0 0 9 4096 1024 " + " ".join(["ew_add_bf16_c0"] * 5) + "\n")
+    with pytest.raises(gdy.GdyError) as e:
+        gdy.Context(-1, table=path)
+    assert e.value.status == 5
