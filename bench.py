@@ -42,6 +42,8 @@ WORKLOADS = {
     "tp8_layer_share_f32": ("3f32", "the 8 GEMMs of tp8_layer_share in fp32 (full precision)"),
     "attn_bgemm_4p": ("attn", "4 heterogeneous strided batched bf16 GEMMs: attention scores Q K^T "
                               "(SL x SL x 64, K transposed) for SL 128/256/384/512, 64 items each"),
+    "gemm_add_pairs": ("pairs", "8 submissions of one bf16 GEMM and an element-wise add sized like its "
+                                "output (2P GEMM + non-GEMM co-runs)"),
 }
 TRAFFIC = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2409_02227_amd", "csrc", f)
@@ -247,6 +249,42 @@ def het_bench(args, desc):
     print(json.dumps(out), flush=True)
 
 
+def pairs_bench(args, desc):
+    """GEMM + non-GEMM co-runs: each pair is one submission (GEMM, then the
+    add of its output size); per-pair times under sequential, default and
+    the selector; aggregate GEMM TFLOP/s and geomean speedups."""
+    import torch
+    from paper_2409_02227_amd import gdy, inputs
+    table = args.table if args.table and os.path.exists(args.table) else None
+    ctx = gdy.Context(0, table=table, max_streams=16)
+    handle = gdy._stream_handle(None)
+    t = {"sequential": [], "default": [], args.mode: []}
+    flops = []
+    for spec, (m, n) in inputs.gemm_add_pairs():
+        g = inputs.materialize(spec, "cuda:0", keep_host=False)
+        x = inputs.materialize_add(m, n, "bf16", seed=spec.seed)
+        members = [gdy.Gemm(g.a, g.b, g.c), gdy.Add(x.a, x.b, x.c)]
+        arr = gdy.descs(members)
+        for mode in t:
+            t[mode].append(time_steps(ctx, arr, 2, mode, args.steps, 2, handle, torch))
+        flops.append(spec.flops)
+    sel = t[args.mode]
+    gm = lambda a, b: round(float(np.exp(np.mean(np.log(np.array(a) / np.array(b))))), 4)
+    value = sum(flops) / sum(sel) / 1e12
+    out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": 2, "ms_per_step": round(1e3 * sum(sel) / len(sel), 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (seeded; GEMM operands as in the other workloads, add operands U[-1,1])",
+           "config": {"workload": f"gemm_add_pairs: {desc}", "mode": args.mode, "pairs": len(sel),
+                      "table": os.path.relpath(table, ROOT) if table else None},
+           "speedup_vs_sequential_geomean": gm(t["sequential"], sel),
+           "speedup_vs_default_geomean": gm(t["default"], sel),
+           "per_pair_ms": {mode: [round(1e3 * v, 4) for v in vals] for mode, vals in t.items()},
+           "sequential_tflops": round(sum(flops) / sum(t["sequential"]) / 1e12, 2),
+           "pct_mfma_peak": round(100 * value / PEAK_TFLOPS["bf16"], 2)}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -262,6 +300,8 @@ def main():
     cfg_id, desc = WORKLOADS[args.workload]
     if cfg_id == 4:
         return het_bench(args, desc)
+    if cfg_id == "pairs":
+        return pairs_bench(args, desc)
     if cfg_id == "3nt":
         specs = inputs.config3(trans_b=1)
     elif cfg_id == "3f32":

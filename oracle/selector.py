@@ -248,22 +248,46 @@ def group(order: list, pref: dict, slots: int) -> list:
 MAX_FUSED = 16
 
 
+def roofline_seconds(g: dict) -> float:
+    """Time bound of one member from MI355X's published peaks: HBM 8 TB/s;
+    dense MFMA 2.5 PFLOP/s (16-bit inputs), 5.0 (fp8), 157.3 TFLOP/s (fp32).
+    An add moves A, B and C once; a GEMM takes the larger of its MFMA time
+    and the time to move A, B and C once."""
+    items = float(max(g.get("batch", 0), 1))
+    m, n, k = float(g["m"]), float(g["n"]), float(g["k"])
+    es = float(elem_bytes(g["a_type"]))
+    if g.get("op", 0) == 1:
+        return items * 3.0 * m * n * es / 8e12
+    peak = {3: 5.0e15, 4: 157.3e12}.get(g["a_type"], 2.5e15)
+    mfma = items * 2.0 * m * n * k / peak
+    out = 4.0 if g["a_type"] == 4 else 2.0
+    bytes_ = (m * k + k * n) * es + m * n * out
+    return max(mfma, items * bytes_ / 8e12)
+
+
 def kernel_of(name: str) -> str:
     return name.rsplit("_c", 1)[0]
 
 
 def dispatches(groups: list, variant_of: dict, variants: list, slots: int):
-    """dispatch_of and stream_of per GEMM for groups launched one after another."""
+    """dispatch_of and stream_of per GEMM for groups launched one after another.
+    Members of one kernel share a dispatch (at most MAX_FUSED); an
+    element-wise add joins the group's first dispatch when that one is a
+    GEMM's and has room, else adds share an add dispatch."""
     dispatch_of, stream_of, nxt = {}, {}, 0
     for grp in groups:
-        opened = []  # [kernel, dispatch id, members]
+        opened = []  # [kernel, dispatch id, members, is an add kernel]
         for i in grp:
-            k = kernel_of(variants[variant_of[i]]["name"])
-            hit = [u for u, o in enumerate(opened) if o[0] == k and o[2] < MAX_FUSED]
+            v = variants[variant_of[i]]
+            k, is_add = kernel_of(v["name"]), v.get("kind", 0) == 1
+            if is_add and opened and not opened[0][3] and opened[0][2] < MAX_FUSED:
+                hit = [0]
+            else:
+                hit = [u for u, o in enumerate(opened) if o[0] == k and o[2] < MAX_FUSED]
             if hit:
                 u = hit[-1]
             else:
-                opened.append([k, nxt, 0])
+                opened.append([k, nxt, 0, is_add])
                 nxt += 1
                 u = len(opened) - 1
             opened[u][2] += 1
@@ -296,19 +320,43 @@ def plan_selector(gemms: list, table: dict, variants: list, cus: int, slots: int
             continue
         x = features(gemms[i], table, variants, by_name, cus)
         out["pred_cd"][i] = clamp(predict_cd(x, lr), n)
-    order = sorted(live, key=lambda i: -out["pred_cd"][i])  # stable: submission order on ties
+    is_add = {i: gemms[i].get("op", 0) == 1 for i in live}
+    order = sorted((i for i in live if not is_add[i]),
+                   key=lambda i: -out["pred_cd"][i])  # stable: submission order on ties
+    groups = group(order, out["pred_cd"], slots)
+    taken = [len(grp) for grp in groups]  # GO-Kernel class of each group
+    adds = [i for i in live if is_add[i]]
+    if adds:
+        # adds join the first group (Sec. 7.1); they take slots of its class,
+        # up to its capacity, only when their roofline time is at least half
+        # an average GEMM's of the group
+        first = groups[0] if groups else []
+        if first:
+            cap = min(min(out["pred_cd"][i], slots) for i in first)
+            t_gemm = 0.0
+            for i in first:
+                t_gemm += roofline_seconds(gemms[i])
+            t_add = 0.0
+            for i in adds:
+                t_add += roofline_seconds(gemms[i])
+            if t_add >= 0.5 * (t_gemm / len(first)):
+                taken[0] = max(len(first), min(len(first) + len(adds), cap))
+        groups = [first + adds] + groups[1:]
+        taken = taken if first else [0] + taken
     out["groups"] = []
-    for grp in group(order, out["pred_cd"], slots):
-        ci = class_for_size(len(grp))
+    for grp, s in zip(groups, taken):
+        ci = class_for_size(max(1, s))
         parts = {}  # kernel -> GEMMs, in order of first appearance
         for i in grp:
             out["variant_of"][i] = bind(gemms[i], ci, table, variants, by_name)
             parts.setdefault(kernel_of(variants[out["variant_of"][i]]["name"]), []).append(i)
-        # inside a dispatch: K descending, then M*N; dispatches: total 2MNK descending
+        # inside a dispatch: K descending, then M*N; dispatches: total 2MNK
+        # descending, adds after every GEMM
         parts = [sorted(v, key=lambda i: (-gemms[i]["k"], -gemms[i]["m"] * gemms[i]["n"]))
                  for v in parts.values()]
         work = [sum(2.0 * gemms[i]["m"] * gemms[i]["n"] * gemms[i]["k"] for i in v) for v in parts]
-        ranked = sorted(range(len(parts)), key=lambda u: -work[u])
+        adds = [variants[out["variant_of"][v[0]]].get("kind", 0) == 1 for v in parts]
+        ranked = sorted(range(len(parts)), key=lambda u: (adds[u], -work[u]))
         out["groups"].append([i for u in ranked for i in parts[u]])
     out["dispatch_of"], out["stream_of"], out["n_dispatches"] = dispatches(
         out["groups"], out["variant_of"], variants, slots)

@@ -459,17 +459,29 @@ void plan_reset(gdy_plan_t* p, int n) {
   }
 }
 
-// Dispatches of one group (members in launch order, variants bound): GEMMs
-// of the same kernel share a dispatch, at most kMaxFused each, numbered in
-// order of first use.  The group's first dispatch runs on the origin
-// stream, the others round-robin on the pool.
+bool is_add_variant(const gdy_ctx* ctx, int vid) {
+  return ctx->kernels[ctx->variants[vid].kernel].d->ew != 0;
+}
+
+// Dispatches of one group (members in launch order, GEMMs before adds,
+// variants bound): GEMMs of the same kernel share a dispatch, at most
+// kMaxFused each, numbered in order of first use.  An element-wise add
+// rides in the group's first dispatch when that one runs a GEMM kernel and
+// has room (GEMM kernels run add members too, so the pair needs no second
+// stream); otherwise adds of one type share an add dispatch.  The group's
+// first dispatch runs on the origin stream, the others round-robin on the
+// pool.
 void form_dispatches(const gdy_ctx* ctx, const std::vector<int>& members, int S, gdy_plan_t* p) {
   std::vector<int> kern, id, cnt;
   for (int i : members) {
     const int k = ctx->variants[p->variant_of[i]].kernel;
     int d = -1;
-    for (size_t u = 0; u < kern.size(); ++u)
-      if (kern[u] == k && cnt[u] < kMaxFused) d = (int)u;
+    if (is_add_variant(ctx, p->variant_of[i]) && !kern.empty() && !ctx->kernels[kern[0]].d->ew &&
+        cnt[0] < kMaxFused)
+      d = 0;
+    else
+      for (size_t u = 0; u < kern.size(); ++u)
+        if (kern[u] == k && cnt[u] < kMaxFused) d = (int)u;
     if (d < 0) {
       d = (int)kern.size();
       kern.push_back(k);
@@ -483,6 +495,23 @@ void form_dispatches(const gdy_ctx* ctx, const std::vector<int>& members, int S,
 }
 
 bool active(const gdy_gemm& g) { return g.m > 0 && g.n > 0; }
+
+// Roofline time of one member from the device's published peaks (8 TB/s of
+// HBM; dense MFMA 2.5 PFLOP/s for 16-bit inputs, 5.0 for fp8, 157.3 TFLOP/s
+// for fp32): an add moves A, B and C once; a GEMM takes the larger of its
+// MFMA time and the time to move its operands once.
+double roofline_s(const gdy_gemm& g) {
+#pragma clang fp contract(off)  // the oracle planner evaluates the same roundings
+  const double items = (double)std::max(g.batch, 1);
+  const double m = (double)g.m, n = (double)g.n, k = (double)g.k;
+  const double es = (double)elem_size(g.a_type);
+  if (g.op == GDY_OP_ADD) return items * 3.0 * m * n * es / 8e12;
+  const double peak = g.a_type == GDY_FP8_E4M3 ? 5.0e15 : g.a_type == GDY_F32 ? 157.3e12 : 2.5e15;
+  const double mfma = items * 2.0 * m * n * k / peak;
+  const double ab = m * k + k * n;
+  const double bytes = ab * es + m * n * (double)out_size(g);
+  return std::max(mfma, items * bytes / 8e12);
+}
 
 int pool_size(const gdy_ctx* ctx) {
   if (ctx->device < 0) return ctx->host_slots;
@@ -552,6 +581,7 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
     for (int q = 0; t < L; ++q) {
       std::vector<int> grp;
       for (; t < L && (int)grp.size() < size; ++t) grp.push_back(live[t]);
+      std::stable_partition(grp.begin(), grp.end(), [&](int i) { return g[i].op != GDY_OP_ADD; });
       const int ci = class_for_size(mode == GDY_GO && forced_cd > 0 ? forced_cd : (int)grp.size());
       for (size_t u = 0; u < grp.size(); ++u) {
         const int i = grp[u];
@@ -594,36 +624,64 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
     pred[i] = std::min(cd, L);
     p->pred_cd[i] = pred[i];
   }
-  std::vector<int> ord(live);
+  std::vector<int> ord, adds;
+  for (int i : live) (g[i].op == GDY_OP_ADD ? adds : ord).push_back(i);
   std::stable_sort(ord.begin(), ord.end(), [&](int a, int b) { return pred[a] > pred[b]; });
   std::vector<std::vector<int>> groups;
+  std::vector<int> caps;  // each group's capacity: its GEMMs' smallest clamped CD
   int gcap = 0;
-  for (int t = 0; t < L; ++t) {
+  for (size_t t = 0; t < ord.size(); ++t) {
     const int i = ord[t];
     const int cap = std::min(pred[i], S);
     if (groups.empty() || (int)groups.back().size() + 1 > std::min(gcap, cap)) {
       groups.emplace_back();
+      caps.push_back(cap);
       gcap = cap;
     }
     gcap = std::min(gcap, cap);
+    caps.back() = gcap;
     groups.back().push_back(i);
+  }
+  // element-wise adds join the first group, whose first dispatch runs them
+  // next to its GEMMs (Sec. 7.1).  An add is a co-runner -- it takes a slot
+  // of the group's GO-Kernel class, up to the group's capacity -- only when
+  // the adds' roofline time is at least half that of an average GEMM of the
+  // group; a smaller add fills the GEMMs' tail and the GEMMs keep the class
+  // of their own count.
+  std::vector<int> slots(groups.size());
+  for (size_t q = 0; q < groups.size(); ++q) slots[q] = (int)groups[q].size();
+  if (!adds.empty()) {
+    if (groups.empty()) {
+      groups.emplace_back();
+      slots.push_back(0);
+      caps.push_back(0);
+    }
+    double t_gemm = 0.0, t_add = 0.0;
+    for (int i : groups[0]) t_gemm += roofline_s(g[i]);
+    for (int i : adds) t_add += roofline_s(g[i]);
+    const int ng = (int)groups[0].size();
+    if (ng > 0 && t_add >= 0.5 * (t_gemm / ng))
+      slots[0] = std::max(ng, std::min(ng + (int)adds.size(), caps[0]));
+    groups[0].insert(groups[0].end(), adds.begin(), adds.end());
   }
   // launch order within a group: the GEMMs bound to one kernel form one
   // dispatch (a group holds at most 16); inside it the longest workgroups
   // go first (tiles of one size take time in proportion to K: K
   // descending, then M*N), and the dispatches go in order of their total
   // work (sum of 2MNK, descending), so the largest one starts first on the
-  // origin stream.  Ties keep the grouping order.
+  // origin stream; adds come after every GEMM.  Ties keep the grouping
+  // order.
   int t = 0;
   p->n_groups = (int)groups.size();
   p->cd = 0;
   for (int q = 0; q < p->n_groups; ++q) {
     const std::vector<int>& grp = groups[q];
     const int s = (int)grp.size();
+    const int ci = class_for_size(std::max(slots[q], 1));
     std::vector<int> kern;                // kernels in order of first appearance
     std::vector<std::vector<int>> parts;  // their GEMMs
     for (int i : grp) {
-      p->variant_of[i] = bind_entry(ctx, g[i], entry[i], class_for_size(s), &fb);
+      p->variant_of[i] = bind_entry(ctx, g[i], entry[i], ci, &fb);
       const int k = ctx->variants[p->variant_of[i]].kernel;
       size_t u = 0;
       while (u < kern.size() && kern[u] != k) ++u;
@@ -643,7 +701,11 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
     }
     std::vector<int> pord(parts.size());
     for (size_t u = 0; u < pord.size(); ++u) pord[u] = (int)u;
-    std::stable_sort(pord.begin(), pord.end(), [&](int a, int b) { return work[a] > work[b]; });
+    std::stable_sort(pord.begin(), pord.end(), [&](int a, int b) {
+      const bool ea = ctx->kernels[kern[a]].d->ew != 0, eb = ctx->kernels[kern[b]].d->ew != 0;
+      if (ea != eb) return eb;
+      return work[a] > work[b];
+    });
     std::vector<int> ordered;
     for (int u : pord) ordered.insert(ordered.end(), parts[u].begin(), parts[u].end());
     p->group_size[q] = s;
@@ -717,6 +779,7 @@ KArgs make_args(const gdy_ctx* ctx, int vid, const gdy_gemm& g, Geometry* geo_ou
   a.group_m = 8;
   a.xcd_remap = 1;
   a.batch = (int32_t)std::max(g.batch, 1);
+  a.ew = add ? g.a_type : 0;
   a.stride_a = a.batch > 1 ? g.stride_a * es : 0;
   a.stride_b = a.batch > 1 ? g.stride_b * es : 0;
   a.stride_c = a.batch > 1 ? g.stride_c * out_size(g) : 0;
@@ -805,7 +868,12 @@ gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, hip
       for (int s : slots) HIP_TRY(ctx, hipStreamWaitEvent(slot_stream(ctx, s), ctx->fork_ev, 0));
     }
     for (size_t u = 0; u < ids.size(); ++u) {
-      const int i0 = members[u][0];
+      int i0 = members[u][0];  // the dispatch runs its first GEMM's kernel (adds ride along)
+      for (int i : members[u])
+        if (!is_add_variant(ctx, p.variant_of[i])) {
+          i0 = i;
+          break;
+        }
       const int vid = p.variant_of[i0];
       const Kernel& k = ctx->kernels[ctx->variants[vid].kernel];
       KLaunch launch;

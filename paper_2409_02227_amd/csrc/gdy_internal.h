@@ -30,6 +30,7 @@ struct KArgs {
   int32_t group_m;    // tile-order swizzle: tile rows per group
   int32_t xcd_remap;  // 1: keep consecutive tiles on one XCD
   int32_t batch;      // items of a strided batch (>= 1); the extents above are per item
+  int32_t ew;         // 0: a GEMM; else the DT_* of an element-wise add (C = A + B)
   int64_t stride_a;   // bytes between consecutive items of A, B and C
   int64_t stride_b;
   int64_t stride_c;

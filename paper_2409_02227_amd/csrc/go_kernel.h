@@ -393,6 +393,123 @@ __device__ __forceinline__ int owner_of(const KLaunch& L) {
   return i;
 }
 
+// ---------------------------------------------------------------------------
+// Element-wise add member (the non-GEMM that co-runs with GEMMs, Sec. 7.1):
+// C = A + B over an M x N region of one type (bf16, fp16 or fp32), summed in
+// fp32 and rounded once.  Its workgroup tile is kEwRows rows x 32 16-byte
+// vectors whatever the block size, so an add has the same tile grid in its
+// own kernel and inside a GEMM kernel's dispatch; a block of NT threads
+// covers a tile in kEwRows * 32 / NT row passes and issues every load of the
+// tile before the first sum.  Reads outside an operand's extent return 0
+// through the buffer resource; stores are masked to the region.
+// ---------------------------------------------------------------------------
+constexpr int kEwRows = 32;
+template <int DT> struct EwCols { static constexpr int v = 32 * 16 / ElemSize<DT>::v; };
+
+template <int DT> __device__ __forceinline__ float ew_decode(unsigned bits);
+template <> __device__ __forceinline__ float ew_decode<DT_BF16>(unsigned bits) {
+  return __builtin_bit_cast(float, bits << 16);
+}
+template <> __device__ __forceinline__ float ew_decode<DT_F16>(unsigned bits) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)bits);
+}
+template <> __device__ __forceinline__ float ew_decode<DT_F32>(unsigned bits) {
+  return __builtin_bit_cast(float, bits);
+}
+
+// The thread's 16 bytes of one operand row: one vector load, or element by
+// element where the base, pitch or item stride is not 16-byte aligned.
+template <int ES>
+__device__ __forceinline__ u32x4 ew_load(Rsrc r, int vec, int off) {
+  if (vec) return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  u32x4 w = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int e = 0; e < 16 / ES; ++e) w[e * ES / 4] |= load_elem<ES>(r, off + e * ES) << ((e * ES * 8) & 31);
+  return w;
+}
+
+template <int DT, int NT>
+__device__ __forceinline__ void ew_add_tiles(const KArgs& p, int lwg, int nwg) {
+  constexpr int ES = ElemSize<DT>::v;
+  constexpr int VEC = 16 / ES;
+  constexpr int RP = NT / 32;  // rows per pass
+  constexpr int PASSES = kEwRows / RP;
+  static_assert(PASSES >= 1 && kEwRows % RP == 0, "the block must tile the add's rows");
+  Rsrc ra = make_rsrc(p.a, p.a_bytes);
+  Rsrc rb = make_rsrc(p.b, p.b_bytes);
+  Rsrc rc = make_rsrc(p.c, p.c_bytes);
+  const int Mrows = (int)p.m, Ncols = (int)p.n;
+  const int lda_b = (int)p.lda * ES, ldb_b = (int)p.ldb * ES, ldc_b = (int)p.ldc * ES;
+  const int ntiles = p.tiles_m * p.tiles_n;
+  const int total = ntiles * p.batch;
+  const int r = threadIdx.x / 32, v = threadIdx.x % 32;
+  for (int tb = lwg; tb < total; tb += nwg) {
+    int t = tb;
+    if (p.batch > 1) {
+      const int item = tb / ntiles;
+      t = tb - item * ntiles;
+      ra = make_rsrc(p.a + item * p.stride_a, p.a_bytes);
+      rb = make_rsrc(p.b + item * p.stride_b, p.b_bytes);
+      rc = make_rsrc(p.c + item * p.stride_c, p.c_bytes);
+    }
+    const int row0 = (t / p.tiles_n) * kEwRows + r;
+    const int col0 = (t % p.tiles_n) * EwCols<DT>::v + v * VEC;
+    if (col0 >= Ncols) continue;
+    u32x4 wa[PASSES], wb[PASSES];
+#pragma unroll
+    for (int s = 0; s < PASSES; ++s) {
+      const int row = row0 + s * RP;
+      if (row < Mrows) {
+        wa[s] = ew_load<ES>(ra, p.a_vec, row * lda_b + col0 * ES);
+        wb[s] = ew_load<ES>(rb, p.b_vec, row * ldb_b + col0 * ES);
+      }
+    }
+    const bool whole = p.c_vec && col0 + VEC <= Ncols;  // two 8-byte stores
+#pragma unroll
+    for (int s = 0; s < PASSES; ++s) {
+      const int row = row0 + s * RP;
+      if (row >= Mrows) break;
+      const int off = row * ldc_b + col0 * ES;
+      u32x4 out = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const int sh = (e * ES * 8) & 31;
+        const unsigned mask = ES == 4 ? 0xffffffffu : 0xffffu;
+        const float x = ew_decode<DT>((wa[s][e * ES / 4] >> sh) & mask);
+        const float y = ew_decode<DT>((wb[s][e * ES / 4] >> sh) & mask);
+        if constexpr (DT == DT_F32) {
+          out[e] = __builtin_bit_cast(unsigned, x + y);
+        } else {
+          out[e * ES / 4] |= (unsigned)to_out<DT>(x + y) << sh;
+        }
+      }
+      if (whole) {
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{out[0], out[1]}, rc, off, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{out[2], out[3]}, rc, off + 8, 0, 0);
+      } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          if (col0 + e >= Ncols) break;
+          const int sh = (e * ES * 8) & 31;
+          if constexpr (DT == DT_F32)
+            __builtin_amdgcn_raw_buffer_store_b32(out[e], rc, off + e * ES, 0, 0);
+          else
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(out[e * ES / 4] >> sh), rc, off + e * ES, 0, 0);
+        }
+      }
+    }
+  }
+}
+
+// An add member of any type run by a block of NT threads (a GEMM kernel's
+// dispatch holds adds next to its GEMMs: KArgs::ew names their type).
+template <int NT>
+__device__ __forceinline__ void ew_member(const KArgs& p, int lwg, int nwg) {
+  if (p.ew == DT_BF16) ew_add_tiles<DT_BF16, NT>(p, lwg, nwg);
+  else if (p.ew == DT_F16) ew_add_tiles<DT_F16, NT>(p, lwg, nwg);
+  else if (p.ew == DT_F32) ew_add_tiles<DT_F32, NT>(p, lwg, nwg);
+}
+
 template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int MM>
 struct GoCfg {
   static constexpr int ES = ElemSize<DT>::v;
@@ -430,6 +547,10 @@ go_gemm(KLaunch L) {
   const KArgs& p = L.g[gi];
   const int wg0 = L.first[gi];
   const int nwg = L.first[gi + 1] - wg0;
+  if (p.ew) {  // an element-wise add fused into this dispatch
+    ew_member<C::NT>(p, (int)blockIdx.x - wg0, nwg);
+    return;
+  }
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;

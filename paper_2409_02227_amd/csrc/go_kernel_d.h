@@ -277,6 +277,10 @@ go_gemm_d(KLaunch L) {
   const KArgs& p = L.g[gi];
   const int wg0 = L.first[gi];
   const int nwg = L.first[gi + 1] - wg0;
+  if (p.ew) {  // an element-wise add fused into this dispatch
+    ew_member<C::NT>(p, (int)blockIdx.x - wg0, nwg);
+    return;
+  }
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;

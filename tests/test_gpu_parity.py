@@ -544,9 +544,53 @@ def test_gemm_add_corun_every_mode(ctx):
         check(g, label=f"corun {mode}")
         for x in adds:
             check_add(x, label=f"corun {mode}")
-    # the two adds share one dispatch when they run in one group
-    plan = ctx.plan([gemm_of(g)] + [gdy.Add(x.a, x.b, x.c) for x in adds], mode="go")
-    assert plan["dispatch_of"][1] == plan["dispatch_of"][2] != plan["dispatch_of"][0]
+    # in one group both adds ride in the GEMM's dispatch: one launch, no second stream
+    plan = ctx.plan([gdy.Add(x.a, x.b, x.c) for x in adds] + [gemm_of(g)], mode="go")
+    assert plan["n_dispatches"] == 1 and plan["order"][:3] == [2, 0, 1], plan["order"][:3]
+    assert plan["dispatch_of"][0] == plan["dispatch_of"][1] == plan["dispatch_of"][2]
+    # a group of adds only keeps the add kernel, both adds in one dispatch
+    plan = ctx.plan([gdy.Add(x.a, x.b, x.c) for x in adds], mode="go")
+    assert plan["n_dispatches"] == 1
+
+
+def test_add_fused_into_every_gemm_kernel(ctx):
+    """An add rides in the dispatch of every GEMM kernel (staged and direct,
+    every block size): adds of each type, ragged, with unaligned rows, or a
+    strided batch; GEMM and add against the oracle, and the add's bits equal
+    to those of its own kernel."""
+    from tests.gpu_helpers import check_add
+    V = ctx.variants()
+    ew = {DT_NAME[v["dtype"]]: i for i, v in enumerate(V) if v["kind"] == 1 and v["grid_cap_cus"] == 0}
+    cases = ((1, 1, 0, "bf16", 0), (37, 300, 3, "f16", 0), (70, 1030, 0, "f32", 0),
+             (257, 4100, 8, "bf16", 0), (96, 520, 0, "f16", 3), (40, 136, 5, "f32", 4))
+    for j, (vid, v) in enumerate(_kernels(ctx)):
+        dt = DT_NAME[v["dtype"]]
+        spec = GemmSpec(v["bm"] * 2, v["bn"] * 2, v["bk"] * 3, dt, v["trans_a"], v["trans_b"],
+                        seed=1000 + vid, name=v["name"])
+        mat = inputs.materialize(spec)
+        m, n, pad, adt, items = cases[j % len(cases)]
+        x = inputs.materialize_add(m * max(items, 1), n, adt, seed=8300 + j, pad=pad)
+
+        def add_of(variant):
+            if items:
+                a, b, c = (t.unflatten(0, (items, m)) for t in (x.a, x.b, x.c))
+                return gdy.Add(a, b, c, variant=variant)
+            return gdy.Add(x.a, x.b, x.c, variant=variant)
+        reset_outputs([mat])
+        plan = ctx.execute([add_of(ew[adt]), gemm_of(mat, vid)], mode="forced_grouped",
+                           want_plan=True)
+        torch.cuda.synchronize()
+        label = f"{v['name']} + add {adt} {m}x{n}+{pad} items {items}"
+        assert plan["n_dispatches"] == 1 and plan["order"][:2] == [1, 0], label
+        assert ctx.variant(plan["variant_of"][1])["kind"] == 0, label
+        check(mat, label=label)
+        check_add(x, label=label)
+        fused = x.c_full.clone()
+        x.c_full.fill_(float("nan"))
+        ctx.execute([add_of(-1)], mode="sequential")
+        torch.cuda.synchronize()
+        raw = torch.int32 if adt == "f32" else torch.int16
+        assert torch.equal(fused.view(raw), x.c_full.view(raw)), f"{label}: fused bits differ"
 
 
 def test_add_validation(ctx):

@@ -255,3 +255,60 @@ def test_no_table_falls_back_to_sequential():
     descs = [_desc(512, 4096, 1024, 2, 0, 0, (i + 1) << 36) for i in range(4)]
     p = ctx.plan(descs, mode="selector")
     assert p["fallback"] == 1 and p["cd"] == 1 and p["n_groups"] == 4
+
+
+def _fixed_cd_table(tmp_path, name, cd_class):
+    """The synthetic table's kernels with a predictor that always answers one
+    CD class (zero weights, one large bias)."""
+    rng = np.random.default_rng(5)
+    path = str(tmp_path / f"{name}.src")
+    _synthetic_table(path, gdy.Context(-1), rng)
+    text = [l for l in open(path).read().split("\n") if not l.startswith("lr_")]
+    b = [0.0] * 5
+    b[cd_class] = 50.0
+    pred = ["lr_min " + " ".join(["0.0"] * sel.N_FEATURES), "lr_max " + " ".join(["1.0"] * sel.N_FEATURES),
+            "lr_w " + " ".join(["0.0"] * (sel.N_FEATURES * 5)), "lr_b " + " ".join(map(repr, b))]
+    out = tmp_path / f"{name}.table"
+    out.write_text("\n".join(text[:3] + pred + text[3:]) + "\n")
+    return str(out)
+
+
+def _add(m, n, dtype, base):
+    d = _desc(m, n, 0, dtype, 0, 0, base)
+    d.lda = d.ldb = d.ldc = n
+    d.op = 1
+    return d
+
+
+def test_add_rides_with_the_first_group(tmp_path):
+    """Element-wise adds join the first group and run in its first dispatch
+    (Sec. 7.1).  An add whose roofline time is at least half a GEMM's takes a
+    co-runner's slot of the GO-Kernel class (within the GEMMs' predicted CD);
+    a smaller one leaves the GEMM its own class."""
+    V = None
+    for cd_class in (4, 0):  # predictor: always CD 16, always CD 1
+        path = _fixed_cd_table(tmp_path, f"cd{cd_class}", cd_class)
+        ctx = gdy.Context(-1, table=path)
+        table = sel.parse_table(path)
+        V = ctx.variants()
+        by_name = {v["name"]: i for i, v in enumerate(V)}
+        for (m, n, k), big in (((4096, 1024, 1024), True), ((512, 8192, 8192), False)):
+            g = _desc(m, n, k, 2, 0, 0, 1 << 37)
+            a = _add(m, n, 2, 2 << 37)
+            # roofline: 16-bit MFMA peak 2.5 PFLOP/s, HBM 8 TB/s
+            t_gemm = max(2.0 * m * n * k / 2.5e15, ((m * k + k * n) * 2 + m * n * 2) / 8e12)
+            assert (3.0 * m * n * 2 / 8e12 >= 0.5 * t_gemm) == big
+            p = ctx.plan([a, g], mode="selector")
+            assert p["n_groups"] == 1 and p["n_dispatches"] == 1 and p["order"][:2] == [1, 0]
+            assert V[p["variant_of"][0]]["kind"] == 1 and p["stream_of"][0] == p["stream_of"][1] == -1
+            ci = 1 if (big and cd_class > 0) else 0
+            assert p["variant_of"][1] == sel.bind(_as_dict(g), ci, table, V, by_name), (m, n, k, cd_class)
+            _check_plan(ctx, table, [a, g])
+        # several groups (CD 1): the add joins the first
+        descs = [_desc(512, 4096, 1024, 2, 0, 0, (i + 1) << 37) for i in range(3)]
+        descs.insert(1, _add(512, 4096, 2, 9 << 37))
+        p = ctx.plan(descs, mode="selector")
+        if cd_class == 0:
+            assert p["n_groups"] == 3 and p["group_size"][:3] == [2, 1, 1]
+        assert p["group_of"][1] == 0 and p["dispatch_of"][1] == p["dispatch_of"][p["order"][0]]
+        _check_plan(ctx, table, descs)
