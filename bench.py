@@ -44,7 +44,11 @@ WORKLOADS = {
                               "(SL x SL x 64, K transposed) for SL 128/256/384/512, 64 items each"),
     "gemm_add_pairs": ("pairs", "8 submissions of one bf16 GEMM and an element-wise add sized like its "
                                 "output (2P GEMM + non-GEMM co-runs)"),
+    "cu_partition": ("parts", "P copies of each of 8 bf16 GEMMs (P = 2, 4, 8) on P CU partitions "
+                              "(CU-masked streams) and unpartitioned"),
 }
+PARTITION_SHAPES = ((4096, 1024, 1024), (8192, 1024, 512), (2048, 2048, 2048), (4096, 4096, 1024),
+                    (1024, 4096, 4096), (512, 8192, 8192), (256, 4096, 4096), (64, 8192, 2048))
 TRAFFIC = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2409_02227_amd", "csrc", f)
                   for f in ("go_kernel.h", "go_kernel_d.h")]
@@ -102,16 +106,17 @@ def parse():
     return ap.parse_args()
 
 
-def time_steps(ctx, arr, n, mode, steps, warmup, handle, torch, timing=False):
+def time_steps(ctx, arr, n, mode, steps, warmup, handle, torch, timing=False, forced_cd=0):
     from paper_2409_02227_amd import gdy
     m = gdy.MODES[mode]
+    fc = forced_cd if mode.startswith("cu_partition") else 0
     ctx.set_timing(timing)
     for _ in range(warmup):
-        ctx.execute_descs(arr, n, m, 0, handle)
+        ctx.execute_descs(arr, n, m, fc, handle)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
-        ctx.execute_descs(arr, n, m, 0, handle)
+        ctx.execute_descs(arr, n, m, fc, handle)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     ctx.set_timing(False)
@@ -285,6 +290,53 @@ def pairs_bench(args, desc):
     print(json.dumps(out), flush=True)
 
 
+def partition_bench(args, desc):
+    """CU-Partition (Sec. 6.9): for P = 2, 4, 8 and each shape, P copies of
+    the GEMM (distinct operands) in every partition mode and unpartitioned;
+    per P the geomean speedup of each mode over CU-Partition with
+    isolation-tuned kernels (each time the best of five runs of --steps
+    submissions).  value: aggregate TFLOP/s of the partition-tuned kernels
+    over every run."""
+    import torch
+    from paper_2409_02227_amd import gdy, inputs
+    table = args.table if args.table and os.path.exists(args.table) else None
+    ctx = gdy.Context(0, table=table, max_streams=8, use_cu_masks=gdy.PARTITION_STREAMS)
+    # CU-masked streams are blocking streams: an origin on the null stream
+    # would synchronise with every partition at each submission
+    origin = torch.cuda.Stream()
+    handle = gdy._stream_handle(origin)
+    modes = ("cu_partition", "cu_partition_go", "cu_partition_rc", "default", "go", "selector")
+    per_p, tot_f, tot_t = {}, 0.0, 0.0
+    for P in (2, 4, 8):
+        t = {m: [] for m in modes}
+        for j, (m_, n_, k_) in enumerate(PARTITION_SHAPES):
+            mats = [inputs.materialize(inputs.GemmSpec(m_, n_, k_, "bf16", seed=7000 + 100 * j + c, name=f"p{j}"),
+                                       "cuda:0", keep_host=False) for c in range(P)]
+            arr = gdy.descs([gdy.Gemm(x.a, x.b, x.c) for x in mats])
+            for mode in modes:  # host jitter of stream launches only adds: best of 5 timings
+                t[mode].append(min(time_steps(ctx, arr, P, mode, args.steps, 2, handle, torch, forced_cd=P)
+                                   for _ in range(5)))
+            tot_f += P * 2.0 * m_ * n_ * k_
+            tot_t += t["cu_partition_rc"][-1]
+            del mats
+        base = np.array(t["cu_partition"])
+        per_p[P] = {m: round(float(np.exp(np.mean(np.log(base / np.array(v))))), 4) for m, v in t.items()}
+        per_p[P]["ms_cu_partition_rc"] = [round(1e3 * v, 4) for v in t["cu_partition_rc"]]
+        per_p[P]["ms_cu_partition"] = [round(1e3 * v, 4) for v in t["cu_partition"]]
+    value = tot_f / tot_t / 1e12
+    out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": 2,
+           "ms_per_step": round(1e3 * tot_t / (3 * len(PARTITION_SHAPES)), 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (seeded; A ~ U[-1,1], B ~ N(0, 0.02))",
+           "config": {"workload": f"cu_partition: {desc}", "mode": "cu_partition_rc",
+                      "shapes": [list(s) for s in PARTITION_SHAPES],
+                      "table": os.path.relpath(table, ROOT) if table else None},
+           "geomean_speedup_over_cu_partition": per_p,
+           "pct_mfma_peak": round(100 * value / PEAK_TFLOPS["bf16"], 2)}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -302,6 +354,8 @@ def main():
         return het_bench(args, desc)
     if cfg_id == "pairs":
         return pairs_bench(args, desc)
+    if cfg_id == "parts":
+        return partition_bench(args, desc)
     if cfg_id == "3nt":
         specs = inputs.config3(trans_b=1)
     elif cfg_id == "3f32":

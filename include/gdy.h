@@ -81,9 +81,18 @@ typedef enum {
                          in submission order, one after another)                          */
   GDY_SELECTOR = 3,   /* GOLDYLOC: predicted CD per GEMM, grouping, GO-Kernels per group        */
   GDY_FORCED = 4,     /* each GEMM's `variant`, round-robin over forced_cd streams (tuning)     */
-  GDY_FORCED_GROUPED = 5 /* each GEMM's `variant`; consecutive runs of forced_cd GEMMs form
-                            groups run one after another, dispatched as GO and SELECTOR
-                            groups are (tuning)                                             */
+  GDY_FORCED_GROUPED = 5, /* each GEMM's `variant`; consecutive runs of forced_cd GEMMs form
+                             groups run one after another, dispatched as GO and SELECTOR
+                             groups are (tuning)                                            */
+  /* CU-Partition (Sec. 5.5, Sec. 6.9): P = forced_cd (2, 4 or 8; 0: the
+     smallest of them >= the number of GEMMs, at most 8) streams on disjoint
+     CU masks of CUs/P each; GEMM t of the submission runs on partition
+     t mod P (plan.stream_of), one dispatch per GEMM.  Needs a context
+     created with use_cu_masks & 2.  The three differ in the kernels:      */
+  GDY_CU_PARTITION = 6,    /* isolation-tuned kernels (the paper's CU-Partition)             */
+  GDY_CU_PARTITION_GO = 7, /* the GO-Kernels of CD class P, tuned for the unpartitioned GPU    */
+  GDY_CU_PARTITION_RC = 8  /* the kernels tuned under CUs/P CUs (the GO table's partition
+                              kernels; GO-Kernels of class P where the table has none)       */
 } gdy_mode;
 
 /*
@@ -175,11 +184,17 @@ typedef struct gdy_ctx gdy_ctx;
  * modes then fall back to isolated heuristics and report fallback = 1).
  * A table built for another device, or naming a variant the library does
  * not have, returns GDY_ERR_TABLE.
- * `use_cu_masks` != 0 also creates one CU-masked stream for each resource
- * constraint GPU/2, GPU/4 and GPU/8 (isolated runs of the tuner).  Every
- * stream needs its own hardware queue (a CU mask is a queue property), so
- * GPU_MAX_HW_QUEUES must cover the pool, the masked streams and the
- * caller's streams (24 for a 16-stream pool).  On error *out is NULL.
+ * `use_cu_masks` is a bit set: bit 0 creates one CU-masked stream for each
+ * resource constraint GPU/2, GPU/4 and GPU/8 (isolated runs of the tuner);
+ * bit 1 creates the CU-Partition streams (2 + 4 + 8 streams whose masks
+ * split the CUs into 2, 4 or 8 disjoint parts).  Every stream needs its own
+ * hardware queue (a CU mask is a queue property), so GPU_MAX_HW_QUEUES must
+ * cover the pool, the masked streams and the caller's streams (24 for a
+ * 16-stream pool alone; 32 for an 8-stream pool with partitions).  HIP
+ * creates CU-masked streams as blocking streams, so work on the null stream
+ * synchronises with all of them: give CU-Partition launches a created
+ * origin stream (on the null stream a submission of 8 partitions measured
+ * 2-3x slower).  On error *out is NULL.
  *
  * device < 0 creates a host-only context that plans without a GPU: its CU
  * count is GDY_HOST_CUS (default 256) or the loaded table's, kernel

@@ -80,7 +80,9 @@ def parse_table(path: str) -> dict:
             elif tok[0] == "entry":
                 t["entries"].append({"dtype": int(tok[1]), "ta": int(tok[2]), "tb": int(tok[3]),
                                      "mlog": int(tok[4]), "n": int(tok[5]), "k": int(tok[6]),
-                                     "variants": tok[7:12]})
+                                     "variants": tok[7:12],
+                                     # best kernels under 128, 64, 32 CUs (CU partitions)
+                                     "partition": tok[12:15] if len(tok) >= 15 else None})
     for d, lr in blocks.items():
         if len(lr) == 4:
             model = {"xmin": lr["lr_min"], "xmax": lr["lr_max"], "w": lr["lr_w"], "b": lr["lr_b"]}
@@ -294,6 +296,47 @@ def dispatches(groups: list, variant_of: dict, variants: list, slots: int):
             dispatch_of[i] = opened[u][1]
             stream_of[i] = -1 if u == 0 else (u - 1) % max(slots, 1)
     return dispatch_of, stream_of, nxt
+
+
+PARTITIONS = (2, 4, 8)  # CU-Partition counts: a partition of P holds 1/P of the CUs
+
+
+def partition_count(forced_cd: int, live: int) -> int:
+    """P of a CU-Partition launch: the requested count, or for 0 the
+    smallest count that gives every GEMM its own partition (at most 8)."""
+    want = forced_cd if forced_cd > 0 else live
+    for p in PARTITIONS:
+        if want <= p:
+            return p
+    return PARTITIONS[-1]
+
+
+def plan_partition(gemms: list, table: dict, variants: list, kernels: str, forced_cd: int = 0) -> dict:
+    """CU-Partition (Sec. 5.5, Sec. 6.9): P streams on disjoint CU masks;
+    GEMM t of the submission runs on partition t mod P.  kernels:
+    "isolated" (the isolation-tuned kernel), "go" (the GO-Kernel of CD
+    class P) or "rc" (the kernel tuned under 1/P of the CUs where the table
+    has one, else the GO-Kernel of class P)."""
+    by_name = {v["name"]: i for i, v in enumerate(variants)}
+    live = [i for i, g in enumerate(gemms) if g["m"] > 0 and g["n"] > 0]
+    P = partition_count(forced_cd, len(live))
+    ci = class_for_size(P)
+    out = {"P": P, "order": live, "stream_of": {}, "variant_of": {}}
+    for t, i in enumerate(live):
+        g = gemms[i]
+        out["stream_of"][i] = t % P
+        if kernels == "isolated":
+            v = bind(g, 0, table, variants, by_name)
+        elif kernels == "go" or g.get("op", 0) == 1:
+            v = bind(g, ci, table, variants, by_name)
+        else:
+            e = nearest_entry(table["entries"], g)
+            if e is not None and e.get("partition"):
+                v = runnable(by_name[e["partition"][PARTITIONS.index(P)]], g, variants)
+            else:
+                v = bind(g, ci, table, variants, by_name)
+        out["variant_of"][i] = v
+    return out
 
 
 def plan_selector(gemms: list, table: dict, variants: list, cus: int, slots: int) -> dict:

@@ -33,6 +33,7 @@ const int kCD[GDY_N_CD] = {1, 2, 4, 8, 16};  // CD classes of the predictor (Sec
 const int kCaps[] = {0, 128, 64, 32};         // grid caps in CUs: GPU, GPU/2, GPU/4, GPU/8
 const int kNumCaps = 4;
 const int kRcBudgets[] = {128, 64, 32};       // CU-masked pools for resource constraints
+const int kParts[] = {2, 4, 8};               // CU-Partition counts; kParts[r] parts of kRcBudgets[r] CUs
 
 struct Kernel {
   const KernelDesc* d;
@@ -52,6 +53,7 @@ struct TableEntry {
   int64_t n, k;
   double ln, lk;  // log2(n), log2(k)
   int v[GDY_N_CD];
+  int rc[3] = {-1, -1, -1};  // best kernel tuned under kRcBudgets[r] CUs (-1: not in the table)
 };
 
 // One CD predictor (Eq. 1): min-max bounds of the features, weights, biases.
@@ -115,6 +117,10 @@ struct gdy_ctx {
   std::vector<hipStream_t> pool;                   // whole GPU
   std::vector<std::vector<hipStream_t>> rc_pools;  // one per kRcBudgets entry
   int rc = 0;                                      // active CU budget, 0 = whole GPU
+  // CU partitions: parts[r] holds GPU/kParts[r]-CU streams on disjoint CU
+  // masks (empty unless created), part_done their join events
+  std::vector<std::vector<hipStream_t>> parts;
+  std::vector<std::vector<hipEvent_t>> part_done;
   int host_slots = 0;                              // host-only context: planned stream slots
   std::vector<hipEvent_t> done;                    // one per stream slot
   hipEvent_t fork_ev = nullptr;
@@ -248,6 +254,7 @@ int bind_variant(const gdy_ctx* ctx, const gdy_gemm& g, int ci, bool* fallback) 
   return bind_entry(ctx, g, nearest_entry(ctx, g), ci, fallback);
 }
 
+
 // CD class whose tuned kernel serves a group of s GEMMs: nearest class in
 // log2, ties upward; with integers, between 2^j and 2^(j+1) go up iff
 // s^2 >= 2^(2j+1).
@@ -259,6 +266,30 @@ int class_for_size(int s) {
     if (s < hi) return ((int64_t)s * s >= 2LL * lo * lo) ? j + 1 : j;
   }
   return GDY_N_CD - 1;
+}
+
+// Kernel tuned for one CU partition of partition count kParts[r] (the
+// nearest entry's best kernel under kRcBudgets[r] CUs); entries without
+// one fall back to the GO-Kernel of CD class kParts[r].
+int bind_partition(const gdy_ctx* ctx, const gdy_gemm& g, int r, bool* fallback) {
+  if (g.op == GDY_OP_ADD) return heuristic_variant(ctx, g);
+  const int entry = nearest_entry(ctx, g);
+  if (entry >= 0 && ctx->table.entries[entry].rc[r] >= 0)
+    return runnable(ctx, ctx->table.entries[entry].rc[r], g);
+  return bind_entry(ctx, g, entry, class_for_size(kParts[r]), fallback);
+}
+
+// Partition count of a CU-Partition launch: forced_cd (2, 4 or 8), or for
+// 0 the smallest count that gives every GEMM a partition (at most 8).
+int partition_index(int forced_cd, int live) {
+  const int want = forced_cd > 0 ? forced_cd : live;
+  for (int r = 0; r < 3; ++r)
+    if (want <= kParts[r]) return r;
+  return 2;
+}
+
+bool partition_mode(int mode) {
+  return mode == GDY_CU_PARTITION || mode == GDY_CU_PARTITION_GO || mode == GDY_CU_PARTITION_RC;
 }
 
 // Sec. 4.3 features: M, N, K and, per CD class, (#WGs, occupancy, #waves)
@@ -422,7 +453,7 @@ gdy_status validate(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode
   if (n < 0) return fail(ctx, GDY_ERR_INVALID_ARG, "n < 0");
   if (n > GDY_MAX_GEMMS) return fail(ctx, GDY_ERR_TOO_MANY, "n = %d > %d", n, GDY_MAX_GEMMS);
   if (n > 0 && !gemms) return fail(ctx, GDY_ERR_INVALID_ARG, "null gemm array");
-  if (mode < GDY_SEQUENTIAL || mode > GDY_FORCED_GROUPED)
+  if (mode < GDY_SEQUENTIAL || mode > GDY_CU_PARTITION_RC)
     return fail(ctx, GDY_ERR_INVALID_ARG, "bad mode %d", mode);
   std::vector<Extent> ea(n), eb(n), ec(n);
   for (int i = 0; i < n; ++i) {
@@ -569,6 +600,32 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
     p->n_dispatches = L;
     p->cd = L > 0 ? cd : 0;
     p->fallback = (mode != GDY_FORCED && (fb || !ctx->table.loaded)) ? 1 : 0;
+    return;
+  }
+
+  if (partition_mode(mode)) {
+    // Sec. 5.5 CU-Partition: P streams on disjoint CU masks of CUs/P each;
+    // GEMM t (submission order) runs on partition t mod P, one dispatch per
+    // GEMM, bound to its isolated kernel (CU_PARTITION), the GO-Kernel of
+    // CD class P (CU_PARTITION_GO) or the kernel tuned under the
+    // partition's CU budget (CU_PARTITION_RC, Sec. 6.9)
+    const int r = partition_index(forced_cd, L);
+    const int P = kParts[r];
+    for (int t = 0; t < L; ++t) {
+      const int i = live[t];
+      p->order[t] = i;
+      p->group_of[i] = 0;
+      p->stream_of[i] = t % P;
+      p->dispatch_of[i] = t;
+      p->variant_of[i] = mode == GDY_CU_PARTITION      ? bind_variant(ctx, g[i], 0, &fb)
+                         : mode == GDY_CU_PARTITION_GO ? bind_variant(ctx, g[i], class_for_size(P), &fb)
+                                                       : bind_partition(ctx, g[i], r, &fb);
+    }
+    p->n_groups = L > 0 ? 1 : 0;
+    p->group_size[0] = L;
+    p->n_dispatches = L;
+    p->cd = L > 0 ? P : 0;
+    p->fallback = (fb || !ctx->table.loaded) ? 1 : 0;
     return;
   }
 
@@ -818,9 +875,18 @@ gdy_status build_launch(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p,
   return GDY_OK;
 }
 
-gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, hipStream_t origin) {
+gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, int mode,
+                       hipStream_t origin) {
   gdy_status st = GDY_OK;
   const int n = p.n;
+  // stream slots: the pool (or the active CU budget's pool), or the CU
+  // partitions of a CU-Partition launch
+  const bool parted = partition_mode(mode);
+  const int pr = parted ? partition_index(p.cd, 0) : 0;
+  if (parted && p.n_dispatches > 0 && ((int)ctx->parts.size() <= pr || ctx->parts[pr].empty()))
+    return fail(ctx, GDY_ERR_UNSUPPORTED, "no CU partitions: create the context with use_cu_masks & 2");
+  auto stream_at = [&](int s) { return parted ? ctx->parts[pr][s] : slot_stream(ctx, s); };
+  auto done_at = [&](int s) { return parted ? ctx->part_done[pr][s] : ctx->done[s]; };
   int L = 0;
   while (L < GDY_MAX_GEMMS && p.order[L] >= 0) ++L;
   const int D = p.n_dispatches;
@@ -865,7 +931,7 @@ gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, hip
     // fork: pool streams start after what the origin holds
     if (!slots.empty()) {
       HIP_TRY(ctx, hipEventRecord(ctx->fork_ev, origin));
-      for (int s : slots) HIP_TRY(ctx, hipStreamWaitEvent(slot_stream(ctx, s), ctx->fork_ev, 0));
+      for (int s : slots) HIP_TRY(ctx, hipStreamWaitEvent(stream_at(s), ctx->fork_ev, 0));
     }
     for (size_t u = 0; u < ids.size(); ++u) {
       int i0 = members[u][0];  // the dispatch runs its first GEMM's kernel (adds ride along)
@@ -882,7 +948,7 @@ gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, hip
       if (st != GDY_OK) break;
       void* argv[] = {&launch};
       const int d = ids[u];
-      hipStream_t hs = p.stream_of[i0] >= 0 ? slot_stream(ctx, p.stream_of[i0]) : origin;
+      hipStream_t hs = p.stream_of[i0] >= 0 ? stream_at(p.stream_of[i0]) : origin;
       hipError_t e = hipExtLaunchKernel(k.d->func, dim3(grid), dim3(k.d->waves * 64), argv, 0, hs,
                                         ts ? ts->start[d] : nullptr, ts ? ts->stop[d] : nullptr, 0);
       if (e != hipSuccess) {
@@ -894,8 +960,8 @@ gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, hip
     }
     // join: the origin continues after the group's pool streams
     for (int s : slots) {
-      HIP_TRY(ctx, hipEventRecord(ctx->done[s], slot_stream(ctx, s)));
-      HIP_TRY(ctx, hipStreamWaitEvent(origin, ctx->done[s], 0));
+      HIP_TRY(ctx, hipEventRecord(done_at(s), stream_at(s)));
+      HIP_TRY(ctx, hipStreamWaitEvent(origin, done_at(s), 0));
     }
   }
   return st;
@@ -968,6 +1034,20 @@ gdy_status load_table(gdy_ctx* ctx, const char* path) {
           return fail(ctx, GDY_ERR_TABLE, "variant %s does not match its entry", name.c_str());
         e.v[c] = vid;
       }
+      // optional: the best kernels under 128, 64 and 32 CUs (CU partitions)
+      std::string rname;
+      for (int r = 0; r < 3 && (in >> rname); ++r) {
+        int vid = -1;
+        for (size_t v = 0; v < ctx->variants.size(); ++v)
+          if (ctx->variants[v].name == rname) vid = (int)v;
+        if (vid < 0) return fail(ctx, GDY_ERR_TABLE, "GO table names unknown variant %s", rname.c_str());
+        const KernelDesc* d = ctx->kernels[ctx->variants[vid].kernel].d;
+        if (d->ew || d->dtype != e.dtype || d->ta != e.ta || d->tb != e.tb)
+          return fail(ctx, GDY_ERR_TABLE, "variant %s does not match its entry", rname.c_str());
+        e.rc[r] = vid;
+        if (r == 2 && (in >> rname)) return fail(ctx, GDY_ERR_TABLE, "bad entry line: %s", line.c_str());
+      }
+      if (e.rc[0] >= 0 && e.rc[2] < 0) return fail(ctx, GDY_ERR_TABLE, "bad entry line: %s", line.c_str());
       e.ln = std::log2((double)e.n);
       e.lk = std::log2((double)e.k);
       if (e.dtype < 1 || e.dtype > 4 || (e.ta & ~1) || (e.tb & ~1))
@@ -1017,6 +1097,10 @@ static void destroy_streams(gdy_ctx* ctx) {
   for (auto& pl : ctx->rc_pools)
     for (hipStream_t s : pl) (void)hipStreamDestroy(s);
   for (hipEvent_t e : ctx->done) (void)hipEventDestroy(e);
+  for (auto& pl : ctx->parts)
+    for (hipStream_t s : pl) (void)hipStreamDestroy(s);
+  for (auto& ev : ctx->part_done)
+    for (hipEvent_t e : ev) (void)hipEventDestroy(e);
   for (TimingSlot& t : ctx->ring) {
     for (hipEvent_t e : t.start) (void)hipEventDestroy(e);
     for (hipEvent_t e : t.stop) (void)hipEventDestroy(e);
@@ -1026,6 +1110,8 @@ static void destroy_streams(gdy_ctx* ctx) {
   if (ctx->fork_ev) (void)hipEventDestroy(ctx->fork_ev);
   ctx->pool.clear();
   ctx->rc_pools.clear();
+  ctx->parts.clear();
+  ctx->part_done.clear();
   ctx->done.clear();
   ctx->fork_ev = nullptr;
 }
@@ -1129,7 +1215,31 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
     HIP_TRY(ctx, hipEventCreateWithFlags(&e, hipEventDisableTiming));
     ctx->done.push_back(e);
   }
-  if (use_cu_masks) {
+  if (use_cu_masks & 2) {
+    // CU-Partition: for P = 2, 4, 8, P streams whose masks split the CUs
+    // into P disjoint runs of consecutive mask bits, each a multiple of 8
+    // bits (bit i is a CU of XCD i mod 8 in the runtime's numbering, so a
+    // run covers the same number of CUs on every XCD)
+    const int words = (ctx->cus + 31) / 32;
+    for (int P : kParts) {
+      std::vector<hipStream_t> pl;
+      std::vector<hipEvent_t> ev;
+      const int per = ctx->cus / P;
+      for (int q = 0; q < P; ++q) {
+        std::vector<uint32_t> mask(words, 0u);
+        for (int cu = q * per; cu < (q + 1) * per; ++cu) mask[cu / 32] |= 1u << (cu % 32);
+        hipStream_t st;
+        HIP_TRY(ctx, hipExtStreamCreateWithCUMask(&st, (uint32_t)words, mask.data()));
+        pl.push_back(st);
+        hipEvent_t e;
+        HIP_TRY(ctx, hipEventCreateWithFlags(&e, hipEventDisableTiming));
+        ev.push_back(e);
+      }
+      ctx->parts.push_back(pl);
+      ctx->part_done.push_back(ev);
+    }
+  }
+  if (use_cu_masks & 1) {
     // One stream per resource constraint: only isolated runs use them.  A CU
     // mask belongs to a hardware queue, and HIP shares queues between streams
     // once GPU_MAX_HW_QUEUES is reached, so every extra masked stream risks
@@ -1186,6 +1296,8 @@ void gdy_destroy(gdy_ctx* ctx) {
   for (hipStream_t s : ctx->pool) (void)hipStreamSynchronize(s);
   for (auto& pl : ctx->rc_pools)
     for (hipStream_t s : pl) (void)hipStreamSynchronize(s);
+  for (auto& pl : ctx->parts)
+    for (hipStream_t s : pl) (void)hipStreamSynchronize(s);
   destroy_streams(ctx);
   delete ctx;
 }
@@ -1211,6 +1323,8 @@ gdy_status gdy_plan(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode
   try {
     gdy_status s = validate(ctx, gemms, n, mode);
     if (s != GDY_OK) return s;
+    if (partition_mode(mode) && forced_cd != 0 && forced_cd != 2 && forced_cd != 4 && forced_cd != 8)
+      return fail(ctx, GDY_ERR_INVALID_ARG, "CU-Partition takes 2, 4 or 8 partitions, not %d", forced_cd);
     make_plan(ctx, gemms, n, mode, forced_cd, out);
   } catch (...) {
     return fail(ctx, GDY_ERR_NOMEM, "host allocation failed");
@@ -1232,7 +1346,7 @@ gdy_status gdy_execute(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t m
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess || cur != ctx->device) HIP_TRY(ctx, hipSetDevice(ctx->device));
   try {
-    return launch_plan(ctx, gemms, *p, (hipStream_t)hip_stream);
+    return launch_plan(ctx, gemms, *p, mode, (hipStream_t)hip_stream);
   } catch (...) {
     return fail(ctx, GDY_ERR_NOMEM, "host allocation failed");
   }

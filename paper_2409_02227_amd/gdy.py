@@ -23,9 +23,14 @@ CD_CLASSES = (1, 2, 4, 8, 16)
 F16, BF16, FP8_E4M3, F32 = 1, 2, 3, 4
 # gdy_mode
 SEQUENTIAL, DEFAULT, GO, SELECTOR, FORCED, FORCED_GROUPED = 0, 1, 2, 3, 4, 5
+CU_PARTITION, CU_PARTITION_GO, CU_PARTITION_RC = 6, 7, 8
 GEMM, ADD = 0, 1  # gdy_op
 MODES = {"sequential": SEQUENTIAL, "default": DEFAULT, "go": GO,
-         "selector": SELECTOR, "forced": FORCED, "forced_grouped": FORCED_GROUPED}
+         "selector": SELECTOR, "forced": FORCED, "forced_grouped": FORCED_GROUPED,
+         "cu_partition": CU_PARTITION, "cu_partition_go": CU_PARTITION_GO,
+         "cu_partition_rc": CU_PARTITION_RC}
+# gdy_create use_cu_masks bits
+RC_STREAMS, PARTITION_STREAMS = 1, 2
 
 STATUS = {0: "GDY_OK", 1: "GDY_ERR_INVALID_ARG", 2: "GDY_ERR_UNSUPPORTED", 3: "GDY_ERR_ALIAS",
           4: "GDY_ERR_TOO_MANY", 5: "GDY_ERR_TABLE", 6: "GDY_ERR_HIP", 7: "GDY_ERR_NOMEM"}
@@ -239,7 +244,7 @@ class Context:
     """A libgdy context on one device (see gdy_create)."""
 
     def __init__(self, device: int = 0, table: str | None = None, max_streams: int = 16,
-                 use_cu_masks: bool = False):
+                 use_cu_masks: int = 0):
         self.lib = load_library()
         h = ctypes.c_void_p()
         st = self.lib.gdy_create(ctypes.byref(h), device,

@@ -259,6 +259,11 @@ def write_table(path, ctx, records, lr=None, lr_by_type=None):
         dtype, ta, tb, m, n, k = r["shape"][:6]
         mlog = max(0, math.ceil(math.log2(max(m, 1))))
         names = [r["go"][str(cd)] for cd in CDS]
+        # the best kernel under each resource constraint: the kernels of the
+        # CU-Partition modes (a partition of 2, 4, 8 holds 128, 64, 32 CUs)
+        rc = r.get("rc_best", {})
+        if all(str(b) in rc for b in RCS[1:]):
+            names += [rc[str(b)][0] for b in RCS[1:]]
         lines.append(f"entry {DT_CODE[dtype]} {ta} {tb} {mlog} {n} {k} " + " ".join(names))
     with open(path, "w") as f:
         f.write("\n".join(lines) + "\n")
@@ -372,7 +377,7 @@ def main(argv=None):
 
     import torch
     from paper_2409_02227_amd import gdy
-    ctx = gdy.Context(0, max_streams=16, use_cu_masks=True)
+    ctx = gdy.Context(0, max_streams=16, use_cu_masks=gdy.RC_STREAMS)
     variants = ctx.variants()
     bench = Bench(ctx, torch)
     records, done = [], set()

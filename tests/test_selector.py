@@ -148,6 +148,8 @@ def _synthetic_table(path, ctx, rng):
                 for n in (1024, 8192):
                     for k in (1024, 8192):
                         names = [pool[int(rng.integers(len(pool)))] for _ in range(5)]
+                        if rng.random() < 0.5:  # kernels tuned for 128, 64 and 32 CUs
+                            names += [pool[int(rng.integers(len(pool)))] for _ in range(3)]
                         lines.append(f"entry {dtype} {ta} {tb} {mlog} {n} {k} " + " ".join(names))
     with open(path, "w") as f:
         f.write("\n".join(lines) + "\n")
@@ -312,3 +314,67 @@ def test_add_rides_with_the_first_group(tmp_path):
             assert p["n_groups"] == 3 and p["group_size"][:3] == [2, 1, 1]
         assert p["group_of"][1] == 0 and p["dispatch_of"][1] == p["dispatch_of"][p["order"][0]]
         _check_plan(ctx, table, descs)
+
+
+# --------------------------------------------------------------------------
+# CU-Partition (Sec. 5.5, Sec. 6.9)
+# --------------------------------------------------------------------------
+
+def test_partition_plans_match_oracle(tmp_path):
+    rng = np.random.default_rng(11)
+    probe = gdy.Context(-1)
+    path = str(tmp_path / "p.table")
+    _synthetic_table(path, probe, rng)
+    ctx = gdy.Context(-1, table=path)
+    table = sel.parse_table(path)
+    assert any(e["partition"] for e in table["entries"]) and not all(e["partition"] for e in table["entries"])
+    V = ctx.variants()
+    kinds = {"cu_partition": "isolated", "cu_partition_go": "go", "cu_partition_rc": "rc"}
+    for _ in range(30):
+        descs = _random_set(rng, int(rng.integers(1, 13)))
+        for mode, kind in kinds.items():
+            for forced in (0, 2, 4, 8):
+                p = ctx.plan(descs, mode=mode, forced_cd=forced)
+                want = sel.plan_partition([_as_dict(d) for d in descs], table, V, kind, forced)
+                live = want["order"]
+                assert p["order"] == live and p["cd"] == (want["P"] if live else 0)
+                assert p["n_dispatches"] == len(live) and p["n_groups"] == (1 if live else 0)
+                for t, i in enumerate(live):
+                    assert p["stream_of"][i] == want["stream_of"][i] == t % want["P"]
+                    assert p["dispatch_of"][i] == t
+                    assert p["variant_of"][i] == want["variant_of"][i], (mode, forced, i)
+
+
+def test_partition_counts_and_errors(tmp_path):
+    assert [sel.partition_count(0, n) for n in (0, 1, 2, 3, 4, 5, 8, 9, 30)] == [2, 2, 2, 4, 4, 8, 8, 8, 8]
+    assert [sel.partition_count(f, 30) for f in (2, 4, 8)] == [2, 4, 8]
+    ctx = gdy.Context(-1, table=TABLE if os.path.exists(TABLE) else None)
+    descs = [_desc(512, 4096, 1024, 2, 0, 0, (i + 1) << 37) for i in range(3)]
+    with pytest.raises(gdy.GdyError) as e:
+        ctx.plan(descs, mode="cu_partition", forced_cd=3)
+    assert e.value.status == 1
+    # the tuned table names a kernel per CU budget for every entry
+    if os.path.exists(TABLE):
+        table = sel.parse_table(TABLE)
+        assert all(e["partition"] for e in table["entries"])
+        V = ctx.variants()
+        p = ctx.plan(descs, mode="cu_partition_rc", forced_cd=4)
+        want = sel.plan_partition([_as_dict(d) for d in descs], table, V, "rc", 4)
+        assert [p["variant_of"][i] for i in range(3)] == [want["variant_of"][i] for i in range(3)]
+
+
+def test_partition_kernels_in_table_lines(tmp_path):
+    """An entry names 5 GO-Kernels and optionally 3 partition kernels; any
+    other count is rejected."""
+    probe = gdy.Context(-1)
+    V = [v["name"] for v in probe.variants() if v["kind"] == 0 and v["dtype"] == 2
+         and v["trans_a"] == 0 and v["trans_b"] == 0]
+    head = ["gdy-go-table 1", "device host cus 256", f"catalogue {probe.catalogue_hash():016x}"]
+    for extra, ok in ((0, True), (3, True), (1, False), (2, False), (4, False)):
+        path = tmp_path / f"e{extra}.table"
+        path.write_text("\n".join(head + ["entry 2 0 0 9 4096 1024 " + " ".join(V[:5 + extra])]) + "\n")
+        if ok:
+            gdy.Context(-1, table=str(path)).close()
+        else:
+            with pytest.raises(gdy.GdyError):
+                gdy.Context(-1, table=str(path))
