@@ -28,6 +28,8 @@ PEAK_TFLOPS = {"bf16": 2516.6, "f16": 2516.6, "fp8": 5033.2, "f32": 157.3}  # MI
 PEAK_HBM_GBS = 8000.0
 METRIC = "aggregate TFLOP/s of concurrent GEMM sets; speedup vs sequential; % MFMA peak"
 DEFAULT_TABLE = os.path.join(ROOT, "paper_2409_02227_amd", "tables", "gfx950.table")
+RECORDS = os.path.join(ROOT, "paper_2409_02227_amd", "tables", "gfx950_records.jsonl")
+KNN_TABLE = os.path.join(ROOT, "paper_2409_02227_amd", "tables", "gfx950_knn.table")
 
 WORKLOADS = {
     "tp8_layer_share": (3, "8 bf16 GEMMs: QKV (512,4608,12288), out-proj (512,12288,1536), "
@@ -46,6 +48,8 @@ WORKLOADS = {
                                 "output (2P GEMM + non-GEMM co-runs)"),
     "cu_partition": ("parts", "P copies of each of 8 bf16 GEMMs (P = 2, 4, 8) on P CU partitions "
                               "(CU-masked streams) and unpartitioned"),
+    "knn_tuning": ("knn", "CD copies (CD = 2, 4, 8, 16) of 40 bf16 shapes whose GO-Kernels a KNN "
+                          "table predicts from the 20% of shapes tuned exhaustively"),
 }
 PARTITION_SHAPES = ((4096, 1024, 1024), (8192, 1024, 512), (2048, 2048, 2048), (4096, 4096, 1024),
                     (1024, 4096, 4096), (512, 8192, 8192), (256, 4096, 4096), (64, 8192, 2048))
@@ -103,6 +107,8 @@ def parse():
                     help="only run a plain 1 GiB device copy 10 times (HBM counter calibration)")
     ap.add_argument("--submissions", type=int, default=24,
                     help="heterogeneous workload: number of seeded submissions timed")
+    ap.add_argument("--knn-table", default=KNN_TABLE,
+                    help="knn_tuning workload: GO table built by tuner --knn from the same records")
     return ap.parse_args()
 
 
@@ -337,6 +343,57 @@ def partition_bench(args, desc):
     print(json.dumps(out), flush=True)
 
 
+def knn_bench(args, desc):
+    """Sec. 7.5: shapes outside the exhaustively tuned 20% (bf16, A and B
+    row-major, every fifth), CD copies each, under default concurrency, GO
+    with the exhaustively tuned table and GO with the KNN table; per CD the
+    geomean speedup over default and of the KNN table over the exhaustive
+    one.  value: aggregate TFLOP/s of GO with the KNN table."""
+    import torch
+    from paper_2409_02227_amd import gdy, tuner
+    if not args.knn_table or not os.path.exists(args.knn_table):
+        raise SystemExit("knn_tuning needs --knn-table (tuner --knn FRAC --records ... --out TABLE)")
+    recs = [json.loads(line) for line in open(RECORDS)]
+    tuned = set(tuner.knn_split(recs, 0.2, 0))
+    shapes = [tuple(r["shape"]) for i, r in enumerate(recs)
+              if i not in tuned and r["shape"][:3] == ["bf16", 0, 0] and len(r["shape"]) == 6]
+    shapes = shapes[::max(1, len(shapes) // 40)][:40]
+    full = gdy.Context(0, table=args.table, max_streams=16)
+    knn = gdy.Context(0, table=args.knn_table, max_streams=16)
+    handle = gdy._stream_handle(None)
+    gen = torch.Generator(device="cuda").manual_seed(75)
+    res, tot_f, tot_t = {}, 0.0, 0.0
+    for cd in (2, 4, 8, 16):
+        t_def, t_full, t_knn = [], [], []
+        for (_, _, _, m, n, k) in shapes:
+            gem = []
+            for _c in range(cd):
+                a = (torch.rand(m, k, device="cuda", generator=gen) * 2 - 1).to(torch.bfloat16)
+                b = (torch.randn(k, n, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+                gem.append(gdy.Gemm(a, b, torch.empty(m, n, dtype=torch.bfloat16, device="cuda")))
+            arr = gdy.descs(gem)
+            t_def.append(time_steps(full, arr, cd, "default", args.steps, 2, handle, torch))
+            t_full.append(time_steps(full, arr, cd, "go", args.steps, 2, handle, torch))
+            t_knn.append(time_steps(knn, arr, cd, "go", args.steps, 2, handle, torch))
+            tot_f += cd * 2.0 * m * n * k
+            tot_t += t_knn[-1]
+            del gem, arr
+        gm = lambda a, b: round(float(np.exp(np.mean(np.log(np.array(a) / np.array(b))))), 4)
+        res[cd] = {"go_full_over_default": gm(t_def, t_full), "go_knn_over_default": gm(t_def, t_knn),
+                   "go_knn_over_go_full": gm(t_full, t_knn)}
+    value = tot_f / tot_t / 1e12
+    out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": 2, "ms_per_step": round(1e3 * tot_t / (4 * len(shapes)), 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (seeded device draws; A ~ U[-1,1], B ~ N(0, 0.02))",
+           "config": {"workload": f"knn_tuning: {desc}", "mode": "go", "shapes": len(shapes),
+                      "table": os.path.relpath(args.table, ROOT),
+                      "knn_table": os.path.relpath(args.knn_table, ROOT)},
+           "geomean_speedups": res,
+           "pct_mfma_peak": round(100 * value / PEAK_TFLOPS["bf16"], 2)}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -356,6 +413,8 @@ def main():
         return pairs_bench(args, desc)
     if cfg_id == "parts":
         return partition_bench(args, desc)
+    if cfg_id == "knn":
+        return knn_bench(args, desc)
     if cfg_id == "3nt":
         specs = inputs.config3(trans_b=1)
     elif cfg_id == "3f32":

@@ -18,6 +18,12 @@ On MI355X the RCs are CU-masked stream pools of 128, 64 and 32 CUs; the
 kernel list is the library's catalogue (tiles x grid caps).  Timings follow
 Sec. 5.3: copies run back-to-back on each stream, several rounds.
 
+Sec. 7.5 cuts the tuning cost: tune a fraction of the shapes exhaustively
+and, for the others, predict each CD's preferred RC (whose candidate wins
+the CD step) by K-nearest neighbours over M*N and the default kernel's tile
+size; a predicted shape needs its isolated sweep and the predicted RCs'
+sweeps only, no CD step (``--knn FRAC`` builds such a table from records).
+
 Usage (on the GPU):  python -m paper_2409_02227_amd.tuner --out TABLE
 """
 from __future__ import annotations
@@ -43,6 +49,7 @@ DT_CODE = {"f16": 1, "bf16": 2, "fp8": 3, "f32": 4}
 BEST_CD_GAIN = 1.05     # Sec. 5.5: sequential unless a CD gives >= 5%
 LABEL_TOL = 0.03        # CDs within 3% of the best speedup count as equally good
 MIN_TYPE_RECORDS = 20   # an input type gets its own predictor from this many tuned shapes
+KNN_K = 3               # neighbours of the preferred-RC vote (Sec. 7.5)
 
 
 # ---------------------------------------------------------------------------
@@ -325,6 +332,118 @@ def train_lr(X, y, seed=0):
             "n_train": len(train), "n_test": len(test), "test": test, "train": train}
 
 
+# ---------------------------------------------------------------------------
+# Sec. 7.5: preferred-RC prediction for untuned shapes
+# ---------------------------------------------------------------------------
+
+def candidate_slots(rec) -> list:
+    """The CD step's seven candidates in a fixed order: the isolated best,
+    then per RC (128, 64, 32 CUs) its best tile uncapped and capped to the
+    RC.  A slot's RC is (slot + 1) // 2 into RCS (slot 0: none)."""
+    names = [rec["rc_best"]["0"][0]]
+    for rc in RCS[1:]:
+        tile = rec["rc_best"][str(rc)][0].rsplit("_c", 1)[0]
+        names += [f"{tile}_c0", f"{tile}_c{rc}"]
+    return names
+
+
+def preferred_slot(rec, cd: int) -> int:
+    """Preferred RC of a tuned shape for one CD: the first candidate slot
+    holding its GO-Kernel."""
+    return candidate_slots(rec).index(rec["go"][str(cd)])
+
+
+def knn_features(records, variants) -> np.ndarray:
+    """log2 of the output size (all items of a batch) and of the default
+    kernel's tile area, per record."""
+    area = {v["name"]: v["bm"] * v["bn"] for v in variants}
+    rows = []
+    for r in records:
+        m, n = r["shape"][3], r["shape"][4]
+        items = max(r["shape"][6], 1) if len(r["shape"]) > 6 else 1
+        rows.append([np.log2(float(m) * n * items), np.log2(float(area[r["rc_best"]["0"][0]]))])
+    return np.array(rows, dtype=np.float64)
+
+
+def knn_vote(tx: np.ndarray, ty: np.ndarray, x: np.ndarray, k: int = KNN_K) -> int:
+    """Majority slot of the k nearest tuned shapes (ordered by distance, then
+    position); vote ties to the smallest slot."""
+    d = np.sqrt(((tx - x) ** 2).sum(axis=1))
+    near = np.lexsort((np.arange(len(d)), d))[:k]
+    counts = np.bincount(ty[near], minlength=7)
+    return int(np.flatnonzero(counts == counts.max())[0])
+
+
+def knn_split(records, frac: float, seed: int = 0) -> list:
+    """Indices of the shapes tuned exhaustively: a seeded `frac` of each
+    (input type, layout) group, at least one per group."""
+    rng = np.random.default_rng(seed)
+    groups = {}
+    for i, r in enumerate(records):
+        groups.setdefault(tuple(r["shape"][:3]), []).append(i)
+    tuned = []
+    for key in sorted(groups, key=str):
+        idx = groups[key]
+        take = max(1, int(math.ceil(frac * len(idx))))
+        tuned += sorted(rng.choice(idx, size=take, replace=False).tolist())
+    return sorted(tuned)
+
+
+def tuning_cost(rec, variants, rcs) -> int:
+    """GEMM executions a shape's tuning times: the isolated sweep, the
+    sweeps of the RCs in `rcs`, and (when `rcs` is all of them) the CD step
+    (per CD: the sequential run and every candidate, CD copies each)."""
+    dtype, ta, tb, m = rec["shape"][:4]
+    cands = candidates(variants, DT_CODE[dtype], ta, tb, m)
+    uncapped = [v for v in cands if variants[v]["grid_cap_cus"] == 0]
+    cost = len(cands) + len(rcs) * len(uncapped)
+    if len(rcs) == len(RCS) - 1:
+        cost += sum((1 + len(rec["pool"])) * cd for cd in CDS[1:])
+    return cost
+
+
+def knn_records(records, variants, frac: float, seed: int = 0, k: int = KNN_K):
+    """Records as tuning with preferred-RC prediction would leave them: the
+    tuned fraction unchanged; every other shape keeps its isolated kernel and
+    RC sweeps, and takes for each CD the candidate of the RC its neighbours
+    prefer (marked "predicted", no label).  Returns (records, stats)."""
+    tuned = knn_split(records, frac, seed)
+    tset = set(tuned)
+    x = knn_features(records, variants)
+    out, hits, cost, full = [], {cd: 0 for cd in CDS[1:]}, 0, 0
+    slots_of = {}
+    for i, r in enumerate(records):
+        full += tuning_cost(r, variants, RCS[1:])
+        if i in tset:
+            out.append(r)
+            cost += tuning_cost(r, variants, RCS[1:])
+            continue
+        group = [j for j in tuned if records[j]["shape"][:3] == r["shape"][:3]]
+        pool = group if len(group) >= k else tuned
+        q = dict(r)
+        q["go"] = {"1": r["go"]["1"]}
+        names = candidate_slots(r)
+        used = set()
+        for cd in CDS[1:]:
+            ty = np.array([preferred_slot(records[j], cd) for j in pool])
+            slot = knn_vote(x[pool], ty, x[i], k)
+            q["go"][str(cd)] = names[slot]
+            hits[cd] += names[slot] == r["go"][str(cd)]
+            if slot > 0:
+                used.add(RCS[(slot + 1) // 2])
+            slots_of.setdefault(cd, []).append(slot)
+        for key in ("label", "speedup", "conc", "seq"):
+            q.pop(key, None)
+        q["predicted"] = True
+        out.append(q)
+        cost += tuning_cost(r, variants, sorted(used))
+    n_pred = len(records) - len(tuned)
+    stats = {"tuned": len(tuned), "predicted": n_pred, "k": k, "seed": seed,
+             "same_kernel_as_exhaustive": {str(cd): hits[cd] / max(n_pred, 1) for cd in CDS[1:]},
+             "tuning_cost_fraction": cost / full}
+    return out, stats
+
+
 def label_of(speedup: dict, tol: float = LABEL_TOL) -> int:
     """Sec. 4.3 label with the Sec. 5.5 threshold: the CD with the most
     speedup over sequential, or 1 when no CD gains 5%.  Speedups within
@@ -373,6 +492,10 @@ def main(argv=None):
     ap.add_argument("--limit", type=int, default=0)
     ap.add_argument("--retrain", action="store_true",
                     help="no timing: rebuild the table and predictor from --records")
+    ap.add_argument("--knn", type=float, default=0.0,
+                    help="no timing: from --records, keep this fraction as exhaustively tuned and "
+                         "predict the other shapes' GO-Kernels by preferred-RC KNN (Sec. 7.5)")
+    ap.add_argument("--knn-seed", type=int, default=0)
     args = ap.parse_args(argv)
 
     import torch
@@ -389,9 +512,9 @@ def main(argv=None):
     shapes = shape_set(args.shapes)
     if args.limit:
         shapes = shapes[:args.limit]
-    if args.retrain:
+    if args.retrain or args.knn:
         if not records:
-            raise SystemExit("--retrain needs --records with tuned shapes")
+            raise SystemExit("--retrain / --knn need --records with tuned shapes")
         shapes = [tuple(r["shape"]) for r in records]
     t0 = time.time()
     for i, s in enumerate(shapes):
@@ -407,8 +530,13 @@ def main(argv=None):
               f"sp={ {c: round(v, 2) for c, v in r['speedup'].items()} }", flush=True)
         torch.cuda.empty_cache()
     records = [r for r in records if tuple(r["shape"]) in set(map(tuple, shapes))]
+    knn_stats = None
+    if args.knn:
+        records, knn_stats = knn_records(records, variants, args.knn, args.knn_seed)
     write_table(args.out, ctx, records)           # GO mapping first: features depend on it
     ctx2 = gdy.Context(0, table=args.out, max_streams=16)
+    # the predictor learns from shapes with measured labels only
+    records_all, records = records, [r for r in records if not r.get("predicted")]
     X, y = feature_rows(ctx2, records)
     lr = train_lr(X, y)
     # one predictor per input type with enough records of its own (precision
@@ -421,7 +549,7 @@ def main(argv=None):
             m = train_lr(X[idx], y[idx])
             m["test"], m["train"] = idx[m["test"]], idx[m["train"]]
             per[code] = m
-    write_table(args.out, ctx, records, lr, per)
+    write_table(args.out, ctx, records_all, lr, per)
     test = np.concatenate([per[c]["test"] if c in per else
                            np.intersect1d(lr["test"], np.where(codes == c)[0])
                            for c in sorted(set(codes.tolist()))])
@@ -432,6 +560,8 @@ def main(argv=None):
                             for c in sorted(set(codes.tolist()))},
                "by_available_test": evaluate(records, X, lr, test, per),
                "by_available_all": evaluate(records, X, lr, np.arange(len(records)), per)}
+    if knn_stats:
+        summary["knn"] = knn_stats
     print(json.dumps(summary), flush=True)
     with open(os.path.splitext(args.out)[0] + "_summary.json", "w") as f:
         json.dump(summary, f, indent=1)
