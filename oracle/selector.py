@@ -267,6 +267,26 @@ def roofline_seconds(g: dict) -> float:
     return max(mfma, items * bytes_ / 8e12)
 
 
+def one_shape(members: list) -> bool:
+    """All GEMMs (adds aside) of one shape, type, layout and batch."""
+    keys = {(g["m"], g["n"], g["k"], g["a_type"], g["trans_a"], g["trans_b"], max(g.get("batch", 0), 1))
+            for g in members if g.get("op", 0) != 1}
+    return len(keys) <= 1
+
+
+def uncapped(vid: int, variants: list) -> int:
+    """The same kernel without a grid cap.  Reading used for heterogeneous
+    groups (the paper's GO-Kernels are tuned on copies of one GEMM and are
+    heterogeneity-agnostic, Sec. 6.7): a group whose GEMMs differ runs every
+    kernel uncapped, since a cap tuned for co-runners that finish together
+    keeps a GEMM on its CU share after different co-runners finish."""
+    name = kernel_of(variants[vid]["name"])
+    for w, u in enumerate(variants):
+        if kernel_of(u["name"]) == name and u["grid_cap_cus"] == 0:
+            return w
+    raise LookupError(f"no uncapped variant of {variants[vid]['name']}")
+
+
 def kernel_of(name: str) -> str:
     return name.rsplit("_c", 1)[0]
 
@@ -390,8 +410,10 @@ def plan_selector(gemms: list, table: dict, variants: list, cus: int, slots: int
     for grp, s in zip(groups, taken):
         ci = class_for_size(max(1, s))
         parts = {}  # kernel -> GEMMs, in order of first appearance
+        mixed = not one_shape([gemms[i] for i in grp])
         for i in grp:
-            out["variant_of"][i] = bind(gemms[i], ci, table, variants, by_name)
+            v = bind(gemms[i], ci, table, variants, by_name)
+            out["variant_of"][i] = uncapped(v, variants) if mixed else v
             parts.setdefault(kernel_of(variants[out["variant_of"][i]]["name"]), []).append(i)
         # inside a dispatch: K descending, then M*N; dispatches: total 2MNK
         # descending, adds after every GEMM

@@ -378,3 +378,29 @@ def test_partition_kernels_in_table_lines(tmp_path):
         else:
             with pytest.raises(gdy.GdyError):
                 gdy.Context(-1, table=str(path))
+
+
+def test_mixed_groups_run_uncapped(tmp_path):
+    """Copies of one shape keep the tuned GO-Kernels (caps included); a group
+    of different shapes runs the same kernels without grid caps."""
+    path = _fixed_cd_table(tmp_path, "cd16", 4)  # every GEMM prefers CD 16: one group
+    ctx = gdy.Context(-1, table=path)
+    table = sel.parse_table(path)
+    V = ctx.variants()
+    by_name = {v["name"]: i for i, v in enumerate(V)}
+    same = [_desc(512, 4096, 1024, 2, 0, 0, (i + 1) << 37) for i in range(4)]
+    p = ctx.plan(same, mode="selector")
+    assert p["n_groups"] == 1
+    want = sel.bind(_as_dict(same[0]), sel.class_for_size(4), table, V, by_name)
+    assert all(p["variant_of"][i] == want for i in range(4))
+    mixed = same[:3] + [_desc(700, 4096, 1024, 2, 0, 0, 9 << 37)]
+    p = ctx.plan(mixed, mode="selector")
+    assert p["n_groups"] == 1
+    for i, d in enumerate(mixed):
+        bound = sel.bind(_as_dict(d), sel.class_for_size(4), table, V, by_name)
+        got = V[p["variant_of"][i]]
+        assert got["grid_cap_cus"] == 0 and sel.kernel_of(got["name"]) == sel.kernel_of(V[bound]["name"])
+    _check_plan(ctx, table, mixed)
+    # GO mode follows the same rule
+    p = ctx.plan(mixed, mode="go")
+    assert all(V[p["variant_of"][i]]["grid_cap_cus"] == 0 for i in range(4))
