@@ -287,6 +287,57 @@ def uncapped(vid: int, variants: list) -> int:
     raise LookupError(f"no uncapped variant of {variants[vid]['name']}")
 
 
+UNIFY_US = 100.0  # roofline time per extra kernel below which a group shares one kernel
+
+
+def group_cost(v: dict, members: list, cus: int) -> float:
+    """Estimated time of `members` fused on one kernel: each tile costs
+    max(tile area / 128, tile perimeter) per K (the isolated heuristic's
+    tile model) plus its area once (the stores), tiles pack into CUs x
+    occupancy slots, direct kernels 1.5x faster."""
+    per = max(v["bm"] * float(v["bn"]) / 128.0, float(v["bm"] + v["bn"]))
+    f = 0.0
+    for g in members:
+        tiles = -(-g["m"] // v["bm"]) * -(-g["n"] // v["bn"]) * max(g.get("batch", 0), 1)
+        f += float(tiles) * (float(g["k"]) * per + v["bm"] * float(v["bn"]))
+    slots = float(cus) * float(max(v["occupancy"], 1))
+    return f / slots / (1.5 if v["direct"] else 1.0)
+
+
+def unify_short_group(grp: list, gemms: list, variant_of: dict, variants: list, cus: int) -> None:
+    """A library launch rule, not the paper's: a group whose GEMMs use
+    several kernels forks one stream per extra kernel.  When the group's
+    roofline time is below UNIFY_US per extra kernel, every GEMM takes the
+    one group kernel that all of them can run (same type and layout; direct
+    kernels only where the GEMM meets their requirements) at the least
+    group_cost, uncapped, so the group is one dispatch."""
+    kern, t = [], 0.0
+    for i in grp:
+        if gemms[i].get("op", 0) == 1:
+            continue
+        t += roofline_seconds(gemms[i])
+        v = uncapped(variant_of[i], variants)
+        if v not in kern:
+            kern.append(v)
+    if len(kern) < 2 or t >= UNIFY_US * 1e-6 * (len(kern) - 1):
+        return
+    best, best_f = None, 0.0
+    for v in kern:
+        u = variants[v]
+        members = [gemms[i] for i in grp if gemms[i].get("op", 0) != 1]
+        if not all(u["dtype"] == g["a_type"] and u["trans_a"] == g["trans_a"] and u["trans_b"] == g["trans_b"]
+                   and direct_ok(u, g) for g in members):
+            continue
+        f = group_cost(u, members, cus)
+        if best is None or f < best_f:
+            best, best_f = v, f
+    if best is None:
+        return
+    for i in grp:
+        if gemms[i].get("op", 0) != 1:
+            variant_of[i] = best
+
+
 def kernel_of(name: str) -> str:
     return name.rsplit("_c", 1)[0]
 
@@ -414,6 +465,8 @@ def plan_selector(gemms: list, table: dict, variants: list, cus: int, slots: int
         for i in grp:
             v = bind(gemms[i], ci, table, variants, by_name)
             out["variant_of"][i] = uncapped(v, variants) if mixed else v
+        unify_short_group(grp, gemms, out["variant_of"], variants, cus)
+        for i in grp:
             parts.setdefault(kernel_of(variants[out["variant_of"][i]]["name"]), []).append(i)
         # inside a dispatch: K descending, then M*N; dispatches: total 2MNK
         # descending, adds after every GEMM

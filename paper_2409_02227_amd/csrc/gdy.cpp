@@ -315,6 +315,62 @@ void uncap_mixed_group(const gdy_ctx* ctx, const gdy_gemm* g, const std::vector<
   for (int i : grp) p->variant_of[i] = ctx->variants[p->variant_of[i]].uncapped;
 }
 
+// A group whose GEMMs bind several kernels forks a pool stream per extra
+// kernel; a fork and join cost 20-30 us on MI355X (measured), more than a
+// short group takes, and short groups run at a quarter to a half of their
+// roofline.  When the group's roofline time is below kUnifyUs per extra
+// kernel (swept on the heterogeneous submissions: 25, 50 and 100 us gave
+// geomeans of 2.02, 2.06 and 2.07 over sequential), every GEMM is rebound to
+// the one group kernel that all of them can run at the least estimated
+// cost, uncapped: one dispatch, no fork.  The estimate extends the isolated
+// heuristic's tile model over the group: each tile costs max(tile area /
+// 128, tile perimeter) per K plus its area once (the stores, which dominate
+// at small K), tiles pack into CUs x occupancy slots, direct kernels count
+// 1.5x faster.
+const double kUnifyUs = 100.0;
+double roofline_s(const gdy_gemm& g);
+
+double group_cost(const gdy_ctx* ctx, int vid, const gdy_gemm* g, const std::vector<int>& grp) {
+  const Kernel& k = ctx->kernels[ctx->variants[vid].kernel];
+  const double per = std::max(k.d->bm * (double)k.d->bn / 128.0, (double)(k.d->bm + k.d->bn));
+  double f = 0.0;
+  for (int i : grp) {
+    if (g[i].op == GDY_OP_ADD) continue;
+    const Geometry geo = geometry(ctx, vid, g[i]);
+    f += (double)geo.tiles * ((double)g[i].k * per + k.d->bm * (double)k.d->bn);
+  }
+  const double slots = (double)ctx->cus * (double)std::max(k.occupancy, 1);
+  return f / slots / (k.d->direct ? 1.5 : 1.0);
+}
+
+void unify_short_group(const gdy_ctx* ctx, const gdy_gemm* g, const std::vector<int>& grp, gdy_plan_t* p) {
+  std::vector<int> kern;  // the GEMMs' kernels as uncapped variants, in order of first use
+  double t = 0.0;
+  for (int i : grp) {
+    if (g[i].op == GDY_OP_ADD) continue;
+    t += roofline_s(g[i]);
+    const int v = ctx->variants[p->variant_of[i]].uncapped;
+    if (std::find(kern.begin(), kern.end(), v) == kern.end()) kern.push_back(v);
+  }
+  if (kern.size() < 2 || t >= kUnifyUs * 1e-6 * (double)(kern.size() - 1)) return;
+  int best = -1;
+  double best_f = 0.0;
+  for (int v : kern) {
+    bool ok = true;
+    for (int i : grp)
+      if (g[i].op != GDY_OP_ADD && (!variant_fits(ctx, v, g[i]) || !direct_ok(ctx, v, g[i]))) ok = false;
+    if (!ok) continue;
+    const double f = group_cost(ctx, v, g, grp);
+    if (best < 0 || f < best_f) {
+      best = v;
+      best_f = f;
+    }
+  }
+  if (best < 0) return;
+  for (int i : grp)
+    if (g[i].op != GDY_OP_ADD) p->variant_of[i] = best;
+}
+
 bool partition_mode(int mode) {
   return mode == GDY_CU_PARTITION || mode == GDY_CU_PARTITION_GO || mode == GDY_CU_PARTITION_RC;
 }
@@ -767,6 +823,7 @@ void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int force
     std::vector<std::vector<int>> parts;  // their GEMMs
     for (int i : grp) p->variant_of[i] = bind_entry(ctx, g[i], entry[i], ci, &fb);
     uncap_mixed_group(ctx, g, grp, p);
+    unify_short_group(ctx, g, grp, p);
     for (int i : grp) {
       const int k = ctx->variants[p->variant_of[i]].kernel;
       size_t u = 0;

@@ -404,3 +404,37 @@ def test_mixed_groups_run_uncapped(tmp_path):
     # GO mode follows the same rule
     p = ctx.plan(mixed, mode="go")
     assert all(V[p["variant_of"][i]]["grid_cap_cus"] == 0 for i in range(4))
+
+
+@pytest.mark.skipif(not os.path.exists(TABLE), reason="no tuned table")
+def test_short_groups_share_one_kernel():
+    """A group shorter (in roofline time) than 100 us per extra
+    kernel runs one kernel, the one with the least padding; long groups keep
+    each GEMM's GO-Kernel."""
+    from paper_2409_02227_amd import inputs
+    ctx = gdy.Context(-1, table=TABLE)
+    table = sel.parse_table(TABLE)
+    V = ctx.variants()
+
+    def descs_of(specs):
+        out = []
+        for i, s in enumerate(specs):
+            d = _desc(s.m, s.n, s.k, {"bf16": 2, "f16": 1, "fp8": 3, "f32": 4}[s.dtype], s.trans_a, s.trans_b,
+                      (i + 1) << 37)
+            if s.batch:
+                d.batch = s.batch
+                d.stride_a, d.stride_b, d.stride_c = s.item_stride("a"), s.item_stride("b"), s.m * s.n
+            out.append(d)
+        return out
+    attn = descs_of(inputs.config_attn())  # 4 B-GEMMs, K = 64: microseconds of work
+    p = ctx.plan(attn, mode="selector")
+    assert p["n_groups"] == 1 and p["n_dispatches"] == 1
+    kern = {V[p["variant_of"][i]]["name"] for i in range(4)}
+    assert len(kern) == 1 and V[p["variant_of"][0]]["grid_cap_cus"] == 0
+    # the chosen tile pads least among the kernels the GEMMs were bound to
+    want = sel.plan_selector([_as_dict(d) for d in attn], table, V, ctx.cus(), 16)
+    assert [p["variant_of"][i] for i in range(4)] == [want["variant_of"][i] for i in range(4)]
+    layer = descs_of(inputs.config3())  # hundreds of microseconds: no rebinding
+    p = ctx.plan(layer, mode="selector")
+    assert p["n_dispatches"] >= 2
+    _check_plan(ctx, table, layer)
