@@ -154,7 +154,24 @@ typedef struct {
   int32_t n_dispatches;                 /* kernel dispatches of the submission              */
   int32_t dispatch_of[GDY_MAX_GEMMS];   /* dispatch that runs GEMM i (-1: none); dispatches
                                            are numbered in launch order                    */
+  int32_t split_of[GDY_MAX_GEMMS];      /* split-K runs of GEMM i (1: none; 0: not launched) */
 } gdy_plan_t;
+
+/*
+ * Split-K (all modes).  A GEMM whose tiles fill less than half of the CU
+ * slots its kernel has (CUs x occupancy; a grid cap does not count) and
+ * whose K is long runs each tile as S work items over consecutive runs of
+ * K tiles, S the largest power of two up to 16 with S x tiles within the
+ * slots, at least 4 K tiles per run and at most 16 MiB of fp32 partial
+ * planes; kernels with tiles above 128 x 128 do not split.  S depends only
+ * on the GEMM and its kernel, so a GEMM gives the same bits alone and
+ * concurrent.  Each run writes an fp32 M x N plane into a workspace the
+ * context allocates at creation (256 MiB); a reduction kernel on the
+ * dispatch's stream sums the planes in run order, scales, rounds and
+ * stores C.  GEMMs of one submission that would overflow the workspace run
+ * unsplit.  Submissions of one context must be ordered (one origin stream
+ * at a time): they share the workspace.
+ */
 
 /* Static description of one catalogue variant (a kernel plus its grid cap). */
 typedef struct {

@@ -369,6 +369,67 @@ def dispatches(groups: list, variant_of: dict, variants: list, slots: int):
     return dispatch_of, stream_of, nxt
 
 
+# Split-K (a property of the library's kernels, not of the paper): a GEMM
+# whose tiles leave CU slots free and whose K is long runs each tile as
+# several K runs whose fp32 partials are summed by the last one.
+MAX_SPLIT, MIN_SPLIT_KTILES = 16, 16
+SPLIT_MEMBER_BYTES, SPLIT_WS_BYTES = 16 << 20, 256 << 20
+SPLIT_MAX_TILE = 128 * 128
+
+
+def tiles_of(v: dict, g: dict) -> int:
+    return -(-g["m"] // v["bm"]) * -(-g["n"] // v["bn"]) * max(g.get("batch", 0), 1)
+
+
+def split_for(v: dict, g: dict, cus: int, together: int) -> int:
+    """K runs of g on variant v when `together` tiles (g's and those of the
+    GEMMs running at the same time) share the GPU: double S (at most
+    MAX_SPLIT) while together x 2S fit in the kernel's slots (CUs times
+    occupancy; the grid cap does not enter), 2S runs keep MIN_SPLIT_KTILES K
+    tiles each and 2S fp32 M x N planes (every batch item) fit in
+    SPLIT_MEMBER_BYTES; then S = the number of runs of ceil(K tiles / S)."""
+    if g.get("op", 0) == 1 or g["k"] <= 0 or g["m"] <= 0 or g["n"] <= 0:
+        return 1
+    if v.get("kind", 0) != 0 or v["bm"] * v["bn"] > SPLIT_MAX_TILE:
+        return 1
+    slots = cus * max(v["occupancy"], 1)
+    nk = -(-g["k"] // v["bk"])
+    plane_bytes = g["m"] * g["n"] * max(g.get("batch", 0), 1) * 4
+    s = 1
+    while (s * 2 <= MAX_SPLIT and together * s * 2 <= slots and nk >= s * 2 * MIN_SPLIT_KTILES
+           and s * 2 * plane_bytes <= SPLIT_MEMBER_BYTES):
+        s *= 2
+    if s > 1:
+        per = -(-nk // s)
+        s = -(-nk // per)
+    return s
+
+
+def plan_splits(order: list, gemms: list, variant_of: dict, variants: list, cus: int,
+                groups: list = None) -> dict:
+    """split_of per launched GEMM, in launch order, within the workspace
+    (GEMMs that would overflow it run unsplit).  `groups`: the sets of GEMMs
+    that run at the same time (None: each GEMM alone)."""
+    together = {}
+    for grp in (groups if groups is not None else [[i] for i in order]):
+        tot = sum(tiles_of(variants[variant_of[i]], gemms[i]) for i in grp if gemms[i].get("op", 0) != 1)
+        for i in grp:
+            together[i] = tot
+    out, ws = {}, 0
+    for i in order:
+        v = variants[variant_of[i]]
+        s = split_for(v, gemms[i], cus, together[i])
+        if s > 1:
+            g = gemms[i]
+            b = (g["m"] * g["n"] * max(g.get("batch", 0), 1) * s * 4 + 255) // 256 * 256
+            if ws + b > SPLIT_WS_BYTES:
+                s = 1
+            else:
+                ws += b
+        out[i] = s
+    return out
+
+
 PARTITIONS = (2, 4, 8)  # CU-Partition counts: a partition of P holds 1/P of the CUs
 
 
@@ -382,7 +443,8 @@ def partition_count(forced_cd: int, live: int) -> int:
     return PARTITIONS[-1]
 
 
-def plan_partition(gemms: list, table: dict, variants: list, kernels: str, forced_cd: int = 0) -> dict:
+def plan_partition(gemms: list, table: dict, variants: list, kernels: str, forced_cd: int = 0,
+                   cus: int = 256) -> dict:
     """CU-Partition (Sec. 5.5, Sec. 6.9): P streams on disjoint CU masks;
     GEMM t of the submission runs on partition t mod P.  kernels:
     "isolated" (the isolation-tuned kernel), "go" (the GO-Kernel of CD
@@ -407,6 +469,7 @@ def plan_partition(gemms: list, table: dict, variants: list, kernels: str, force
             else:
                 v = bind(g, ci, table, variants, by_name)
         out["variant_of"][i] = v
+    out["split_of"] = plan_splits(live, gemms, out["variant_of"], variants, cus, [live])
     return out
 
 
@@ -423,6 +486,7 @@ def plan_selector(gemms: list, table: dict, variants: list, cus: int, slots: int
         out["groups"] = [live] if live else []
         out["dispatch_of"], out["stream_of"], out["n_dispatches"] = dispatches(
             out["groups"], out["variant_of"], variants, slots)
+        out["split_of"] = plan_splits(live, gemms, out["variant_of"], variants, cus)  # alone
         return out
     for i in live:
         if gemms[i].get("op", 0) == 1:  # a non-GEMM restricts no group (Sec. 7.1)
@@ -478,4 +542,6 @@ def plan_selector(gemms: list, table: dict, variants: list, cus: int, slots: int
         out["groups"].append([i for u in ranked for i in parts[u]])
     out["dispatch_of"], out["stream_of"], out["n_dispatches"] = dispatches(
         out["groups"], out["variant_of"], variants, slots)
+    out["split_of"] = plan_splits([i for grp in out["groups"] for i in grp], gemms, out["variant_of"],
+                                  variants, cus, out["groups"])
     return out

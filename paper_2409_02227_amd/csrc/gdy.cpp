@@ -34,6 +34,12 @@ const int kCaps[] = {0, 128, 64, 32};         // grid caps in CUs: GPU, GPU/2, G
 const int kNumCaps = 4;
 const int kRcBudgets[] = {128, 64, 32};       // CU-masked pools for resource constraints
 const int kParts[] = {2, 4, 8};               // CU-Partition counts; kParts[r] parts of kRcBudgets[r] CUs
+// split-K limits
+const int kMaxSplit = 16;
+const int kMinSplitKTiles = 16;                // K tiles per run at least
+const int64_t kSplitMemberBytes = 16LL << 20;  // fp32 partial planes of one GEMM at most
+const int64_t kSplitWsBytes = 256LL << 20;     // workspace of a context
+const int kSplitMaxTile = 128 * 128;           // larger tiles' split twins spill registers
 
 struct Kernel {
   const KernelDesc* d;
@@ -122,6 +128,7 @@ struct gdy_ctx {
   // masks (empty unless created), part_done their join events
   std::vector<std::vector<hipStream_t>> parts;
   std::vector<std::vector<hipEvent_t>> part_done;
+  float* split_ws = nullptr;  // split-K partial planes (kSplitWsBytes)
   int host_slots = 0;                              // host-only context: planned stream slots
   std::vector<hipEvent_t> done;                    // one per stream slot
   hipEvent_t fork_ev = nullptr;
@@ -570,6 +577,7 @@ void plan_reset(gdy_plan_t* p, int n) {
     p->stream_of[i] = -1;
     p->variant_of[i] = -1;
     p->dispatch_of[i] = -1;
+    p->split_of[i] = 0;
   }
 }
 
@@ -635,8 +643,77 @@ int pool_size(const gdy_ctx* ctx) {
   return (int)ctx->pool.size();
 }
 
+// Split-K runs of GEMM g on variant vid (1: none), where `together` tiles
+// (of g and every GEMM running at the same time) share the GPU.  S doubles
+// (up to kMaxSplit) while together x 2S fit in the kernel's slots (CUs x
+// occupancy; a grid cap does not enter, so a cap never changes a tile's
+// sum), each of 2S runs keeps kMinSplitKTiles K tiles and the 2S fp32 M x N
+// planes (of every batch item) fit in kSplitMemberBytes; then S shrinks to
+// the number of runs of ceil(K tiles / S) tiles, so no run is empty.
+int split_for(const gdy_ctx* ctx, int vid, const gdy_gemm& g, int64_t together) {
+  if (vid < 0 || g.op == GDY_OP_ADD || g.k <= 0 || !active(g)) return 1;
+  const Variant& v = ctx->variants[vid];
+  const Kernel& k = ctx->kernels[v.kernel];
+  if (k.d->ew || !k.d->func_split || k.d->bm * k.d->bn > kSplitMaxTile) return 1;
+  const int64_t slots = (int64_t)ctx->cus * std::max(k.occupancy, 1);
+  const int64_t nk = (g.k + k.d->bk - 1) / k.d->bk;
+  const int64_t plane_bytes = (int64_t)g.m * g.n * std::max(g.batch, 1) * 4;
+  int64_t s = 1;
+  while (s * 2 <= kMaxSplit && together * s * 2 <= slots && nk >= s * 2 * kMinSplitKTiles &&
+         s * 2 * plane_bytes <= kSplitMemberBytes)
+    s *= 2;
+  if (s > 1) {
+    const int64_t per = (nk + s - 1) / s;
+    s = (nk + per - 1) / per;
+  }
+  return (int)s;
+}
+
+// Workspace bytes of a split GEMM's planes (rounded up to 256).
+int64_t split_ws_bytes(const gdy_gemm& g, int s) {
+  return ((int64_t)g.m * g.n * std::max(g.batch, 1) * s * 4 + 255) / 256 * 256;
+}
+
+// split_of for every launched GEMM, in launch order, within the workspace.
+// The GEMMs running at the same time are the GEMM alone (SEQUENTIAL) or
+// its group (every other mode: a group's dispatches or streams run
+// together); their tiles, adds aside, decide whether the GPU has room.
+void plan_splits(const gdy_ctx* ctx, const gdy_gemm* g, gdy_plan_t* p, int mode) {
+  std::vector<int64_t> group_tiles(GDY_MAX_GEMMS, 0);
+  for (int t = 0; t < GDY_MAX_GEMMS && p->order[t] >= 0; ++t) {
+    const int i = p->order[t];
+    if (p->variant_of[i] >= 0 && g[i].op != GDY_OP_ADD && p->group_of[i] >= 0)
+      group_tiles[p->group_of[i]] += geometry(ctx, p->variant_of[i], g[i]).tiles;
+  }
+  int64_t ws = 0;
+  for (int t = 0; t < GDY_MAX_GEMMS && p->order[t] >= 0; ++t) {
+    const int i = p->order[t];
+    if (p->variant_of[i] < 0) continue;
+    const int64_t together = mode == GDY_SEQUENTIAL ? geometry(ctx, p->variant_of[i], g[i]).tiles
+                                                    : group_tiles[p->group_of[i]];
+    int s = split_for(ctx, p->variant_of[i], g[i], together);
+    if (s > 1) {
+      const int64_t b = split_ws_bytes(g[i], s);
+      if (ws + b > kSplitWsBytes)
+        s = 1;
+      else
+        ws += b;
+    }
+    p->split_of[i] = s;
+  }
+}
+
+void make_plan_core(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int forced_cd,
+                    gdy_plan_t* p);
+
 void make_plan(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int forced_cd,
                gdy_plan_t* p) {
+  make_plan_core(ctx, g, n, mode, forced_cd, p);
+  plan_splits(ctx, g, p, mode);
+}
+
+void make_plan_core(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int forced_cd,
+                    gdy_plan_t* p) {
   plan_reset(p, n);
   bool fb = false;
   const int S = pool_size(ctx);
@@ -923,6 +1000,7 @@ KArgs make_args(const gdy_ctx* ctx, int vid, const gdy_gemm& g, Geometry* geo_ou
   a.xcd_remap = 1;
   a.batch = (int32_t)std::max(g.batch, 1);
   a.ew = add ? g.a_type : 0;
+  a.split = 1;
   a.stride_a = a.batch > 1 ? g.stride_a * es : 0;
   a.stride_b = a.batch > 1 ? g.stride_b * es : 0;
   a.stride_c = a.batch > 1 ? g.stride_c * out_size(g) : 0;
@@ -942,9 +1020,11 @@ hipStream_t slot_stream(const gdy_ctx* ctx, int slot) {
 // its cap x occupancy), every range but the last rounded up to a multiple
 // of 8 so each GEMM starts on XCD 0 (the extra workgroups find no tile).
 gdy_status build_launch(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p,
-                        const std::vector<int>& members, KLaunch* L, int* grid) {
+                        const std::vector<int>& members, const std::vector<int64_t>& ws_off,
+                        KLaunch* L, int* grid, bool* split) {
   std::memset(L, 0, sizeof *L);
   L->count = (int)members.size();
+  *split = false;
   int64_t wg = 0;
   for (int u = 0; u < L->count; ++u) {
     const int i = members[u];
@@ -952,6 +1032,21 @@ gdy_status build_launch(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p,
     L->g[u] = make_args(ctx, p.variant_of[i], g[i], &geo);
     L->first[u] = (int32_t)wg;
     int span = std::max(geo.grid, 1);
+    const int s = std::max(p.split_of[i], 1);
+    if (s > 1) {  // every tile in s K runs; a capped variant keeps its cap
+      const Variant& v = ctx->variants[p.variant_of[i]];
+      const KernelDesc* d = ctx->kernels[v.kernel].d;
+      if (!ctx->split_ws || ws_off[i] < 0 || ws_off[i] + split_ws_bytes(g[i], s) > kSplitWsBytes)
+        return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: split-K workspace exhausted", i);
+      const int64_t nk = (g[i].k + d->bk - 1) / d->bk;
+      L->g[u].split = s;
+      L->g[u].split_kt = (int32_t)((nk + s - 1) / s);
+      L->g[u].ws = ctx->split_ws + ws_off[i] / 4;
+      span = (int)std::min<int64_t>((int64_t)geo.tiles * s,
+                                    v.cap > 0 ? (int64_t)v.cap * std::max(ctx->kernels[v.kernel].occupancy, 1)
+                                              : INT32_MAX);
+      *split = true;
+    }
     if (u + 1 < L->count) span = (span + 7) & ~7;
     wg += span;
   }
@@ -959,6 +1054,28 @@ gdy_status build_launch(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p,
   L->first[L->count] = (int32_t)wg;
   *grid = (int)wg;
   return GDY_OK;
+}
+
+// Launch block of the split-K reduction for the split members of one GEMM
+// dispatch (their KArgs as built for it): each gets tiles of 8 rows x 128
+// columns over every batch item, ranges rounded to multiples of 8.
+void build_reduce(const gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, const std::vector<int>& members,
+                  const KLaunch& gemm, KLaunch* R, int* grid) {
+  (void)ctx;
+  std::memset(R, 0, sizeof *R);
+  int64_t wg = 0;
+  for (int u = 0; u < gemm.count; ++u) {
+    if (gemm.g[u].split <= 1) continue;
+    const int i = members[u];
+    const int c = R->count++;
+    R->g[c] = gemm.g[u];
+    R->first[c] = (int32_t)wg;
+    const int64_t tiles = ((g[i].m + 7) / 8) * ((g[i].n + 127) / 128) * std::max<int64_t>(g[i].batch, 1);
+    wg += (tiles + 7) & ~7LL;
+  }
+  R->first[R->count] = (int32_t)wg;
+  *grid = (int)std::max<int64_t>(wg, 1);
+  (void)p;
 }
 
 gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, int mode,
@@ -973,6 +1090,17 @@ gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, int
     return fail(ctx, GDY_ERR_UNSUPPORTED, "no CU partitions: create the context with use_cu_masks & 2");
   auto stream_at = [&](int s) { return parted ? ctx->parts[pr][s] : slot_stream(ctx, s); };
   auto done_at = [&](int s) { return parted ? ctx->part_done[pr][s] : ctx->done[s]; };
+  // split-K workspace: consecutive regions in launch order (as planned)
+  std::vector<int64_t> ws_off(n > 0 ? n : 1, -1);
+  {
+    int64_t ws = 0;
+    for (int t = 0; t < GDY_MAX_GEMMS && p.order[t] >= 0; ++t) {
+      const int i = p.order[t];
+      if (p.split_of[i] <= 1) continue;
+      ws_off[i] = ws;
+      ws += split_ws_bytes(g[i], p.split_of[i]);
+    }
+  }
   int L = 0;
   while (L < GDY_MAX_GEMMS && p.order[L] >= 0) ++L;
   const int D = p.n_dispatches;
@@ -1030,13 +1158,23 @@ gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, int
       const Kernel& k = ctx->kernels[ctx->variants[vid].kernel];
       KLaunch launch;
       int grid = 0;
-      st = build_launch(ctx, g, p, members[u], &launch, &grid);
+      bool split = false;
+      st = build_launch(ctx, g, p, members[u], ws_off, &launch, &grid, &split);
       if (st != GDY_OK) break;
       void* argv[] = {&launch};
       const int d = ids[u];
       hipStream_t hs = p.stream_of[i0] >= 0 ? stream_at(p.stream_of[i0]) : origin;
-      hipError_t e = hipExtLaunchKernel(k.d->func, dim3(grid), dim3(k.d->waves * 64), argv, 0, hs,
-                                        ts ? ts->start[d] : nullptr, ts ? ts->stop[d] : nullptr, 0);
+      hipError_t e = hipExtLaunchKernel(split ? k.d->func_split : k.d->func, dim3(grid), dim3(k.d->waves * 64), argv, 0, hs,
+                                        ts ? ts->start[d] : nullptr, ts && !split ? ts->stop[d] : nullptr, 0);
+      if (e == hipSuccess && split) {
+        // the split members' planes summed into C, on the same stream
+        KLaunch red;
+        int rgrid = 0;
+        build_reduce(ctx, g, p, members[u], launch, &red, &rgrid);
+        void* rargv[] = {&red};
+        e = hipExtLaunchKernel(split_reduce_kernel(g[i0].c_type), dim3(rgrid), dim3(256), rargv, 0, hs, nullptr,
+                               ts ? ts->stop[d] : nullptr, 0);
+      }
       if (e != hipSuccess) {
         st = fail(ctx, GDY_ERR_HIP, "launch of %s (%d GEMMs, first %d) failed: %s",
                   ctx->variants[vid].name.c_str(), (int)members[u].size(), i0, hipGetErrorString(e));
@@ -1194,6 +1332,10 @@ static void destroy_streams(gdy_ctx* ctx) {
     t = TimingSlot();
   }
   if (ctx->fork_ev) (void)hipEventDestroy(ctx->fork_ev);
+  if (ctx->split_ws) (void)hipFree(ctx->split_ws);
+
+  ctx->split_ws = nullptr;
+
   ctx->pool.clear();
   ctx->rc_pools.clear();
   ctx->parts.clear();
@@ -1347,6 +1489,8 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
     }
   }
   HIP_TRY(ctx, hipEventCreateWithFlags(&ctx->fork_ev, hipEventDisableTiming));
+  HIP_TRY(ctx, hipMalloc((void**)&ctx->split_ws, kSplitWsBytes));
+
   if (table_path && table_path[0]) {
     gdy_status s = load_table(ctx, table_path);
     if (s != GDY_OK) return s;

@@ -31,6 +31,9 @@ struct KArgs {
   int32_t xcd_remap;  // 1: keep consecutive tiles on one XCD
   int32_t batch;      // items of a strided batch (>= 1); the extents above are per item
   int32_t ew;         // 0: a GEMM; else the DT_* of an element-wise add (C = A + B)
+  int32_t split;      // split-K: K tiles are cut into `split` runs of `split_kt` tiles;
+  int32_t split_kt;   //   each run writes an fp32 M x N plane, a reduction kernel sums them
+  float* ws;          // split > 1: the planes, batch x split of them, leading dimension N
   int64_t stride_a;   // bytes between consecutive items of A, B and C
   int64_t stride_b;
   int64_t stride_c;
@@ -61,6 +64,7 @@ struct KernelDesc {
   const void* func;   // __global__ entry, launched with hipExtLaunchKernel
   int direct;         // 1: global->LDS copies; needs K % bk == 0 and 16-byte alignment
   int ew;             // 1: the element-wise add (a non-GEMM op), not a GEMM kernel
+  const void* func_split;  // GEMM kernels: the split-K twin (runs split = 1 GEMMs too)
 };
 
 // Each instantiation unit exports its table.
@@ -69,6 +73,8 @@ int kernels_f16(const KernelDesc** out);
 int kernels_fp8(const KernelDesc** out);
 int kernels_f32(const KernelDesc** out);
 int kernels_ew(const KernelDesc** out);
+// Split-K reduction kernel for an output type (DT_BF16, DT_F16, DT_F32).
+const void* split_reduce_kernel(int out_dt);
 int kernels_d_bf16(const KernelDesc** out);
 int kernels_d_f16(const KernelDesc** out);
 int kernels_d_fp8(const KernelDesc** out);

@@ -510,6 +510,78 @@ __device__ __forceinline__ void ew_member(const KArgs& p, int lwg, int nwg) {
   else if (p.ew == DT_F32) ew_add_tiles<DT_F32, NT>(p, lwg, nwg);
 }
 
+// ---------------------------------------------------------------------------
+// Split-K.  A GEMM with few tiles and a long K runs each tile as `split`
+// work items over consecutive runs of `split_kt` K tiles, so more CUs stream
+// its operands at once.  Each work item stores its unscaled fp32 partial
+// into its run's row-major M x N plane of the workspace (plane (item *
+// split + run), leading dimension N); a reduction kernel on the same stream
+// then sums the planes in run order 0, 1, ..., scales, rounds and stores C.
+// The kernel boundary orders the two: no atomics, no fences, no counters,
+// and the sum does not depend on which run finished first.
+// ---------------------------------------------------------------------------
+// K range of split run s: the operand resources start at its first K tile
+// and the GEMM's K shrinks to the run's length.
+__device__ __forceinline__ int split_k0(const KArgs& p, int s, int bk) { return s * p.split_kt * bk; }
+
+// The fp32 partial plane of run s of batch item `item`.
+__device__ __forceinline__ float* split_plane(const KArgs& p, int item, int s) {
+  return p.ws + ((size_t)item * p.split + s) * (size_t)p.m * (size_t)p.n;
+}
+
+// Reduction of the split planes of up to kMaxFused GEMMs (one launch per
+// dispatch that split): 256 threads, 8 rows x 128 columns per tile, four
+// consecutive columns per thread; C = round(scale * (P0 + P1 + ...)).
+template <int OUT>
+__global__ void __launch_bounds__(256) split_reduce(KLaunch L) {
+  const int gi = owner_of(L);
+  const KArgs& p = L.g[gi];
+  const int wg0 = L.first[gi];
+  const int nwg = L.first[gi + 1] - wg0;
+  constexpr int OS = OUT == DT_F32 ? 4 : 2;
+  const int M = (int)p.m, N = (int)p.n, S = p.split;
+  const int tn = (N + 127) / 128, tm = (M + 7) / 8;
+  const int ntiles = tm * tn, total = ntiles * p.batch;
+  const int r = threadIdx.x / 32, v = threadIdx.x % 32;
+  const int ldc_b = (int)p.ldc * OS;
+  const size_t plane = (size_t)M * (size_t)N;
+  for (int tb = (int)blockIdx.x - wg0; tb < total; tb += nwg) {
+    const int item = tb / ntiles, t = tb - item * ntiles;
+    const int row = (t / tn) * 8 + r, col0 = (t % tn) * 128 + v * 4;
+    if (row >= M || col0 >= N) continue;
+    const Rsrc rc = make_rsrc(p.c + item * p.stride_c, p.c_bytes);
+    const float* P = p.ws + (size_t)item * S * plane + (size_t)row * N + col0;
+    const int cols = min(4, N - col0);
+    float acc[4];
+    if (cols == 4 && (N & 3) == 0) {  // 16-byte aligned rows of the planes
+      float4 x = *reinterpret_cast<const float4*>(P);
+      acc[0] = x.x, acc[1] = x.y, acc[2] = x.z, acc[3] = x.w;
+      for (int q = 1; q < S; ++q) {
+        x = *reinterpret_cast<const float4*>(P + q * plane);
+        acc[0] += x.x, acc[1] += x.y, acc[2] += x.z, acc[3] += x.w;
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (e >= cols) break;
+        acc[e] = P[e];
+        for (int q = 1; q < S; ++q) acc[e] += P[q * plane + e];
+      }
+    }
+    const int off = row * ldc_b + col0 * OS;
+    if (OUT != DT_F32 && cols == 4 && p.c_vec) {
+      u32x2 w;
+      w[0] = (unsigned)to_out<OUT>(acc[0] * p.scale) | ((unsigned)to_out<OUT>(acc[1] * p.scale) << 16);
+      w[1] = (unsigned)to_out<OUT>(acc[2] * p.scale) | ((unsigned)to_out<OUT>(acc[3] * p.scale) << 16);
+      __builtin_amdgcn_raw_buffer_store_b64(w, rc, off, 0, 0);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (e < cols) store_out<OUT>(acc[e] * p.scale, rc, off + e * OS);
+    }
+  }
+}
+
 template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int MM>
 struct GoCfg {
   static constexpr int ES = ElemSize<DT>::v;
@@ -531,7 +603,7 @@ struct GoCfg {
   static_assert(LDS <= 160 * 1024, "LDS budget");
 };
 
-template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int MM>
+template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int MM, bool SPLIT>
 __global__ void __launch_bounds__(WM * WN * 64)
 go_gemm(KLaunch L) {
   typedef GoCfg<DT, TA, TB, BM, BN, WM, WN, MM> C;
@@ -558,8 +630,6 @@ go_gemm(KLaunch L) {
   const int wm = wave / WN;
   const int wn = wave % WN;
   const int ntiles = p.tiles_m * p.tiles_n;
-  const int K = (int)p.k;
-  const int nk = (K + C::BK - 1) / C::BK;
   Rsrc ra = make_rsrc(p.a, p.a_bytes);
   Rsrc rb = make_rsrc(p.b, p.b_bytes);
   Rsrc rc = make_rsrc(p.c, p.c_bytes);
@@ -569,16 +639,30 @@ go_gemm(KLaunch L) {
   const int ldc_b = (int)p.ldc * OS;
   const int Mrows = (int)p.m, Ncols = (int)p.n;
 
-  const int total = ntiles * p.batch;  // tiles of every item of a strided batch
+  // work items: every tile of every item of a strided batch; in the split
+  // twin, each in `split` K runs (split innermost)
+  const int nsplit = SPLIT ? p.split : 1;
+  const int total = ntiles * p.batch * nsplit;
   for (int tb = (int)blockIdx.x - wg0; tb < total; tb += nwg) {
-    int t = tb;
-    if (p.batch > 1) {  // item-major: the item's operands get buffer resources of their own
-      const int item = tb / ntiles;
-      t = tb - item * ntiles;
-      ra = make_rsrc(p.a + item * p.stride_a, p.a_bytes);
-      rb = make_rsrc(p.b + item * p.stride_b, p.b_bytes);
+    const int s_run = SPLIT ? tb % nsplit : 0;
+    const int tile_all = SPLIT ? tb / nsplit : tb;  // item * ntiles + tile
+    const int item = tile_all / ntiles;
+    const int t = tile_all - item * ntiles;
+    // this run's K range: operands start at its first K tile
+    int K = (int)p.k;
+    int64_t a_shift = 0, b_shift = 0;
+    if (SPLIT && nsplit > 1) {
+      const int k0 = split_k0(p, s_run, C::BK);
+      K = min(K - k0, p.split_kt * C::BK);
+      a_shift = TA == 0 ? (int64_t)k0 * C::ES : (int64_t)k0 * lda_b;
+      b_shift = TB == 1 ? (int64_t)k0 * C::ES : (int64_t)k0 * ldb_b;
+    }
+    if (p.batch > 1 || (SPLIT && nsplit > 1)) {  // item and K run: buffer resources of their own
+      ra = make_rsrc(p.a + item * p.stride_a + a_shift, p.a_bytes - (int32_t)a_shift);
+      rb = make_rsrc(p.b + item * p.stride_b + b_shift, p.b_bytes - (int32_t)b_shift);
       rc = make_rsrc(p.c + item * p.stride_c, p.c_bytes);
     }
+    const int nk = (K + C::BK - 1) / C::BK;
     int tm, tn;
     tile_coords(t, p, tm, tn);
     const int m0 = tm * BM;
@@ -636,6 +720,26 @@ go_gemm(KLaunch L) {
       }
     }
 
+    if constexpr (SPLIT) {
+      if (nsplit > 1) {  // the run's unscaled fp32 partial into its plane
+        float* P = split_plane(p, item, s_run);
+#pragma unroll
+        for (int i = 0; i < C::FM; ++i) {
+#pragma unroll
+          for (int j = 0; j < C::FN; ++j) {
+            const int col = n0 + wn * C::WTN + j * MM + (lane % MM);
+#pragma unroll
+            for (int r = 0; r < M::NACC; ++r) {
+              const int rr = MM == 32 ? 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3) : 4 * (lane >> 4) + r;
+              const int row = m0 + wm * C::WTM + i * MM + rr;
+              if (row < Mrows && col < Ncols) P[(size_t)row * Ncols + col] = acc[i][j][r];
+            }
+          }
+        }
+        continue;
+      }
+    }
+
     // epilogue: scale, round, bounds-checked 16-bit stores
     const float s = p.scale;
 #pragma unroll
@@ -666,4 +770,5 @@ go_gemm(KLaunch L) {
   {DTNAME "_" LAYOUT "_" #BM "x" #BN "_w" #WM "x" #WN "_m" #MM,                                       \
    DT, TA, TB, BM, BN, ::gdy::GoCfg<DT, TA, TB, BM, BN, WM, WN, MM>::BK, WM * WN,                      \
    MM, ::gdy::GoCfg<DT, TA, TB, BM, BN, WM, WN, MM>::LDS,                                             \
-   reinterpret_cast<const void*>(&::gdy::go_gemm<DT, TA, TB, BM, BN, WM, WN, MM>), 0}
+   reinterpret_cast<const void*>(&::gdy::go_gemm<DT, TA, TB, BM, BN, WM, WN, MM, false>), 0, 0,      \
+   reinterpret_cast<const void*>(&::gdy::go_gemm<DT, TA, TB, BM, BN, WM, WN, MM, true>)}

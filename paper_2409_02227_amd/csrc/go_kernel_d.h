@@ -255,7 +255,7 @@ struct DCfg {
       FM * FN * 16 + 2 * (FM + FN) * FRAG_REGS <= 512 / WAVES_PER_SIMD - 56;
 };
 
-template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int STAGES, int KB>
+template <int DT, int TA, int TB, int BM, int BN, int WM, int WN, int STAGES, int KB, bool SPLIT>
 __global__ void __launch_bounds__(WM * WN * 64)
 go_gemm_d(KLaunch L) {
   typedef DCfg<DT, TA, TB, BM, BN, WM, WN, STAGES, KB> C;
@@ -288,7 +288,6 @@ go_gemm_d(KLaunch L) {
   const int wm = wave / WN;
   const int wn = wave % WN;
   const int ntiles = p.tiles_m * p.tiles_n;
-  const int nk = (int)p.k / C::BK;  // host guarantees K % BK == 0
   sdesc ra = make_sdesc(p.a, p.a_bytes);
   sdesc rb = make_sdesc(p.b, p.b_bytes);
   Rsrc rc = make_rsrc(p.c, p.c_bytes);
@@ -315,14 +314,28 @@ go_gemm_d(KLaunch L) {
       for (int hh = 0; hh < NHH; ++hh) boff[j][hh] = kt_lane<C::ES, BT>(lane, wn * C::WTN + j * 32, hh);
   }
 
-  const int total = ntiles * p.batch;  // tiles of every item of a strided batch
+  // work items: every tile of every item of a strided batch; in the split
+  // twin, each in `split` K runs (split innermost)
+  const int nsplit = SPLIT ? p.split : 1;
+  const int total = ntiles * p.batch * nsplit;
   for (int tb = (int)blockIdx.x - wg0; tb < total; tb += nwg) {
-    int t = tb;
-    if (p.batch > 1) {  // item-major: the item's operands get buffer resources of their own
-      const int item = tb / ntiles;
-      t = tb - item * ntiles;
-      ra = make_sdesc(p.a + item * p.stride_a, p.a_bytes);
-      rb = make_sdesc(p.b + item * p.stride_b, p.b_bytes);
+    const int s_run = SPLIT ? tb % nsplit : 0;
+    const int tile_all = SPLIT ? tb / nsplit : tb;  // item * ntiles + tile
+    const int item = tile_all / ntiles;
+    const int t = tile_all - item * ntiles;
+    // K tiles of this run (the host guarantees K % BK == 0); operands start
+    // at the run's first K tile
+    int nk = (int)p.k / C::BK;
+    int64_t a_shift = 0, b_shift = 0;
+    if (SPLIT && nsplit > 1) {
+      const int k0 = split_k0(p, s_run, C::BK);
+      nk = min(nk - s_run * p.split_kt, p.split_kt);
+      a_shift = TA == 0 ? (int64_t)k0 * C::ES : (int64_t)k0 * lda_b;
+      b_shift = TB == 1 ? (int64_t)k0 * C::ES : (int64_t)k0 * ldb_b;
+    }
+    if (p.batch > 1 || (SPLIT && nsplit > 1)) {  // item and K run: buffer resources of their own
+      ra = make_sdesc(p.a + item * p.stride_a + a_shift, p.a_bytes - (int32_t)a_shift);
+      rb = make_sdesc(p.b + item * p.stride_b + b_shift, p.b_bytes - (int32_t)b_shift);
       rc = make_rsrc(p.c + item * p.stride_c, p.c_bytes);
     }
     int tm, tn;
@@ -521,6 +534,37 @@ go_gemm_d(KLaunch L) {
     }
     __syncthreads();  // every wave is done with the ring before the next tile refills it
 
+    if constexpr (SPLIT) {
+      if (nsplit > 1) {  // the run's unscaled fp32 partial into its plane
+        float* P = split_plane(p, item, s_run);
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j) {
+#pragma unroll
+          for (int i = 0; i < C::FM; ++i) {
+            if constexpr (C::FM * C::FN * M::NACC > 128) asm volatile("" : "+a"(acc[j][i]));
+            const int row = m0 + wm * C::WTM + i * 32 + (lane & 31);
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const int col = n0 + wn * C::WTN + j * 32 + 8 * g + 4 * (lane >> 5);
+              if (row < Mrows) {
+                float* dst = P + (size_t)row * Ncols + col;
+                if (col + 4 <= Ncols && (Ncols & 3) == 0) {
+                  *reinterpret_cast<float4*>(dst) = make_float4(acc[j][i][4 * g], acc[j][i][4 * g + 1],
+                                                                acc[j][i][4 * g + 2], acc[j][i][4 * g + 3]);
+                } else {
+#pragma unroll
+                  for (int e = 0; e < 4; ++e)
+                    if (col + e < Ncols) dst[e] = acc[j][i][4 * g + e];
+                }
+              }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
+        continue;
+      }
+    }
+
     // epilogue: block (j, i) holds C^T; accumulator r of lane l is
     // n = 8*(r/4) + 4*(l/32) + r%4, m = l%32 -- 4 consecutive n per group of 4
     const float s = p.scale;
@@ -571,7 +615,8 @@ go_gemm_d(KLaunch L) {
   {DTNAME "_" LAYOUT "_" #BM "x" #BN "_w" #WM "x" #WN "_d" #ST SUFFIX,                             \
    DT, TA, TB, BM, BN, ::gdy::DCfg<DT, TA, TB, BM, BN, WM, WN, ST, KB>::BK, WM * WN,               \
    32, ::gdy::DCfg<DT, TA, TB, BM, BN, WM, WN, ST, KB>::LDS,                                        \
-   reinterpret_cast<const void*>(&::gdy::go_gemm_d<DT, TA, TB, BM, BN, WM, WN, ST, KB>), 1}
+   reinterpret_cast<const void*>(&::gdy::go_gemm_d<DT, TA, TB, BM, BN, WM, WN, ST, KB, false>), 1, 0, \
+   reinterpret_cast<const void*>(&::gdy::go_gemm_d<DT, TA, TB, BM, BN, WM, WN, ST, KB, true>)}
 #define GDY_KERNEL_D(DT, DTNAME, TA, TB, LAYOUT, BM, BN, WM, WN, ST) \
   GDY_KERNEL_DK(DT, DTNAME, TA, TB, LAYOUT, BM, BN, WM, WN, ST, 128, "")
 #define GDY_KERNEL_DH(DT, DTNAME, TA, TB, LAYOUT, BM, BN, WM, WN, ST) \

@@ -62,7 +62,8 @@ class Plan(ctypes.Structure):
                 ("order", ctypes.c_int32 * MAX_GEMMS), ("group_of", ctypes.c_int32 * MAX_GEMMS),
                 ("stream_of", ctypes.c_int32 * MAX_GEMMS), ("variant_of", ctypes.c_int32 * MAX_GEMMS),
                 ("pred_cd", ctypes.c_int32 * MAX_GEMMS), ("group_size", ctypes.c_int32 * MAX_GEMMS),
-                ("n_dispatches", ctypes.c_int32), ("dispatch_of", ctypes.c_int32 * MAX_GEMMS)]
+                ("n_dispatches", ctypes.c_int32), ("dispatch_of", ctypes.c_int32 * MAX_GEMMS),
+                ("split_of", ctypes.c_int32 * MAX_GEMMS)]
 
     def as_dict(self) -> dict:
         n = self.n
@@ -71,7 +72,8 @@ class Plan(ctypes.Structure):
                 "group_of": list(self.group_of[:n]), "stream_of": list(self.stream_of[:n]),
                 "variant_of": list(self.variant_of[:n]), "pred_cd": list(self.pred_cd[:n]),
                 "group_size": list(self.group_size[:self.n_groups]),
-                "n_dispatches": self.n_dispatches, "dispatch_of": list(self.dispatch_of[:n])}
+                "n_dispatches": self.n_dispatches, "dispatch_of": list(self.dispatch_of[:n]),
+                "split_of": list(self.split_of[:n])}
 
 
 class VariantDesc(ctypes.Structure):

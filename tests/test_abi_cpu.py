@@ -36,7 +36,7 @@ def test_struct_layouts_match_header():
     assert ctypes.sizeof(gdy.GemmDesc) == 3 * 8 + 5 * 4 + 4 + 6 * 8 + 2 * 4 + 2 * 4 + 2 * 4 + 3 * 8
     assert gdy.GemmDesc.batch.offset == 112 and gdy.GemmDesc.stride_a.offset == 120
     assert gdy.GemmDesc.a.offset == 48
-    assert ctypes.sizeof(gdy.Plan) == 4 * 4 + 6 * 4 * gdy.MAX_GEMMS + 4 + 4 * gdy.MAX_GEMMS
+    assert ctypes.sizeof(gdy.Plan) == 4 * 4 + 6 * 4 * gdy.MAX_GEMMS + 4 + 2 * 4 * gdy.MAX_GEMMS
     assert gdy.Plan.dispatch_of.offset == 4 * 4 + 6 * 4 * gdy.MAX_GEMMS + 4
     assert ctypes.sizeof(gdy.VariantDesc) == 64 + 14 * 4
     text = open(HEADER).read()

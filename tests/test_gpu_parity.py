@@ -205,14 +205,16 @@ def test_validation_errors(ctx):
 
 def test_concurrent_kernels_overlap(ctx):
     """With CD > 1 the per-kernel intervals overlap (streams really run
-    concurrently; needs GPU_MAX_HW_QUEUES >= the CD)."""
-    specs = [GemmSpec(64, 4096, 4096, "bf16", seed=300 + i, name=f"ov{i}") for i in range(4)]
+    concurrently; needs GPU_MAX_HW_QUEUES >= the CD).  The GEMMs fill the
+    CU slots by their tiles, so none is split into K runs."""
+    specs = [GemmSpec(1024, 4096, 2048, "bf16", seed=300 + i, name=f"ov{i}") for i in range(4)]
     mats = [inputs.materialize(s) for s in specs]
     ctx.set_timing(True)
     try:
         best = 0.0
         for _ in range(5):
-            _run(ctx, mats, "default")
+            plan = _run(ctx, mats, "default")
+            assert plan["split_of"] == [1, 1, 1, 1]
             st, en = ctx.kernel_times(4)
             iv = sorted(zip(st, en))
             ov = max(0.0, min(e for _, e in iv) - max(s for s, _ in iv))
@@ -506,6 +508,67 @@ def test_bgemm_shared_operand_and_validation(ctx):
     with pytest.raises(gdy.GdyError) as e:
         ctx.execute([d])
     assert e.value.status == 1
+
+
+# --------------------------------------------------------------------------
+# Split-K: skinny GEMMs with a long K run each tile as several K runs
+# --------------------------------------------------------------------------
+
+def test_split_k_every_small_tile_kernel(ctx):
+    """Every kernel with tiles up to 128x128 on a GEMM of three tiles and a
+    long K (whole K tiles, and a ragged K tail for staged kernels): the plan
+    splits it; the result meets the oracle's bound, repeats bit for bit, and
+    is bit-identical fused with another GEMM whenever the plan gives it the
+    same number of K runs there."""
+    for vid, v in _kernels(ctx):
+        if v["bm"] * v["bn"] > 128 * 128:
+            continue
+        dt = DT_NAME[v["dtype"]]
+        for tail in (0, 0 if v["direct"] else 17):
+            # ragged M and N tails that keep 16-byte rows (direct kernels stay direct)
+            spec = GemmSpec(max(v["bm"] - 16, 8), 2 * v["bn"] + 16, 64 * v["bk"] + tail, dt, v["trans_a"],
+                            v["trans_b"], seed=5000 + vid + tail, name=v["name"])
+            mat = inputs.materialize(spec)
+            other = inputs.materialize(GemmSpec(v["bm"], v["bn"], v["bk"] * 2, dt, v["trans_a"], v["trans_b"],
+                                                seed=5500 + vid, name="other"))
+            label = f"{v['name']} K={spec.k}"
+            plan = _run(ctx, [mat], "forced", 1, [vid])
+            assert plan["split_of"][0] > 1, label
+            check(mat, label=label)
+            ref = out_codes(mat).copy()
+            _run(ctx, [mat], "forced", 1, [vid])
+            assert np.array_equal(out_codes(mat), ref), f"{label}: repeat differs"
+            alone = plan["split_of"][0]
+            plan = _run(ctx, [other, mat], "forced_grouped", 0, [vid, vid])
+            assert plan["n_dispatches"] == 1 and plan["split_of"][1] > 1, label
+            if plan["split_of"][1] == alone:
+                assert np.array_equal(out_codes(mat), ref), f"{label}: fused differs"
+            else:
+                check(mat, label=label + " fused")
+            check(other, label=label + " co-runner")
+
+
+def test_split_k_batched_and_modes(ctx):
+    """A strided batch of skinny GEMMs and a set of skinny GEMMs in every
+    execution mode: split plans, oracle bound, bits equal across modes that
+    bind the same variant."""
+    b = inputs.materialize(GemmSpec(20, 100, 3000, "bf16", seed=5900, batch=5, name="bsplit"))
+    plan = _run(ctx, [b], "sequential")
+    assert plan["split_of"][0] > 1
+    check(b, label="batched split")
+    specs = [GemmSpec(16, 1024, 4096, "bf16", seed=5901 + i, name=f"skinny{i}") for i in range(3)]
+    specs.append(GemmSpec(64, 2048, 2048, "f16", seed=5905, name="skinny-f16"))
+    mats = [inputs.materialize(sp) for sp in specs]
+    seen = {}
+    for mode in ("sequential", "default", "go", "selector"):
+        plan = _run(ctx, mats, mode)
+        assert any(s > 1 for s in plan["split_of"]), mode
+        for i, m in enumerate(mats):
+            check(m, label=f"{mode} {m.spec.name}")
+            key = (i, plan["variant_of"][i], plan["split_of"][i])
+            if key in seen:
+                assert np.array_equal(seen[key], out_codes(m)), f"{mode} {m.spec.name}"
+            seen[key] = out_codes(m).copy()
 
 
 # --------------------------------------------------------------------------

@@ -174,6 +174,7 @@ def _check_plan(ctx, table, descs, slots=16):
     for i in live:
         assert p["dispatch_of"][i] == want["dispatch_of"][i], i
         assert p["stream_of"][i] == want["stream_of"][i], i
+        assert p["split_of"][i] == want["split_of"][i], (i, V[p["variant_of"][i]]["name"])
 
 
 def _random_set(rng, n):
@@ -343,6 +344,7 @@ def test_partition_plans_match_oracle(tmp_path):
                     assert p["stream_of"][i] == want["stream_of"][i] == t % want["P"]
                     assert p["dispatch_of"][i] == t
                     assert p["variant_of"][i] == want["variant_of"][i], (mode, forced, i)
+                    assert p["split_of"][i] == want["split_of"][i], (mode, forced, i)
 
 
 def test_partition_counts_and_errors(tmp_path):
