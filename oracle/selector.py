@@ -291,17 +291,25 @@ UNIFY_US = 100.0  # roofline time per extra kernel below which a group shares on
 
 
 def group_cost(v: dict, members: list, cus: int) -> float:
-    """Estimated time of `members` fused on one kernel: each tile costs
-    max(tile area / 128, tile perimeter) per K (the isolated heuristic's
-    tile model) plus its area once (the stores), tiles pack into CUs x
-    occupancy slots, direct kernels 1.5x faster."""
+    """Estimated time of `members` fused on one kernel: a work item (a tile,
+    or one K run of it when the GEMM splits) costs max(tile area / 128,
+    tile perimeter) per K (the isolated heuristic's tile model) plus its
+    area once (the stores); the group takes the larger of its items packed
+    into CUs x occupancy slots and its longest item; direct kernels 1.5x
+    faster."""
     per = max(v["bm"] * float(v["bn"]) / 128.0, float(v["bm"] + v["bn"]))
-    f = 0.0
+    area = v["bm"] * float(v["bn"])
+    work = sum(work_of(v, g) for g in members)
+    f, longest = 0.0, 0.0
     for g in members:
         tiles = -(-g["m"] // v["bm"]) * -(-g["n"] // v["bn"]) * max(g.get("batch", 0), 1)
-        f += float(tiles) * (float(g["k"]) * per + v["bm"] * float(v["bn"]))
+        f += float(tiles) * (float(g["k"]) * per + area)
+        nk = -(-g["k"] // v["bk"])
+        sp = split_for(v, g, cus, work)
+        item = float(-(-nk // sp) * v["bk"]) * per + area
+        longest = max(longest, item)
     slots = float(cus) * float(max(v["occupancy"], 1))
-    return f / slots / (1.5 if v["direct"] else 1.0)
+    return max(f / slots, longest) / (1.5 if v["direct"] else 1.0)
 
 
 def unify_short_group(grp: list, gemms: list, variant_of: dict, variants: list, cus: int) -> None:
@@ -381,13 +389,21 @@ def tiles_of(v: dict, g: dict) -> int:
     return -(-g["m"] // v["bm"]) * -(-g["n"] // v["bn"]) * max(g.get("batch", 0), 1)
 
 
-def split_for(v: dict, g: dict, cus: int, together: int) -> int:
-    """K runs of g on variant v when `together` tiles (g's and those of the
-    GEMMs running at the same time) share the GPU: double S (at most
-    MAX_SPLIT) while together x 2S fit in the kernel's slots (CUs times
-    occupancy; the grid cap does not enter), 2S runs keep MIN_SPLIT_KTILES K
-    tiles each and 2S fp32 M x N planes (every batch item) fit in
-    SPLIT_MEMBER_BYTES; then S = the number of runs of ceil(K tiles / S)."""
+def work_of(v: dict, g: dict) -> int:
+    """K tiles over every tile of g on variant v (adds: none)."""
+    if g.get("op", 0) == 1 or v.get("kind", 0) != 0 or v["bk"] <= 0:
+        return 0
+    return tiles_of(v, g) * -(-g["k"] // v["bk"])
+
+
+def split_for(v: dict, g: dict, cus: int, work: int) -> int:
+    """K runs of g on variant v when `work` K tiles (over every tile of g and
+    of the GEMMs running at the same time) share the GPU: work / slots (CUs
+    times occupancy; the grid cap does not enter) is each slot's even share.
+    Double S (at most MAX_SPLIT) while each of 2S runs stays at least that
+    long and keeps MIN_SPLIT_KTILES K tiles, and 2S fp32 M x N planes (every
+    batch item) fit in SPLIT_MEMBER_BYTES; then S = the number of runs of
+    ceil(K tiles / S)."""
     if g.get("op", 0) == 1 or g["k"] <= 0 or g["m"] <= 0 or g["n"] <= 0:
         return 1
     if v.get("kind", 0) != 0 or v["bm"] * v["bn"] > SPLIT_MAX_TILE:
@@ -396,7 +412,7 @@ def split_for(v: dict, g: dict, cus: int, together: int) -> int:
     nk = -(-g["k"] // v["bk"])
     plane_bytes = g["m"] * g["n"] * max(g.get("batch", 0), 1) * 4
     s = 1
-    while (s * 2 <= MAX_SPLIT and together * s * 2 <= slots and nk >= s * 2 * MIN_SPLIT_KTILES
+    while (s * 2 <= MAX_SPLIT and nk * slots >= s * 2 * work and nk >= s * 2 * MIN_SPLIT_KTILES
            and s * 2 * plane_bytes <= SPLIT_MEMBER_BYTES):
         s *= 2
     if s > 1:
@@ -408,17 +424,18 @@ def split_for(v: dict, g: dict, cus: int, together: int) -> int:
 def plan_splits(order: list, gemms: list, variant_of: dict, variants: list, cus: int,
                 groups: list = None) -> dict:
     """split_of per launched GEMM, in launch order, within the workspace
-    (GEMMs that would overflow it run unsplit).  `groups`: the sets of GEMMs
-    that run at the same time (None: each GEMM alone)."""
-    together = {}
+    (GEMMs that would overflow it run unsplit); a split GEMM's variant
+    becomes its kernel's uncapped one (variant_of is updated).  `groups`:
+    the sets of GEMMs that run at the same time (None: each GEMM alone)."""
+    work = {}
     for grp in (groups if groups is not None else [[i] for i in order]):
-        tot = sum(tiles_of(variants[variant_of[i]], gemms[i]) for i in grp if gemms[i].get("op", 0) != 1)
+        tot = sum(work_of(variants[variant_of[i]], gemms[i]) for i in grp if gemms[i].get("op", 0) != 1)
         for i in grp:
-            together[i] = tot
+            work[i] = tot
     out, ws = {}, 0
     for i in order:
         v = variants[variant_of[i]]
-        s = split_for(v, gemms[i], cus, together[i])
+        s = split_for(v, gemms[i], cus, work[i])
         if s > 1:
             g = gemms[i]
             b = (g["m"] * g["n"] * max(g.get("batch", 0), 1) * s * 4 + 255) // 256 * 256
@@ -426,6 +443,7 @@ def plan_splits(order: list, gemms: list, variant_of: dict, variants: list, cus:
                 s = 1
             else:
                 ws += b
+                variant_of[i] = uncapped(variant_of[i], variants)  # runs spread over the GPU
         out[i] = s
     return out
 

@@ -330,24 +330,35 @@ void uncap_mixed_group(const gdy_ctx* ctx, const gdy_gemm* g, const std::vector<
 // geomeans of 2.02, 2.06 and 2.07 over sequential), every GEMM is rebound to
 // the one group kernel that all of them can run at the least estimated
 // cost, uncapped: one dispatch, no fork.  The estimate extends the isolated
-// heuristic's tile model over the group: each tile costs max(tile area /
-// 128, tile perimeter) per K plus its area once (the stores, which dominate
-// at small K), tiles pack into CUs x occupancy slots, direct kernels count
-// 1.5x faster.
+// heuristic's tile model over the group: a work item (a tile, or one K run
+// of it when the GEMM splits) costs max(tile area / 128, tile perimeter) per
+// K plus its area once (the stores, which dominate at small K); the group
+// takes the larger of its items packed into CUs x occupancy slots and its
+// longest item; direct kernels count 1.5x faster.
 const double kUnifyUs = 100.0;
 double roofline_s(const gdy_gemm& g);
+int split_for(const gdy_ctx* ctx, int vid, const gdy_gemm& g, int64_t work);
+int64_t gemm_work(const gdy_ctx* ctx, int vid, const gdy_gemm& g);
 
 double group_cost(const gdy_ctx* ctx, int vid, const gdy_gemm* g, const std::vector<int>& grp) {
   const Kernel& k = ctx->kernels[ctx->variants[vid].kernel];
   const double per = std::max(k.d->bm * (double)k.d->bn / 128.0, (double)(k.d->bm + k.d->bn));
-  double f = 0.0;
+  const double area = k.d->bm * (double)k.d->bn;
+  int64_t work = 0;
+  for (int i : grp)
+    if (g[i].op != GDY_OP_ADD) work += gemm_work(ctx, vid, g[i]);
+  double f = 0.0, longest = 0.0;
   for (int i : grp) {
     if (g[i].op == GDY_OP_ADD) continue;
     const Geometry geo = geometry(ctx, vid, g[i]);
-    f += (double)geo.tiles * ((double)g[i].k * per + k.d->bm * (double)k.d->bn);
+    f += (double)geo.tiles * ((double)g[i].k * per + area);
+    const int64_t nk = (g[i].k + k.d->bk - 1) / k.d->bk;
+    const int64_t s = split_for(ctx, vid, g[i], work);
+    const double item = (double)(((nk + s - 1) / s) * k.d->bk) * per + area;
+    longest = std::max(longest, item);
   }
   const double slots = (double)ctx->cus * (double)std::max(k.occupancy, 1);
-  return f / slots / (k.d->direct ? 1.5 : 1.0);
+  return std::max(f / slots, longest) / (k.d->direct ? 1.5 : 1.0);
 }
 
 void unify_short_group(const gdy_ctx* ctx, const gdy_gemm* g, const std::vector<int>& grp, gdy_plan_t* p) {
@@ -643,14 +654,17 @@ int pool_size(const gdy_ctx* ctx) {
   return (int)ctx->pool.size();
 }
 
-// Split-K runs of GEMM g on variant vid (1: none), where `together` tiles
-// (of g and every GEMM running at the same time) share the GPU.  S doubles
-// (up to kMaxSplit) while together x 2S fit in the kernel's slots (CUs x
-// occupancy; a grid cap does not enter, so a cap never changes a tile's
-// sum), each of 2S runs keeps kMinSplitKTiles K tiles and the 2S fp32 M x N
-// planes (of every batch item) fit in kSplitMemberBytes; then S shrinks to
-// the number of runs of ceil(K tiles / S) tiles, so no run is empty.
-int split_for(const gdy_ctx* ctx, int vid, const gdy_gemm& g, int64_t together) {
+// Split-K runs of GEMM g on variant vid (1: none).  `work` is the K tiles
+// summed over every tile of g and of the GEMMs running at the same time;
+// work / slots (CUs x occupancy; a grid cap does not enter, so a cap never
+// changes a tile's sum) is the K length each slot would get if the work
+// were spread evenly.  S doubles (up to kMaxSplit) while each of 2S runs
+// stays at least that long, keeps kMinSplitKTiles K tiles, and the 2S fp32
+// M x N planes (of every batch item) fit in kSplitMemberBytes; then S
+// shrinks to the number of runs of ceil(K tiles / S) tiles, so no run is
+// empty.  Alone, this splits until the tiles' runs fill the slots; in a
+// group, it splits the members whose K is long next to the rest.
+int split_for(const gdy_ctx* ctx, int vid, const gdy_gemm& g, int64_t work) {
   if (vid < 0 || g.op == GDY_OP_ADD || g.k <= 0 || !active(g)) return 1;
   const Variant& v = ctx->variants[vid];
   const Kernel& k = ctx->kernels[v.kernel];
@@ -659,7 +673,7 @@ int split_for(const gdy_ctx* ctx, int vid, const gdy_gemm& g, int64_t together) 
   const int64_t nk = (g.k + k.d->bk - 1) / k.d->bk;
   const int64_t plane_bytes = (int64_t)g.m * g.n * std::max(g.batch, 1) * 4;
   int64_t s = 1;
-  while (s * 2 <= kMaxSplit && together * s * 2 <= slots && nk >= s * 2 * kMinSplitKTiles &&
+  while (s * 2 <= kMaxSplit && nk * slots >= s * 2 * work && nk >= s * 2 * kMinSplitKTiles &&
          s * 2 * plane_bytes <= kSplitMemberBytes)
     s *= 2;
   if (s > 1) {
@@ -674,30 +688,41 @@ int64_t split_ws_bytes(const gdy_gemm& g, int s) {
   return ((int64_t)g.m * g.n * std::max(g.batch, 1) * s * 4 + 255) / 256 * 256;
 }
 
-// split_of for every launched GEMM, in launch order, within the workspace.
+// split_of for every launched GEMM, in launch order, within the workspace;
+// a split GEMM runs its kernel uncapped.
 // The GEMMs running at the same time are the GEMM alone (SEQUENTIAL) or
 // its group (every other mode: a group's dispatches or streams run
-// together); their tiles, adds aside, decide whether the GPU has room.
+// together); their work, adds aside, sets the even share per slot.
+int64_t gemm_work(const gdy_ctx* ctx, int vid, const gdy_gemm& g) {
+  const KernelDesc* d = ctx->kernels[ctx->variants[vid].kernel].d;
+  if (g.op == GDY_OP_ADD || d->ew || d->bk <= 0) return 0;  // adds have no K
+  return (int64_t)geometry(ctx, vid, g).tiles * ((g.k + d->bk - 1) / d->bk);
+}
+
 void plan_splits(const gdy_ctx* ctx, const gdy_gemm* g, gdy_plan_t* p, int mode) {
-  std::vector<int64_t> group_tiles(GDY_MAX_GEMMS, 0);
+  std::vector<int64_t> group_work(GDY_MAX_GEMMS, 0);
   for (int t = 0; t < GDY_MAX_GEMMS && p->order[t] >= 0; ++t) {
     const int i = p->order[t];
     if (p->variant_of[i] >= 0 && g[i].op != GDY_OP_ADD && p->group_of[i] >= 0)
-      group_tiles[p->group_of[i]] += geometry(ctx, p->variant_of[i], g[i]).tiles;
+      group_work[p->group_of[i]] += gemm_work(ctx, p->variant_of[i], g[i]);
   }
   int64_t ws = 0;
   for (int t = 0; t < GDY_MAX_GEMMS && p->order[t] >= 0; ++t) {
     const int i = p->order[t];
     if (p->variant_of[i] < 0) continue;
-    const int64_t together = mode == GDY_SEQUENTIAL ? geometry(ctx, p->variant_of[i], g[i]).tiles
-                                                    : group_tiles[p->group_of[i]];
-    int s = split_for(ctx, p->variant_of[i], g[i], together);
+    const int64_t work = mode == GDY_SEQUENTIAL ? gemm_work(ctx, p->variant_of[i], g[i])
+                                                : group_work[p->group_of[i]];
+    int s = split_for(ctx, p->variant_of[i], g[i], work);
     if (s > 1) {
       const int64_t b = split_ws_bytes(g[i], s);
-      if (ws + b > kSplitWsBytes)
+      if (ws + b > kSplitWsBytes) {
         s = 1;
-      else
+      } else {
         ws += b;
+        // the runs are meant to spread over the GPU: a split GEMM's grid is
+        // not capped (a cap changes where a tile runs, never its sum)
+        p->variant_of[i] = ctx->variants[p->variant_of[i]].uncapped;
+      }
     }
     p->split_of[i] = s;
   }

@@ -207,7 +207,7 @@ def test_concurrent_kernels_overlap(ctx):
     """With CD > 1 the per-kernel intervals overlap (streams really run
     concurrently; needs GPU_MAX_HW_QUEUES >= the CD).  The GEMMs fill the
     CU slots by their tiles, so none is split into K runs."""
-    specs = [GemmSpec(1024, 4096, 2048, "bf16", seed=300 + i, name=f"ov{i}") for i in range(4)]
+    specs = [GemmSpec(1024, 4096, 8192, "bf16", seed=300 + i, name=f"ov{i}") for i in range(4)]
     mats = [inputs.materialize(s) for s in specs]
     ctx.set_timing(True)
     try:

@@ -440,3 +440,16 @@ def test_short_groups_share_one_kernel():
     p = ctx.plan(layer, mode="selector")
     assert p["n_dispatches"] >= 2
     _check_plan(ctx, table, layer)
+
+
+def test_every_mode_plans_adds_and_gemms(tmp_path):
+    """Host planning of submissions that mix GEMMs and element-wise adds in
+    every mode (adds have no K: nothing may divide by their K tile)."""
+    ctx = gdy.Context(-1, table=TABLE if os.path.exists(TABLE) else None)
+    descs = [_add(64, 300, 2, 1 << 37), _desc(16, 1024, 8192, 2, 0, 0, 2 << 37), _add(7, 9, 4, 3 << 37),
+             _desc(512, 4096, 1024, 2, 0, 0, 4 << 37)]
+    for mode in ("sequential", "default", "go", "selector", "cu_partition", "cu_partition_go", "cu_partition_rc"):
+        for sub in (descs[:1], descs[2:3], descs):
+            p = ctx.plan(sub, mode=mode)
+            for i, d in enumerate(sub):
+                assert p["split_of"][i] == (1 if d.op == 1 else p["split_of"][i]) >= 1, (mode, i)
