@@ -312,13 +312,16 @@ def group_cost(v: dict, members: list, cus: int) -> float:
     return max(f / slots, longest) / (1.5 if v["direct"] else 1.0)
 
 
-def unify_short_group(grp: list, gemms: list, variant_of: dict, variants: list, cus: int) -> None:
+def unify_short_group(grp: list, gemms: list, variant_of: dict, variants: list, cus: int,
+                      isolated: dict) -> None:
     """A library launch rule, not the paper's: a group whose GEMMs use
     several kernels forks one stream per extra kernel.  When the group's
     roofline time is below UNIFY_US per extra kernel, every GEMM takes the
-    one group kernel that all of them can run (same type and layout; direct
+    one kernel that all of them can run (same type and layout; direct
     kernels only where the GEMM meets their requirements) at the least
-    group_cost, uncapped, so the group is one dispatch."""
+    group_cost, uncapped, so the group is one dispatch.  Candidates: the
+    group's kernels in order of first use, then each member's isolated
+    kernel (`isolated`: GEMM index -> variant); the first listed wins a tie."""
     kern, t = [], 0.0
     for i in grp:
         if gemms[i].get("op", 0) == 1:
@@ -329,8 +332,15 @@ def unify_short_group(grp: list, gemms: list, variant_of: dict, variants: list, 
             kern.append(v)
     if len(kern) < 2 or t >= UNIFY_US * 1e-6 * (len(kern) - 1):
         return
+    cand = list(kern)
+    for i in grp:
+        if gemms[i].get("op", 0) == 1:
+            continue
+        v = uncapped(isolated[i], variants)
+        if v not in cand:
+            cand.append(v)
     best, best_f = None, 0.0
-    for v in kern:
+    for v in cand:
         u = variants[v]
         members = [gemms[i] for i in grp if gemms[i].get("op", 0) != 1]
         if not all(u["dtype"] == g["a_type"] and u["trans_a"] == g["trans_a"] and u["trans_b"] == g["trans_b"]
@@ -547,7 +557,8 @@ def plan_selector(gemms: list, table: dict, variants: list, cus: int, slots: int
         for i in grp:
             v = bind(gemms[i], ci, table, variants, by_name)
             out["variant_of"][i] = uncapped(v, variants) if mixed else v
-        unify_short_group(grp, gemms, out["variant_of"], variants, cus)
+        iso = {i: bind(gemms[i], 0, table, variants, by_name) for i in grp if gemms[i].get("op", 0) != 1}
+        unify_short_group(grp, gemms, out["variant_of"], variants, cus, iso)
         for i in grp:
             parts.setdefault(kernel_of(variants[out["variant_of"][i]]["name"]), []).append(i)
         # inside a dispatch: K descending, then M*N; dispatches: total 2MNK

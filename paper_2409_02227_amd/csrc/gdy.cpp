@@ -328,8 +328,11 @@ void uncap_mixed_group(const gdy_ctx* ctx, const gdy_gemm* g, const std::vector<
 // roofline.  When the group's roofline time is below kUnifyUs per extra
 // kernel (swept on the heterogeneous submissions: 25, 50 and 100 us gave
 // geomeans of 2.02, 2.06 and 2.07 over sequential), every GEMM is rebound to
-// the one group kernel that all of them can run at the least estimated
-// cost, uncapped: one dispatch, no fork.  The estimate extends the isolated
+// the one kernel that all of them can run at the least estimated cost,
+// uncapped: one dispatch, no fork.  The candidates are the kernels the group
+// binds, then each member's isolated kernel (first listed wins a tie): a
+// group bound only to small-tile kernels tuned for its skinny members would
+// otherwise put its large members on them too.  The estimate extends the isolated
 // heuristic's tile model over the group: a work item (a tile, or one K run
 // of it when the GEMM splits) costs max(tile area / 128, tile perimeter) per
 // K plus its area once (the stores, which dominate at small K); the group
@@ -371,9 +374,17 @@ void unify_short_group(const gdy_ctx* ctx, const gdy_gemm* g, const std::vector<
     if (std::find(kern.begin(), kern.end(), v) == kern.end()) kern.push_back(v);
   }
   if (kern.size() < 2 || t >= kUnifyUs * 1e-6 * (double)(kern.size() - 1)) return;
+  std::vector<int> cand = kern;
+  for (int i : grp) {
+    if (g[i].op == GDY_OP_ADD) continue;
+    const int iso = bind_variant(ctx, g[i], 0, nullptr);
+    if (iso < 0) continue;
+    const int v = ctx->variants[iso].uncapped;
+    if (std::find(cand.begin(), cand.end(), v) == cand.end()) cand.push_back(v);
+  }
   int best = -1;
   double best_f = 0.0;
-  for (int v : kern) {
+  for (int v : cand) {
     bool ok = true;
     for (int i : grp)
       if (g[i].op != GDY_OP_ADD && (!variant_fits(ctx, v, g[i]) || !direct_ok(ctx, v, g[i]))) ok = false;

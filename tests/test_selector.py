@@ -411,8 +411,9 @@ def test_mixed_groups_run_uncapped(tmp_path):
 @pytest.mark.skipif(not os.path.exists(TABLE), reason="no tuned table")
 def test_short_groups_share_one_kernel():
     """A group shorter (in roofline time) than 100 us per extra
-    kernel runs one kernel, the one with the least padding; long groups keep
-    each GEMM's GO-Kernel."""
+    kernel runs one kernel, the one the planner's tile model rates cheapest
+    (equal to the oracle planner's choice); long groups keep each GEMM's
+    GO-Kernel."""
     from paper_2409_02227_amd import inputs
     ctx = gdy.Context(-1, table=TABLE)
     table = sel.parse_table(TABLE)
@@ -433,12 +434,19 @@ def test_short_groups_share_one_kernel():
     assert p["n_groups"] == 1 and p["n_dispatches"] == 1
     kern = {V[p["variant_of"][i]]["name"] for i in range(4)}
     assert len(kern) == 1 and V[p["variant_of"][0]]["grid_cap_cus"] == 0
-    # the chosen tile pads least among the kernels the GEMMs were bound to
+    # the chosen kernel is the oracle planner's
     want = sel.plan_selector([_as_dict(d) for d in attn], table, V, ctx.cus(), 16)
     assert [p["variant_of"][i] for i in range(4)] == [want["variant_of"][i] for i in range(4)]
     layer = descs_of(inputs.config3())  # hundreds of microseconds: no rebinding
     p = ctx.plan(layer, mode="selector")
-    assert p["n_dispatches"] >= 2
+    assert sum(sel.roofline_seconds(_as_dict(d)) for d in layer) >= sel.UNIFY_US * 1e-6
+    by_name = {v["name"]: i for i, v in enumerate(V)}
+    for gid in range(p["n_groups"]):  # every GEMM keeps its group-size GO-Kernel (uncapped: mixed shapes)
+        members = [i for i in range(len(layer)) if p["group_of"][i] == gid]
+        ci = sel.class_for_size(len(members))
+        for i in members:
+            go = sel.bind(_as_dict(layer[i]), ci, table, V, by_name)
+            assert p["variant_of"][i] == sel.uncapped(go, V), (i, V[p["variant_of"][i]]["name"])
     _check_plan(ctx, table, layer)
 
 
