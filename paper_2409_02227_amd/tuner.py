@@ -56,6 +56,9 @@ KNN_K = 3               # neighbours of the preferred-RC vote (Sec. 7.5)
 # tuning shape sets
 # ---------------------------------------------------------------------------
 
+LARGE_SET = 1072  # the paper's tuning set size (Sec. 5.4)
+
+
 def shape_set(kind: str) -> list:
     """(dtype, trans_a, trans_b, M, N, K) tuples to tune."""
     shapes = []
@@ -88,6 +91,22 @@ def shape_set(kind: str) -> list:
         # K used transposed) and context P V (SL x 64 x SL), 64 items
         for sl in (128, 256, 512):
             shapes += [("bf16", 0, 1, sl, sl, 64, 64), ("bf16", 0, 0, sl, 64, sl, 64)]
+    if kind == "large":
+        shapes = shape_set("full")
+        # the paper tunes 1072 GEMMs over outputs of 32K-168M elements and K up
+        # to 20K (Sec. 5.4); draw bf16 shapes to that count: M log-uniform in
+        # [1, 8192], N and K from 512 to 16384, outputs at most 168M elements
+        # and at most 2 * 8192^3 flops (a bound on tuning time)
+        rng = np.random.default_rng(2409)
+        seen = set(shapes)
+        while len(shapes) < LARGE_SET:
+            m = int(round(2.0 ** rng.uniform(0.0, 13.0)))
+            n, k = (int(x) for x in 512 * 2 ** rng.integers(0, 6, size=2))
+            s = ("bf16", 0, 0, m, n, k)
+            if s in seen or m * n > 168 * 2 ** 20 or m * n * k > 8192 ** 3:
+                continue
+            seen.add(s)
+            shapes.append(s)
     seen, out = set(), []
     for s in shapes:
         if s not in seen:
@@ -488,7 +507,7 @@ def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--out", required=True, help="GO table to write")
     ap.add_argument("--records", default=None, help="JSONL of per-shape results (appended, resumable)")
-    ap.add_argument("--shapes", default="small", choices=("small", "full"))
+    ap.add_argument("--shapes", default="small", choices=("small", "full", "large"))
     ap.add_argument("--limit", type=int, default=0)
     ap.add_argument("--retrain", action="store_true",
                     help="no timing: rebuild the table and predictor from --records")
@@ -496,6 +515,8 @@ def main(argv=None):
                     help="no timing: from --records, keep this fraction as exhaustively tuned and "
                          "predict the other shapes' GO-Kernels by preferred-RC KNN (Sec. 7.5)")
     ap.add_argument("--knn-seed", type=int, default=0)
+    ap.add_argument("--max-seconds", type=float, default=0.0,
+                    help="start no new shape after this many seconds (resume later from --records)")
     args = ap.parse_args(argv)
 
     import torch
@@ -520,6 +541,9 @@ def main(argv=None):
     for i, s in enumerate(shapes):
         if tuple(s) in done:
             continue
+        if args.max_seconds and time.time() - t0 > args.max_seconds:
+            print(f"time budget reached after {len(records)} of {len(shapes)} shapes", flush=True)
+            break
         r = tune_shape(ctx, bench, torch, variants, s)
         records.append(r)
         if args.records:
