@@ -461,3 +461,37 @@ def test_every_mode_plans_adds_and_gemms(tmp_path):
             p = ctx.plan(sub, mode=mode)
             for i, d in enumerate(sub):
                 assert p["split_of"][i] == (1 if d.op == 1 else p["split_of"][i]) >= 1, (mode, i)
+
+
+def test_short_group_weighs_members_isolated_kernels(tmp_path):
+    """The one kernel of a short group may be a member's isolated kernel,
+    not only one of the group's GO-Kernels: a large GEMM whose GO-Kernels
+    are small tiles (as a skinny co-runner's are) runs on its isolated
+    128x128 tile when the tile model rates that cheapest for the group."""
+    probe = gdy.Context(-1)
+    head = ["gdy-go-table 1", "device host cus 256", f"catalogue {probe.catalogue_hash():016x}"]
+    b = ["0.0"] * 5
+    b[4] = "50.0"  # the predictor always answers CD 16
+    head += ["lr_min " + " ".join(["0.0"] * sel.N_FEATURES), "lr_max " + " ".join(["1.0"] * sel.N_FEATURES),
+             "lr_w " + " ".join(["0.0"] * (sel.N_FEATURES * 5)), "lr_b " + " ".join(b)]
+    iso, small_a, small_b = ("bf16_nn_128x128_w2x2_d2_c0", "bf16_nn_32x128_w1x4_d4_c0",
+                             "bf16_nn_64x64_w2x2_d4_c0")
+    lines = head + ["entry 2 0 0 12 2048 1024 " + " ".join([iso] + [small_a] * 4),
+                    "entry 2 0 0 4 1024 1024 " + " ".join([small_b] * 5)]
+    path = tmp_path / "iso.table"
+    path.write_text("\n".join(lines) + "\n")
+    ctx = gdy.Context(-1, table=str(path))
+    table = sel.parse_table(str(path))
+    V = ctx.variants()
+    descs = [_desc(4096, 2048, 1024, 2, 0, 0, 1 << 37), _desc(16, 1024, 1024, 2, 0, 0, 2 << 37)]
+    p = ctx.plan(descs, mode="selector")
+    assert p["n_groups"] == 1 and p["n_dispatches"] == 1
+    assert [V[p["variant_of"][i]]["name"] for i in range(2)] == [iso, iso]
+    _check_plan(ctx, table, descs)
+    # with the group's own kernels as the only candidates a small tile would win
+    gemms = [_as_dict(d) for d in descs]
+    by_name = {v["name"]: i for i, v in enumerate(V)}
+    go = {0: by_name[small_a], 1: by_name[small_b]}
+    variant_of = dict(go)
+    sel.unify_short_group([0, 1], gemms, variant_of, V, ctx.cus(), go)
+    assert {V[v]["name"] for v in variant_of.values()} <= {small_a, small_b}

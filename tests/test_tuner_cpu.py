@@ -91,3 +91,21 @@ def test_library_rejects_the_add_kernel_in_a_gemm_entry(tmp_path):
     with pytest.raises(gdy.GdyError) as e:
         gdy.Context(-1, table=path)
     assert e.value.status == 5
+
+
+def test_shape_sets():
+    """The full set holds every workload's own shapes; the large set extends
+    it to the paper's 1072 tuned GEMMs with seeded bf16 draws inside the
+    stated bounds (outputs of at most 168M elements, at most 2 * 8192^3
+    flops, N and K from 512 to 16384)."""
+    full, large = tuner.shape_set("full"), tuner.shape_set("large")
+    assert len(set(full)) == len(full) and len(set(large)) == len(large) == tuner.LARGE_SET == 1072
+    assert large[:len(full)] == full
+    for s in [("bf16", 0, 0, 512, 4608, 12288), ("bf16", 0, 0, 64, 4096, 1024), ("f16", 0, 0, 256, 256, 256),
+              ("fp8", 0, 0, 2048, 8192, 8192), ("bf16", 0, 1, 512, 12288, 1536)]:
+        assert s in full
+    for dt, ta, tb, m, n, k in large[len(full):]:
+        assert (dt, ta, tb) == ("bf16", 0, 0) and 1 <= m <= 8192
+        assert n in (512, 1024, 2048, 4096, 8192, 16384) and k in (512, 1024, 2048, 4096, 8192, 16384)
+        assert m * n <= 168 * 2 ** 20 and m * n * k <= 8192 ** 3
+    assert tuner.shape_set("large") == large  # seeded
