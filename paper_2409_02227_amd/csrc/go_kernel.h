@@ -569,12 +569,17 @@ __global__ void __launch_bounds__(256) split_reduce(KLaunch L) {
       }
     }
     const int off = row * ldc_b + col0 * OS;
-    if (OUT != DT_F32 && cols == 4 && p.c_vec) {
-      u32x2 w;
-      w[0] = (unsigned)to_out<OUT>(acc[0] * p.scale) | ((unsigned)to_out<OUT>(acc[1] * p.scale) << 16);
-      w[1] = (unsigned)to_out<OUT>(acc[2] * p.scale) | ((unsigned)to_out<OUT>(acc[3] * p.scale) << 16);
-      __builtin_amdgcn_raw_buffer_store_b64(w, rc, off, 0, 0);
-    } else {
+    bool stored = false;
+    if constexpr (OUT != DT_F32) {  // four 16-bit outputs in one 8-byte store
+      if (cols == 4 && p.c_vec) {
+        u32x2 w;
+        w[0] = (unsigned)to_out<OUT>(acc[0] * p.scale) | ((unsigned)to_out<OUT>(acc[1] * p.scale) << 16);
+        w[1] = (unsigned)to_out<OUT>(acc[2] * p.scale) | ((unsigned)to_out<OUT>(acc[3] * p.scale) << 16);
+        __builtin_amdgcn_raw_buffer_store_b64(w, rc, off, 0, 0);
+        stored = true;
+      }
+    }
+    if (!stored) {
 #pragma unroll
       for (int e = 0; e < 4; ++e)
         if (e < cols) store_out<OUT>(acc[e] * p.scale, rc, off + e * OS);
