@@ -34,8 +34,8 @@
  *
  * Ownership: all matrices are device buffers owned by the caller, who keeps
  * them alive until the origin stream passes the work.  The library owns its
- * stream pool, events and plan state.  No call allocates device memory
- * after gdy_create.
+ * stream pool, events, split-K workspace and plan state.  No call allocates
+ * device memory after gdy_create.
  *
  * Errors: every call returns a gdy_status; nothing is thrown across the ABI.
  * gdy_execute validates all descriptors before launching anything (all or
@@ -66,7 +66,7 @@ typedef enum {
   GDY_ERR_UNSUPPORTED = 2, /* dtype triple, alignment or extent the kernels cannot take */
   GDY_ERR_ALIAS = 3,       /* a C range overlaps an A, B or C range of the submission */
   GDY_ERR_TOO_MANY = 4,    /* n > GDY_MAX_GEMMS                                      */
-  GDY_ERR_TABLE = 5,       /* GO table unreadable or built for another device/catalogue */
+  GDY_ERR_TABLE = 5,       /* reserved: a bad GO table falls back instead (gdy_create)  */
   GDY_ERR_HIP = 6,         /* a HIP runtime call failed                              */
   GDY_ERR_NOMEM = 7        /* host allocation failed                                 */
 } gdy_status;
@@ -144,7 +144,7 @@ typedef struct {
   int32_t n;                            /* GEMMs planned                                   */
   int32_t cd;                           /* largest number of GEMMs launched together       */
   int32_t n_groups;                     /* groups run one after another                    */
-  int32_t fallback;                     /* 1: no GO table, isolated heuristics were used    */
+  int32_t fallback;                     /* 1: no usable GO table, isolated heuristics used  */
   int32_t order[GDY_MAX_GEMMS];         /* launch order: order[t] is a GEMM index          */
   int32_t group_of[GDY_MAX_GEMMS];      /* group of GEMM i                                 */
   int32_t stream_of[GDY_MAX_GEMMS];     /* pool stream slot of GEMM i's dispatch (-1: origin) */
@@ -158,18 +158,22 @@ typedef struct {
 } gdy_plan_t;
 
 /*
- * Split-K (all modes).  A GEMM whose tiles fill less than half of the CU
- * slots its kernel has (CUs x occupancy; a grid cap does not count) and
- * whose K is long runs each tile as S work items over consecutive runs of
- * K tiles, S the largest power of two up to 16 with S x tiles within the
- * slots, at least 4 K tiles per run and at most 16 MiB of fp32 partial
- * planes; kernels with tiles above 128 x 128 do not split.  S depends only
- * on the GEMM and its kernel, so a GEMM gives the same bits alone and
- * concurrent.  Each run writes an fp32 M x N plane into a workspace the
- * context allocates at creation (256 MiB); a reduction kernel on the
- * dispatch's stream sums the planes in run order, scales, rounds and
- * stores C.  GEMMs of one submission that would overflow the workspace run
- * unsplit.  Submissions of one context must be ordered (one origin stream
+ * Split-K (all modes; a property of the library's kernels, not of the
+ * paper).  A GEMM whose tiles fill at most half of the CU slots its kernel
+ * has (CUs x occupancy; a grid cap does not count) and whose K is long runs
+ * each tile as S work items over consecutive runs of K tiles: S is the
+ * largest power of two up to 16 with S x tiles within the slots, at least
+ * 16 K tiles per run and at most 16 MiB of fp32 partial planes; kernels with
+ * tiles above 128 x 128 do not split.  S depends only on the GEMM and its
+ * kernel -- never on what runs at the same time -- so a variant gives a GEMM
+ * the same bits alone and concurrent.  Each run writes an fp32 M x N plane
+ * into a workspace the context allocates at creation (256 MiB); a reduction
+ * kernel on the dispatch's stream sums the planes in run order, scales,
+ * rounds and stores C.  The split GEMMs of a group take consecutive regions
+ * of the workspace and groups reuse it (in SEQUENTIAL each GEMM starts at
+ * the beginning); a split GEMM that no longer fits in what its group has
+ * left moves, with its split, to a group appended after the others (the plan
+ * shows it).  Submissions of one context must be ordered (one origin stream
  * at a time): they share the workspace.
  */
 
@@ -194,13 +198,18 @@ typedef struct {
 typedef struct gdy_ctx gdy_ctx;
 
 /*
- * Create a context on HIP device `device`.  Loads the catalogue, queries
- * each kernel's occupancy, creates `max_streams` (1..64; 0 means 16) pool
- * streams at default priority and their events.  `table_path` names a GO
- * table written by the offline tuner (NULL or "" = none: SELECTOR and GO
- * modes then fall back to isolated heuristics and report fallback = 1).
- * A table built for another device, or naming a variant the library does
- * not have, returns GDY_ERR_TABLE.
+ * Create a context on HIP device `device` (the one-time set-up of Sec. 4.1:
+ * the GO library tuned offline for this GPU, Sec. 4.2, and the concurrency
+ * the runtime may use).  Loads the catalogue, queries each kernel's
+ * occupancy, creates `max_streams` (1..64; 0 means 16) pool streams at
+ * default priority and their events, and allocates the split-K workspace.
+ * `table_path` names a GO table written by the offline tuner.  Without a
+ * usable table -- NULL or "", missing, unreadable, built for another device
+ * or naming a variant the library does not have -- the context still
+ * returns GDY_OK: SELECTOR and GO modes fall back to isolated heuristics
+ * (every GEMM at CD 1, i.e. isolated kernels one after another, Sec. 5.5's
+ * sequential configuration) and every plan reports fallback = 1;
+ * gdy_last_error() gives the reason until the next call.
  * `use_cu_masks` is a bit set: bit 0 creates one CU-masked stream for each
  * resource constraint GPU/2, GPU/4 and GPU/8 (isolated runs of the tuner);
  * bit 1 creates the CU-Partition streams (2 + 4 + 8 streams whose masks
@@ -242,23 +251,32 @@ gdy_status gdy_plan(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode
                     int32_t forced_cd, gdy_plan_t* out);
 
 /*
- * Plan and launch a submission.  Asynchronous to the host: the work is
+ * Plan and launch a submission: the problem statement of Sec. 4.1 -- given a
+ * set of independent GEMMs, predict a performant CD and schedule that many
+ * GEMMs at a time with the kernels tuned for it (SELECTOR, Sec. 4.3), or run
+ * one of the other execution configurations of Sec. 5.5 (see gdy_mode).
+ * `gemms` (host array of n descriptors, read during the call only) names
+ * caller-owned device buffers.  Asynchronous to the host: the work is
  * ordered after what is already on `hip_stream` (a hipStream_t; NULL is the
  * null stream) and `hip_stream` is ordered after all of it when this
- * returns.  `out` (nullable) receives the plan.  On GDY_ERR_HIP the streams
- * are still joined back to the origin stream.
+ * returns.  `out` (nullable) receives the plan.  Every descriptor is
+ * validated before anything launches (all or nothing).  On GDY_ERR_HIP the
+ * streams are still joined back to the origin stream.
  */
 gdy_status gdy_execute(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode,
                        int32_t forced_cd, void* hip_stream, gdy_plan_t* out);
 
 /*
- * Per-kernel timing.  When enabled, every dispatch of gdy_execute records a
- * start and a stop event on the stream it runs on (hipExtLaunchKernel), and
- * a submission start event on the origin stream.  After the caller has
- * synchronised, gdy_last_kernel_times fills start_ms[i] / end_ms[i]
- * (milliseconds from the submission start) for GEMM i of the last
- * submission; GEMMs that launched nothing get -1.  GEMMs that share a
- * dispatch report that dispatch's interval.
+ * Per-kernel timing (Sec. 5.3 measures each GEMM's kernel runtime, with the
+ * GEMMs run back-to-back on their streams).  When enabled, every dispatch
+ * of gdy_execute records a start and a stop event on the stream it runs on
+ * (hipExtLaunchKernel), and a submission start event on the origin stream.
+ * After the caller has synchronised, gdy_last_kernel_times fills
+ * start_ms[i] / end_ms[i] (host arrays of n floats; milliseconds from the
+ * submission start) for GEMM i of the last submission; GEMMs that launched
+ * nothing get -1.  GEMMs that share a dispatch report that dispatch's
+ * interval (a split GEMM's interval ends with its reduction).
+ * GDY_ERR_INVALID_ARG when no timed submission exists or a pointer is NULL.
  */
 gdy_status gdy_set_timing(gdy_ctx* ctx, int32_t enable);
 gdy_status gdy_last_kernel_times(gdy_ctx* ctx, float* start_ms, float* end_ms, int32_t n);

@@ -340,23 +340,20 @@ void uncap_mixed_group(const gdy_ctx* ctx, const gdy_gemm* g, const std::vector<
 // longest item; direct kernels count 1.5x faster.
 const double kUnifyUs = 100.0;
 double roofline_s(const gdy_gemm& g);
-int split_for(const gdy_ctx* ctx, int vid, const gdy_gemm& g, int64_t work);
-int64_t gemm_work(const gdy_ctx* ctx, int vid, const gdy_gemm& g);
+int split_for(const gdy_ctx* ctx, int vid, const gdy_gemm& g);
+bool active(const gdy_gemm& g);
 
 double group_cost(const gdy_ctx* ctx, int vid, const gdy_gemm* g, const std::vector<int>& grp) {
   const Kernel& k = ctx->kernels[ctx->variants[vid].kernel];
   const double per = std::max(k.d->bm * (double)k.d->bn / 128.0, (double)(k.d->bm + k.d->bn));
   const double area = k.d->bm * (double)k.d->bn;
-  int64_t work = 0;
-  for (int i : grp)
-    if (g[i].op != GDY_OP_ADD) work += gemm_work(ctx, vid, g[i]);
   double f = 0.0, longest = 0.0;
   for (int i : grp) {
     if (g[i].op == GDY_OP_ADD) continue;
     const Geometry geo = geometry(ctx, vid, g[i]);
     f += (double)geo.tiles * ((double)g[i].k * per + area);
     const int64_t nk = (g[i].k + k.d->bk - 1) / k.d->bk;
-    const int64_t s = split_for(ctx, vid, g[i], work);
+    const int64_t s = split_for(ctx, vid, g[i]);
     const double item = (double)(((nk + s - 1) / s) * k.d->bk) * per + area;
     longest = std::max(longest, item);
   }
@@ -665,26 +662,27 @@ int pool_size(const gdy_ctx* ctx) {
   return (int)ctx->pool.size();
 }
 
-// Split-K runs of GEMM g on variant vid (1: none).  `work` is the K tiles
-// summed over every tile of g and of the GEMMs running at the same time;
-// work / slots (CUs x occupancy; a grid cap does not enter, so a cap never
-// changes a tile's sum) is the K length each slot would get if the work
-// were spread evenly.  S doubles (up to kMaxSplit) while each of 2S runs
-// stays at least that long, keeps kMinSplitKTiles K tiles, and the 2S fp32
-// M x N planes (of every batch item) fit in kSplitMemberBytes; then S
-// shrinks to the number of runs of ceil(K tiles / S) tiles, so no run is
-// empty.  Alone, this splits until the tiles' runs fill the slots; in a
-// group, it splits the members whose K is long next to the rest.
-int split_for(const gdy_ctx* ctx, int vid, const gdy_gemm& g, int64_t work) {
+// Split-K runs of GEMM g on variant vid (1: none), a function of the GEMM
+// and its kernel only -- never of what runs at the same time -- so a kernel
+// gives a GEMM the same bits alone and concurrent.  slots = CUs x occupancy
+// (a grid cap does not enter: a split GEMM runs uncapped).  S doubles (up to
+// kMaxSplit) while 2S work items per tile (over every batch item) still fit
+// in the slots, each of the 2S runs keeps kMinSplitKTiles K tiles, and the
+// 2S fp32 M x N planes fit in kSplitMemberBytes; then S shrinks to the number
+// of runs of ceil(K tiles / S) tiles, so no run is empty.  So a GEMM whose
+// tiles leave most of the GPU idle and whose K is long splits until its runs
+// fill the GPU.
+int split_for(const gdy_ctx* ctx, int vid, const gdy_gemm& g) {
   if (vid < 0 || g.op == GDY_OP_ADD || g.k <= 0 || !active(g)) return 1;
   const Variant& v = ctx->variants[vid];
   const Kernel& k = ctx->kernels[v.kernel];
   if (k.d->ew || !k.d->func_split || k.d->bm * k.d->bn > kSplitMaxTile) return 1;
   const int64_t slots = (int64_t)ctx->cus * std::max(k.occupancy, 1);
+  const int64_t tiles = geometry(ctx, vid, g).tiles;
   const int64_t nk = (g.k + k.d->bk - 1) / k.d->bk;
   const int64_t plane_bytes = (int64_t)g.m * g.n * std::max(g.batch, 1) * 4;
   int64_t s = 1;
-  while (s * 2 <= kMaxSplit && nk * slots >= s * 2 * work && nk >= s * 2 * kMinSplitKTiles &&
+  while (s * 2 <= kMaxSplit && s * 2 * tiles <= slots && nk >= s * 2 * kMinSplitKTiles &&
          s * 2 * plane_bytes <= kSplitMemberBytes)
     s *= 2;
   if (s > 1) {
@@ -699,43 +697,111 @@ int64_t split_ws_bytes(const gdy_gemm& g, int s) {
   return ((int64_t)g.m * g.n * std::max(g.batch, 1) * s * 4 + 255) / 256 * 256;
 }
 
-// split_of for every launched GEMM, in launch order, within the workspace;
-// a split GEMM runs its kernel uncapped.
-// The GEMMs running at the same time are the GEMM alone (SEQUENTIAL) or
-// its group (every other mode: a group's dispatches or streams run
-// together); their work, adds aside, sets the even share per slot.
-int64_t gemm_work(const gdy_ctx* ctx, int vid, const gdy_gemm& g) {
-  const KernelDesc* d = ctx->kernels[ctx->variants[vid].kernel].d;
-  if (g.op == GDY_OP_ADD || d->ew || d->bk <= 0) return 0;  // adds have no K
-  return (int64_t)geometry(ctx, vid, g).tiles * ((g.k + d->bk - 1) / d->bk);
+bool grouped_mode(int mode) { return mode == GDY_GO || mode == GDY_SELECTOR || mode == GDY_FORCED_GROUPED; }
+
+// Bytes of split-K workspace a plan needs at once: the split GEMMs of a
+// group take consecutive regions (a group's GEMMs run at the same time) and
+// groups run one after another, so the need is the largest group's sum; in
+// SEQUENTIAL every GEMM runs alone on one stream and starts at offset 0.
+int64_t plan_ws_need(const gdy_gemm* g, const gdy_plan_t& p, int mode) {
+  int64_t need = 0, ws = 0;
+  int cur = -1;
+  for (int t = 0; t < GDY_MAX_GEMMS && p.order[t] >= 0; ++t) {
+    const int i = p.order[t];
+    if (p.group_of[i] != cur || mode == GDY_SEQUENTIAL) {
+      cur = p.group_of[i];
+      ws = 0;
+    }
+    if (p.split_of[i] > 1) ws += split_ws_bytes(g[i], p.split_of[i]);
+    need = std::max(need, ws);
+  }
+  return need;
 }
 
+// split_of for every launched GEMM (split_for: the GEMM and its kernel
+// alone decide); a split GEMM runs its kernel uncapped (its runs are meant
+// to spread over the GPU; a cap changes where a tile runs, never its sum).
+// A split GEMM whose planes no longer fit in what its group has left of the
+// kSplitWsBytes workspace keeps its split and moves to a group appended
+// after the others (filled greedily in launch order), so the workspace
+// never changes a GEMM's bits, only when it runs.  A single GEMM's planes
+// (<= kSplitMemberBytes) always fit.
 void plan_splits(const gdy_ctx* ctx, const gdy_gemm* g, gdy_plan_t* p, int mode) {
-  std::vector<int64_t> group_work(GDY_MAX_GEMMS, 0);
-  for (int t = 0; t < GDY_MAX_GEMMS && p->order[t] >= 0; ++t) {
-    const int i = p->order[t];
-    if (p->variant_of[i] >= 0 && g[i].op != GDY_OP_ADD && p->group_of[i] >= 0)
-      group_work[p->group_of[i]] += gemm_work(ctx, p->variant_of[i], g[i]);
-  }
-  int64_t ws = 0;
-  for (int t = 0; t < GDY_MAX_GEMMS && p->order[t] >= 0; ++t) {
+  int L = 0;
+  while (L < GDY_MAX_GEMMS && p->order[L] >= 0) ++L;
+  for (int t = 0; t < L; ++t) {
     const int i = p->order[t];
     if (p->variant_of[i] < 0) continue;
-    const int64_t work = mode == GDY_SEQUENTIAL ? gemm_work(ctx, p->variant_of[i], g[i])
-                                                : group_work[p->group_of[i]];
-    int s = split_for(ctx, p->variant_of[i], g[i], work);
-    if (s > 1) {
-      const int64_t b = split_ws_bytes(g[i], s);
-      if (ws + b > kSplitWsBytes) {
-        s = 1;
-      } else {
-        ws += b;
-        // the runs are meant to spread over the GPU: a split GEMM's grid is
-        // not capped (a cap changes where a tile runs, never its sum)
-        p->variant_of[i] = ctx->variants[p->variant_of[i]].uncapped;
-      }
-    }
+    const int s = split_for(ctx, p->variant_of[i], g[i]);
+    if (s > 1) p->variant_of[i] = ctx->variants[p->variant_of[i]].uncapped;
     p->split_of[i] = s;
+  }
+  if (mode == GDY_SEQUENTIAL) return;
+  std::vector<int> keep, deferred;
+  int64_t ws = 0;
+  int cur = -1;
+  for (int t = 0; t < L; ++t) {
+    const int i = p->order[t];
+    if (p->group_of[i] != cur) {
+      cur = p->group_of[i];
+      ws = 0;
+    }
+    if (p->split_of[i] > 1) {
+      const int64_t b = split_ws_bytes(g[i], p->split_of[i]);
+      if (ws > 0 && ws + b > kSplitWsBytes) {
+        deferred.push_back(i);
+        continue;
+      }
+      ws += b;
+    }
+    keep.push_back(i);
+  }
+  if (deferred.empty()) return;
+  // the kept members keep their groups (none empties: a group's first split
+  // GEMM always fits); the deferred ones form new groups after them
+  for (int q = 0; q < p->n_groups; ++q) p->group_size[q] = 0;
+  for (int i : keep) ++p->group_size[p->group_of[i]];
+  const int S = pool_size(ctx);
+  std::vector<int> grp;
+  auto close_group = [&]() {
+    if (grp.empty()) return;
+    const int q = p->n_groups++;
+    p->group_size[q] = (int)grp.size();
+    for (int i : grp) p->group_of[i] = q;
+    if (grouped_mode(mode)) {
+      form_dispatches(ctx, grp, S, p);
+    } else {  // one dispatch per GEMM on its planned stream (partition, pool slot)
+      for (int i : grp) p->dispatch_of[i] = p->n_dispatches++;
+    }
+    grp.clear();
+  };
+  ws = 0;
+  for (int i : deferred) {
+    const int64_t b = split_ws_bytes(g[i], p->split_of[i]);
+    if (ws > 0 && ws + b > kSplitWsBytes) {
+      close_group();
+      ws = 0;
+    }
+    ws += b;
+    grp.push_back(i);
+  }
+  close_group();
+  // launch order: kept, then deferred; dispatches renumbered by first use
+  int t = 0;
+  for (int i : keep) p->order[t++] = i;
+  for (int i : deferred) p->order[t++] = i;
+  std::vector<int> remap(p->n_dispatches, -1);
+  int nd = 0;
+  for (int u = 0; u < t; ++u) {
+    int& d = p->dispatch_of[p->order[u]];
+    if (d < 0) continue;
+    if (remap[d] < 0) remap[d] = nd++;
+    d = remap[d];
+  }
+  p->n_dispatches = nd;
+  if (grouped_mode(mode)) {
+    p->cd = 0;
+    for (int q = 0; q < p->n_groups; ++q) p->cd = std::max(p->cd, p->group_size[q]);
   }
 }
 
@@ -1057,7 +1123,7 @@ hipStream_t slot_stream(const gdy_ctx* ctx, int slot) {
 // of 8 so each GEMM starts on XCD 0 (the extra workgroups find no tile).
 gdy_status build_launch(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p,
                         const std::vector<int>& members, const std::vector<int64_t>& ws_off,
-                        KLaunch* L, int* grid, bool* split) {
+                        float* ws_base, int64_t ws_cap, KLaunch* L, int* grid, bool* split) {
   std::memset(L, 0, sizeof *L);
   L->count = (int)members.size();
   *split = false;
@@ -1072,12 +1138,12 @@ gdy_status build_launch(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p,
     if (s > 1) {  // every tile in s K runs; a capped variant keeps its cap
       const Variant& v = ctx->variants[p.variant_of[i]];
       const KernelDesc* d = ctx->kernels[v.kernel].d;
-      if (!ctx->split_ws || ws_off[i] < 0 || ws_off[i] + split_ws_bytes(g[i], s) > kSplitWsBytes)
+      if (!ws_base || ws_off[i] < 0 || ws_off[i] + split_ws_bytes(g[i], s) > ws_cap)
         return fail(ctx, GDY_ERR_UNSUPPORTED, "gemm %d: split-K workspace exhausted", i);
       const int64_t nk = (g[i].k + d->bk - 1) / d->bk;
       L->g[u].split = s;
       L->g[u].split_kt = (int32_t)((nk + s - 1) / s);
-      L->g[u].ws = ctx->split_ws + ws_off[i] / 4;
+      L->g[u].ws = ws_base + ws_off[i] / 4;
       span = (int)std::min<int64_t>((int64_t)geo.tiles * s,
                                     v.cap > 0 ? (int64_t)v.cap * std::max(ctx->kernels[v.kernel].occupancy, 1)
                                               : INT32_MAX);
@@ -1115,7 +1181,7 @@ void build_reduce(const gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, co
 }
 
 gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, int mode,
-                       hipStream_t origin) {
+                       hipStream_t origin, float* ws_base, int64_t ws_cap) {
   gdy_status st = GDY_OK;
   const int n = p.n;
   // stream slots: the pool (or the active CU budget's pool), or the CU
@@ -1126,12 +1192,19 @@ gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, int
     return fail(ctx, GDY_ERR_UNSUPPORTED, "no CU partitions: create the context with use_cu_masks & 2");
   auto stream_at = [&](int s) { return parted ? ctx->parts[pr][s] : slot_stream(ctx, s); };
   auto done_at = [&](int s) { return parted ? ctx->part_done[pr][s] : ctx->done[s]; };
-  // split-K workspace: consecutive regions in launch order (as planned)
+  // split-K workspace: consecutive regions per group in launch order (the
+  // groups run one after another and reuse it; in SEQUENTIAL each GEMM runs
+  // alone on the origin stream and starts at offset 0), as plan_ws_need counts
   std::vector<int64_t> ws_off(n > 0 ? n : 1, -1);
   {
     int64_t ws = 0;
+    int cur = -1;
     for (int t = 0; t < GDY_MAX_GEMMS && p.order[t] >= 0; ++t) {
       const int i = p.order[t];
+      if (p.group_of[i] != cur || mode == GDY_SEQUENTIAL) {
+        cur = p.group_of[i];
+        ws = 0;
+      }
       if (p.split_of[i] <= 1) continue;
       ws_off[i] = ws;
       ws += split_ws_bytes(g[i], p.split_of[i]);
@@ -1195,7 +1268,7 @@ gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, int
       KLaunch launch;
       int grid = 0;
       bool split = false;
-      st = build_launch(ctx, g, p, members[u], ws_off, &launch, &grid, &split);
+      st = build_launch(ctx, g, p, members[u], ws_off, ws_base, ws_cap, &launch, &grid, &split);
       if (st != GDY_OK) break;
       void* argv[] = {&launch};
       const int d = ids[u];
@@ -1389,6 +1462,19 @@ static int host_occupancy(const KernelDesc* d) {
   return std::max(1, std::min(by_lds, by_waves));
 }
 
+// A missing, unreadable or mismatched GO table (another device, a variant
+// the library does not have) leaves the context without a table: SELECTOR
+// and GO then use the isolated heuristics, plans report fallback = 1, and
+// gdy_last_error() keeps the reason until the next call.
+static void open_table(gdy_ctx* ctx, const char* table_path) {
+  if (!table_path || !table_path[0]) return;
+  if (load_table(ctx, table_path) != GDY_OK) {
+    fprintf(stderr, "gdy_create: GO table not used (%s); isolated heuristics, fallback = 1\n", ctx->err.c_str());
+    ctx->table = Table();
+    ctx->err = "GO table not used: " + ctx->err;
+  }
+}
+
 static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, int32_t max_streams,
                               int32_t use_cu_masks) {
   const bool host_only = device < 0;
@@ -1471,7 +1557,7 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
   if (S > 64) return fail(ctx, GDY_ERR_INVALID_ARG, "max_streams %d > 64", S);
   if (host_only) {
     ctx->host_slots = S;
-    if (table_path && table_path[0]) return load_table(ctx, table_path);
+    open_table(ctx, table_path);
     return GDY_OK;
   }
   for (int s = 0; s < S; ++s) {
@@ -1526,11 +1612,7 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
   }
   HIP_TRY(ctx, hipEventCreateWithFlags(&ctx->fork_ev, hipEventDisableTiming));
   HIP_TRY(ctx, hipMalloc((void**)&ctx->split_ws, kSplitWsBytes));
-
-  if (table_path && table_path[0]) {
-    gdy_status s = load_table(ctx, table_path);
-    if (s != GDY_OK) return s;
-  }
+  open_table(ctx, table_path);
   return GDY_OK;
 }
 
@@ -1604,21 +1686,28 @@ gdy_status gdy_plan(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode
   return GDY_OK;
 }
 
-gdy_status gdy_execute(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode, int32_t forced_cd,
-                       void* hip_stream, gdy_plan_t* out) {
+static gdy_status execute_impl(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode, int32_t forced_cd,
+                               void* hip_stream, gdy_plan_t* out) {
   if (!ctx) return GDY_ERR_INVALID_ARG;
   gdy_plan_t local;
   gdy_plan_t* p = out ? out : &local;
   gdy_status s = gdy_plan(ctx, gemms, n, mode, forced_cd, p);
   if (s != GDY_OK) return s;
   if (ctx->device < 0) return fail(ctx, GDY_ERR_UNSUPPORTED, "host-only context cannot execute");
+  float* ws = ctx->split_ws;
+  const int64_t cap = kSplitWsBytes;
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess || cur != ctx->device) HIP_TRY(ctx, hipSetDevice(ctx->device));
   try {
-    return launch_plan(ctx, gemms, *p, mode, (hipStream_t)hip_stream);
+    return launch_plan(ctx, gemms, *p, mode, (hipStream_t)hip_stream, ws, cap);
   } catch (...) {
     return fail(ctx, GDY_ERR_NOMEM, "host allocation failed");
   }
+}
+
+gdy_status gdy_execute(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode, int32_t forced_cd,
+                       void* hip_stream, gdy_plan_t* out) {
+  return execute_impl(ctx, gemms, n, mode, forced_cd, hip_stream, out);
 }
 
 gdy_status gdy_set_timing(gdy_ctx* ctx, int32_t enable) {

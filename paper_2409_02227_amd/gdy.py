@@ -266,6 +266,11 @@ class Context:
         except Exception:
             pass
 
+    def last_error(self) -> str:
+        """gdy_last_error: the message of the last failure (after creation:
+        why a GO table was not used), "" if none."""
+        return self.lib.gdy_last_error(self.h).decode()
+
     def _check(self, st):
         if st != 0:
             raise GdyError(st, self.lib.gdy_last_error(self.h).decode())

@@ -518,8 +518,8 @@ def test_split_k_every_small_tile_kernel(ctx):
     """Every kernel with tiles up to 128x128 on a GEMM of three tiles and a
     long K (whole K tiles, and a ragged K tail for staged kernels): the plan
     splits it; the result meets the oracle's bound, repeats bit for bit, and
-    is bit-identical fused with another GEMM whenever the plan gives it the
-    same number of K runs there."""
+    is bit-identical fused with another GEMM (the split count depends on the
+    GEMM and its kernel only)."""
     for vid, v in _kernels(ctx):
         if v["bm"] * v["bn"] > 128 * 128:
             continue
@@ -540,18 +540,16 @@ def test_split_k_every_small_tile_kernel(ctx):
             assert np.array_equal(out_codes(mat), ref), f"{label}: repeat differs"
             alone = plan["split_of"][0]
             plan = _run(ctx, [other, mat], "forced_grouped", 0, [vid, vid])
-            assert plan["n_dispatches"] == 1 and plan["split_of"][1] > 1, label
-            if plan["split_of"][1] == alone:
-                assert np.array_equal(out_codes(mat), ref), f"{label}: fused differs"
-            else:
-                check(mat, label=label + " fused")
+            assert plan["n_dispatches"] == 1 and plan["split_of"][1] == alone, label
+            assert np.array_equal(out_codes(mat), ref), f"{label}: fused differs"
             check(other, label=label + " co-runner")
 
 
 def test_split_k_batched_and_modes(ctx):
     """A strided batch of skinny GEMMs and a set of skinny GEMMs in every
     execution mode: split plans, oracle bound, bits equal across modes that
-    bind the same variant."""
+    bind the same kernel (a grid cap changes where a tile runs, never its
+    bits; the split count follows the GEMM and its kernel)."""
     b = inputs.materialize(GemmSpec(20, 100, 3000, "bf16", seed=5900, batch=5, name="bsplit"))
     plan = _run(ctx, [b], "sequential")
     assert plan["split_of"][0] > 1
@@ -565,7 +563,7 @@ def test_split_k_batched_and_modes(ctx):
         assert any(s > 1 for s in plan["split_of"]), mode
         for i, m in enumerate(mats):
             check(m, label=f"{mode} {m.spec.name}")
-            key = (i, plan["variant_of"][i], plan["split_of"][i])
+            key = (i, ctx.variant(plan["variant_of"][i])["name"].rsplit("_c", 1)[0])
             if key in seen:
                 assert np.array_equal(seen[key], out_codes(m)), f"{mode} {m.spec.name}"
             seen[key] = out_codes(m).copy()

@@ -34,6 +34,16 @@ def test_oracle_hand_cases():
     assert oknn.predict(xs, [0, 1, 2, 3], (0.0, 0.0), 4) == 0      # four-way tie
 
 
+def test_oracle_feature_hand_values():
+    """Sec. 7.5 features: log2 of the output size and of the default
+    kernel's tile area (a batch counts every item's output)."""
+    rec = {"shape": ["bf16", 0, 0, 64, 4096, 1024], "rc_best": {"0": ["k64x128_c0"]}}
+    assert oknn.feature(rec, {"k64x128_c0": 64 * 128}) == (18.0, 13.0)   # 2^6 x 2^12; 2^13
+    rec = {"shape": ["bf16", 0, 1, 256, 256, 64, 12], "rc_best": {"0": ["k128_c0"]}}
+    x = oknn.feature(rec, {"k128_c0": 128 * 128})  # 12 x 2^16 outputs: 16 + log2(12) = 19.58496...
+    assert abs(x[0] - 19.584962500721156) < 1e-12 and x[1] == 14.0
+
+
 @pytest.mark.skipif(not os.path.exists(RECORDS), reason="no tuning records")
 def test_preferred_slots_hold_every_go_kernel():
     recs = [json.loads(line) for line in open(RECORDS)]

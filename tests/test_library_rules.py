@@ -1,0 +1,344 @@
+"""The library's own planning rules -- not defined by the paper, so not in the
+oracle -- pinned by hand-worked expected plans on a host-only context
+(gdy_create with device -1: 256 CUs, each kernel's occupancy from its LDS
+size and wave count).  Every expected value is derived in the comment next
+to it from the rule as documented in include/gdy.h and the kernel
+descriptions (tile, K tile, occupancy) the context reports.
+
+Rules covered: split-K (a function of the GEMM and its kernel only), the
+workspace budget with deferred groups, fused group dispatches, the nearest
+tuned shape for untuned GEMMs, the direct-to-staged kernel substitution,
+grid caps dropped in mixed groups, one kernel for short groups (its roofline
+threshold and its tile-cost model), and the element-wise add's slot rule.
+"""
+import pytest
+
+from paper_2409_02227_amd import gdy
+
+K64 = "bf16_nn_64x64_w2x2_d4"       # 64 x 64 tile, K tile 64, occupancy 2 (64 KiB of LDS)
+K128 = "bf16_nn_128x128_w2x2_d2"    # 128 x 128, K tile 64, occupancy 2 (64 KiB)
+K128S = "bf16_nn_128x128_w2x2_m32"  # its register-staged twin (same tile)
+K256 = "bf16_nn_256x256_w2x4_d2"    # 256 x 256, K tile 64, occupancy 1 (128 KiB)
+K32 = "bf16_nn_32x128_w1x4_d4"      # 32 x 128, K tile 64, occupancy 2 (80 KiB)
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    c = gdy.Context(-1)
+    yield c
+    c.close()
+
+
+def test_kernel_descriptions(ctx):
+    """The numbers the derivations below use."""
+    want = {K64: (64, 64, 64, 2, 1), K128: (128, 128, 64, 2, 1), K128S: (128, 128, 64, 2, 0),
+            K256: (256, 256, 64, 1, 1), K32: (32, 128, 64, 2, 1)}
+    for name, (bm, bn, bk, occ, direct) in want.items():
+        v = ctx.variant(ctx.find(name + "_c0"))
+        assert (v["bm"], v["bn"], v["bk"], v["occupancy"], v["direct"]) == (bm, bn, bk, occ, direct), name
+    assert ctx.cus() == 256
+
+
+def desc(m, n, k, slot, variant=-1, batch=0, ta=0, tb=0, pad=0):
+    d = gdy.GemmDesc()
+    d.m, d.n, d.k = m, n, k
+    d.a_type = d.b_type = d.c_type = 2
+    d.trans_a, d.trans_b = ta, tb
+    d.lda, d.ldb, d.ldc = (m if ta else k) + pad, (k if tb else n) + pad, n
+    base = (slot + 1) << 40
+    d.a, d.b, d.c = base, base + (1 << 38), base + (2 << 38)
+    d.scale_a = d.scale_b = 1.0
+    d.variant = variant
+    if batch:
+        d.batch = batch
+        d.stride_a, d.stride_b, d.stride_c = m * k, k * n, m * n
+    return d
+
+
+def v(ctx, name):
+    return ctx.find(name)
+
+
+# --------------------------------------------------------------------------
+# split-K: S = largest power of two <= 16 with S x tiles <= CUs x occupancy,
+# at least 16 K tiles per run and S fp32 M x N planes within 16 MiB; tiles
+# above 128 x 128 never split
+# --------------------------------------------------------------------------
+
+SPLIT_CASES = [
+    # (16, 1024, 8192) on 64x64: tiles 1 x 16 = 16, slots 256 x 2 = 512,
+    # K tiles 8192/64 = 128.  S = 8: 8 x 16 = 128 <= 512 and 128 >= 8 x 16;
+    # S = 16 needs 256 K tiles.  Planes 8 x 16 x 1024 x 4 B = 512 KiB.
+    ((16, 1024, 8192), K64, 0, 8),
+    # K = 1024: 16 K tiles, S = 2 would need 32
+    ((16, 1024, 1024), K64, 0, 1),
+    # (512, 4096, 8192) on 64x64: tiles 8 x 64 = 512 fill the 512 slots
+    ((512, 4096, 8192), K64, 0, 1),
+    # (16, 8192, 8192) on 128x128: tiles 1 x 64 = 64; S = 8: 512 <= 512;
+    # planes 8 x 16 x 8192 x 4 B = 4 MiB
+    ((16, 8192, 8192), K128, 0, 8),
+    # (128, 8192, 8192) on 128x128: tiles 64; slots allow 8, but 8 planes of
+    # 128 x 8192 x 4 B = 4 MiB are 32 MiB > 16 MiB: S = 4 (16 MiB)
+    ((128, 8192, 8192), K128, 0, 4),
+    # a batch of 4 x (16, 1024, 8192) on 64x64: tiles 4 x 16 = 64; S = 8:
+    # 512 <= 512, planes 8 x 4 x 16 x 1024 x 4 B = 2 MiB
+    ((16, 1024, 8192), K64, 4, 8),
+    # 256 x 256 tiles never split
+    ((16, 1024, 8192), K256, 0, 1),
+]
+
+
+@pytest.mark.parametrize("shape,kernel,batch,want", SPLIT_CASES)
+def test_split_count_hand_values(ctx, shape, kernel, batch, want):
+    d = desc(*shape, 0, v(ctx, kernel + "_c0"), batch=batch)
+    p = ctx.plan([d], mode="forced")
+    assert p["split_of"][0] == want
+
+
+@pytest.mark.parametrize("shape,kernel,batch,want", [c for c in SPLIT_CASES if c[3] > 1])
+def test_split_does_not_depend_on_co_runners(ctx, shape, kernel, batch, want):
+    """The same GEMM on the same kernel splits the same way alone, in a group
+    of eight (FORCED_GROUPED), next to a large GEMM, and in GO mode: a kernel
+    gives a GEMM the same bits alone and concurrent."""
+    vid = v(ctx, kernel + "_c0")
+    alone = ctx.plan([desc(*shape, 0, vid, batch=batch)], mode="forced")["split_of"][0]
+    eight = ctx.plan([desc(*shape, j, vid, batch=batch) for j in range(8)], mode="forced_grouped", forced_cd=8)
+    big = ctx.plan([desc(4096, 4096, 4096, 0, v(ctx, K128 + "_c0")), desc(*shape, 1, vid, batch=batch)],
+                   mode="forced_grouped", forced_cd=2)
+    assert alone == want and eight["split_of"][:8] == [want] * 8 and big["split_of"][1] == want
+    assert big["split_of"][0] == 1  # 32 x 32 = 1024 tiles of 4096^2 overfill 512 slots
+
+
+def test_capped_variant_splits_uncapped(ctx):
+    """A split GEMM runs its kernel without the grid cap (the runs spread over
+    the GPU; a cap only changes where a tile runs)."""
+    p = ctx.plan([desc(16, 1024, 8192, 0, v(ctx, K64 + "_c64"))], mode="forced")
+    assert p["split_of"][0] == 8 and p["variant_of"][0] == v(ctx, K64 + "_c0")
+    p = ctx.plan([desc(16, 1024, 1024, 0, v(ctx, K64 + "_c64"))], mode="forced")
+    assert p["split_of"][0] == 1 and p["variant_of"][0] == v(ctx, K64 + "_c64")
+
+
+# --------------------------------------------------------------------------
+# workspace: a group's split GEMMs share 256 MiB; the overflow moves, with its
+# split, to groups appended after the others
+# --------------------------------------------------------------------------
+
+def test_overflowing_split_gemms_move_to_later_groups(ctx):
+    # (128, 8192, 8192) on 128x128 splits 4 ways: 4 planes of 4 MiB = 16 MiB.
+    # 40 of them in one FORCED_GROUPED group: 16 fit (256 MiB), 24 move.  The
+    # group's 40 GEMMs of one kernel were dispatches of 16, 16 and 8; the
+    # kept 16 are the first dispatch (origin stream).  The deferred 24 fill
+    # new groups greedily: 16 (256 MiB), then 8, each one dispatch on the
+    # origin stream.  Dispatches renumbered in launch order: 0, 1, 2.
+    vid = v(ctx, K128 + "_c0")
+    descs = [desc(128, 8192, 8192, j, vid) for j in range(40)]
+    p = ctx.plan(descs, mode="forced_grouped", forced_cd=40)
+    assert p["split_of"] == [4] * 40
+    assert p["n_groups"] == 3 and p["group_size"] == [16, 16, 8] and p["cd"] == 16
+    assert p["order"] == list(range(40))
+    assert p["group_of"] == [0] * 16 + [1] * 16 + [2] * 8
+    assert p["n_dispatches"] == 3 and p["dispatch_of"] == [0] * 16 + [1] * 16 + [2] * 8
+    assert p["stream_of"] == [-1] * 40
+
+
+def test_overflow_in_default_mode_keeps_streams(ctx):
+    # DEFAULT: 20 GEMMs on streams t mod 16, one dispatch each.  16 fit; the
+    # last 4 (streams 0..3) form group 1 with dispatches 16..19.
+    descs = [desc(128, 8192, 8192, j) for j in range(20)]
+    for d in descs:  # pin the kernel: DEFAULT binds the isolated one, so use a table-free forced plan
+        d.variant = v(ctx, K128 + "_c0")
+    p = ctx.plan(descs, mode="forced", forced_cd=16)
+    assert p["n_groups"] == 2 and p["group_size"] == [16, 4]
+    assert p["stream_of"] == [t % 16 for t in range(20)]
+    assert p["dispatch_of"] == list(range(20)) and p["n_dispatches"] == 20
+
+
+def test_sequential_needs_one_gemm_of_workspace(ctx):
+    # SEQUENTIAL runs one GEMM at a time on one stream: no deferral, 40 x
+    # 16 MiB of planes reuse one region
+    descs = [desc(128, 8192, 8192, j) for j in range(40)]
+    p = ctx.plan(descs, mode="sequential")
+    assert p["n_groups"] == 1 and p["n_dispatches"] == 40
+
+
+# --------------------------------------------------------------------------
+# fused group dispatches
+# --------------------------------------------------------------------------
+
+def test_group_dispatches_by_kernel(ctx):
+    # one group of six (forced_cd 6) with kernels A, B, A, C, B, A in
+    # submission order: A opens dispatch 0 (origin stream), B dispatch 1 (pool
+    # slot 0), C dispatch 2 (pool slot 1); later GEMMs join their kernel's
+    # dispatch.  (1024, 1024, 1024) never splits: 16 K tiles.
+    A, B, C = v(ctx, K64 + "_c0"), v(ctx, K128 + "_c0"), v(ctx, K256 + "_c0")
+    descs = [desc(1024, 1024, 1024, j, x) for j, x in enumerate([A, B, A, C, B, A])]
+    p = ctx.plan(descs, mode="forced_grouped", forced_cd=6)
+    assert p["n_groups"] == 1 and p["n_dispatches"] == 3
+    assert p["dispatch_of"] == [0, 1, 0, 2, 1, 0]
+    assert p["stream_of"] == [-1, 0, -1, 1, 0, -1]
+    # 18 GEMMs of one kernel: dispatches of 16 and 2 (at most 16 per dispatch)
+    p = ctx.plan([desc(1024, 1024, 1024, j, A) for j in range(18)], mode="forced_grouped", forced_cd=18)
+    assert p["dispatch_of"] == [0] * 16 + [1] * 2 and p["stream_of"] == [-1] * 16 + [0] * 2
+    # forced_cd 4 over six GEMMs: groups of 4 and 2, each starting on the origin
+    p = ctx.plan(descs, mode="forced_grouped", forced_cd=4)
+    assert p["group_size"] == [4, 2] and p["group_of"] == [0, 0, 0, 0, 1, 1]
+    assert p["dispatch_of"] == [0, 1, 0, 2, 3, 4] and p["stream_of"] == [-1, 0, -1, 1, -1, 0]
+
+
+# --------------------------------------------------------------------------
+# GO table lookups (synthetic tables; predictor answers one class)
+# --------------------------------------------------------------------------
+
+def _table(tmp_path, ctx, entries, cd_class=4, name="t"):
+    """A GO table whose predictor always answers CD class `cd_class` (zero
+    weights, one large bias) and the given entry lines."""
+    b = ["0.0"] * 5
+    b[cd_class] = "50.0"
+    lines = ["gdy-go-table 1", "device host cus 256", f"catalogue {ctx.catalogue_hash():016x}",
+             "lr_min " + " ".join(["0.0"] * 18), "lr_max " + " ".join(["1.0"] * 18),
+             "lr_w " + " ".join(["0.0"] * 90), "lr_b " + " ".join(b)]
+    path = tmp_path / f"{name}.table"
+    path.write_text("\n".join(lines + entries) + "\n")
+    return gdy.Context(-1, table=str(path))
+
+
+def test_nearest_tuned_shape(tmp_path, ctx):
+    # entries: E0 = (mlog 6, 4096, 1024) -> K64; E1 = (mlog 9, 4608, 12288) ->
+    # K128; E2 = (mlog 8, 4096, 1024) -> K32; an fp8 entry of E1's shape.
+    # Distance |mlog - ceil(log2 M)| + |log2 N - log2 n| + |log2 K - log2 k|.
+    fp8 = "fp8_nn_128x128_w2x2_d2_c0"
+    t = _table(tmp_path, ctx, [
+        "entry 2 0 0 6 4096 1024 " + " ".join([K64 + "_c0"] * 5),
+        "entry 2 0 0 9 4608 12288 " + " ".join([K128 + "_c0"] * 5),
+        "entry 2 0 0 8 4096 1024 " + " ".join([K32 + "_c0"] * 5),
+        "entry 3 0 0 9 4608 12288 " + " ".join([fp8] * 5)])
+    iso = lambda m, n, k: t.variant(t.isolated_variant(desc(m, n, k, 0)))["name"]  # noqa: E731
+    # (K multiples of 64 and 16-byte rows, so the direct kernels stay runnable)
+    # (500, 5000, 10048): mlog 9; E1 at 0 + 0.118 + 0.290 = 0.408; E0 at
+    # 3 + 0.288 + 3.295; E2 at 1 + 0.288 + 3.295
+    assert iso(500, 5000, 10048) == K128 + "_c0"
+    # (60, 4000, 960): mlog 6; E0 at 0 + 0.034 + 0.093
+    assert iso(60, 4000, 960) == K64 + "_c0"
+    # (128, 4096, 1024): mlog 7; E0 and E2 both at 1: the first listed wins
+    assert iso(128, 4096, 1024) == K64 + "_c0"
+    # (200, 4096, 1024): mlog 8: E2 at 0
+    assert iso(200, 4096, 1024) == K32 + "_c0"
+    # the fp8 entry serves fp8 GEMMs only (its K tile is 128 one-byte elements)
+    d = desc(500, 4608, 12288, 0)
+    d.a_type = d.b_type = 3
+    assert t.variant(t.isolated_variant(d))["name"] == fp8
+
+
+def test_direct_kernel_falls_back_to_staged(tmp_path, ctx):
+    # the entry names the direct 128x128 kernel (isolated) and its 64-CU cap
+    # (class 2); direct kernels need K % 64 == 0 and 16-byte aligned bases
+    # and rows, else the staged kernel of the same tile and cap runs
+    t = _table(tmp_path, ctx, ["entry 2 0 0 10 4096 4096 " + " ".join(
+        [K128 + "_c0", K128 + "_c64", K128 + "_c64", K128 + "_c64", K128 + "_c64"])])
+    iso = lambda d: t.variant(t.isolated_variant(d))["name"]  # noqa: E731
+    assert iso(desc(1024, 4096, 4096, 0)) == K128 + "_c0"
+    assert iso(desc(1024, 4096, 4000, 0)) == K128S + "_c0"          # 4000 % 64 = 32
+    assert iso(desc(1024, 4096, 4096, 0, pad=3)) == K128S + "_c0"   # row pitch 4099 x 2 B
+    d = desc(1024, 4096, 4096, 0)
+    d.a += 8                                                        # base not 16-byte aligned
+    assert iso(d) == K128S + "_c0"
+    # GO with two copies binds class 2 (nearest class to 2): the cap stays
+    p = t.plan([desc(1024, 4096, 4000, 0), desc(1024, 4096, 4000, 1)], mode="go")
+    assert [t.variant(x)["name"] for x in p["variant_of"][:2]] == [K128S + "_c64"] * 2
+
+
+def test_mixed_groups_run_uncapped(tmp_path, ctx):
+    # class 4 (index 2) of (512, 4096, 1024) is K128 capped at 64 CUs; no split
+    # (16 K tiles).  Four copies keep the cap; a group with another shape
+    # (700 rows, the same nearest entry) runs every kernel uncapped.
+    t = _table(tmp_path, ctx, ["entry 2 0 0 9 4096 1024 " + " ".join(
+        [K64 + "_c0", K64 + "_c128", K128 + "_c64", K128 + "_c32", K128 + "_c32"])])
+    same = [desc(512, 4096, 1024, j) for j in range(4)]
+    p = t.plan(same, mode="selector")
+    assert p["n_groups"] == 1 and [t.variant(x)["name"] for x in p["variant_of"][:4]] == [K128 + "_c64"] * 4
+    mixed = same[:3] + [desc(700, 4096, 1024, 9)]
+    p = t.plan(mixed, mode="selector")
+    assert p["n_groups"] == 1 and [t.variant(x)["name"] for x in p["variant_of"][:4]] == [K128 + "_c0"] * 4
+    p = t.plan(mixed, mode="go")
+    assert [t.variant(x)["name"] for x in p["variant_of"][:4]] == [K128 + "_c0"] * 4
+
+
+def test_short_group_threshold(tmp_path, ctx):
+    # A group whose GEMMs bind several kernels runs them all on one kernel
+    # when its roofline time is below 100 us per extra kernel.  Roofline of a
+    # bf16 GEMM: max(2MNK / 2.5 PFLOP/s, bytes / 8 TB/s).
+    #   X = (4096, 4096, 4096): 2 x 4096^3 / 2.5e15 = 54.98 us (bytes 100.7 MB:
+    #       12.6 us) -> entry kernel K256
+    #   Y = (4096, 4096, 3072): 41.23 us -> K128;  X + Y = 96.2 us < 100: one kernel
+    #   Y' = (4096, 4096, 3584): 48.10 us -> K128; X + Y' = 103.1 us: two kernels
+    # The one kernel is the cheaper under the tile model: a tile costs
+    # max(area / 128, perimeter) per K plus its area; the group takes the
+    # larger of its tiles over CUs x occupancy slots and its longest tile;
+    # direct kernels count 1.5x faster (both are direct here):
+    #   K256: per 512, area 65536; X 256 tiles x (4096 x 512 + 65536) +
+    #         Y 256 x (3072 x 512 + 65536) = 973,078,528 / 256 slots = 3,801,088
+    #   K128: per 256, area 16384; X 1024 x (4096 x 256 + 16384) +
+    #         Y 1024 x (3072 x 256 + 16384) = 1,912,602,624 / 512 = 3,735,552
+    # so K128 (uncapped).
+    t = _table(tmp_path, ctx, ["entry 2 0 0 12 4096 4096 " + " ".join([K256 + "_c0"] * 5),
+                               "entry 2 0 0 12 4096 3072 " + " ".join([K128 + "_c0"] * 5),
+                               "entry 2 0 0 12 4096 3584 " + " ".join([K128 + "_c0"] * 5)])
+    p = t.plan([desc(4096, 4096, 4096, 0), desc(4096, 4096, 3072, 1)], mode="selector")
+    assert p["n_dispatches"] == 1 and [t.variant(x)["name"] for x in p["variant_of"][:2]] == [K128 + "_c0"] * 2
+    p = t.plan([desc(4096, 4096, 4096, 0), desc(4096, 4096, 3584, 1)], mode="selector")
+    assert p["n_dispatches"] == 2
+    assert [t.variant(x)["name"] for x in p["variant_of"][:2]] == [K256 + "_c0", K128 + "_c0"]
+
+
+def test_short_group_weighs_members_isolated_kernels(tmp_path, ctx):
+    # X = (4096, 2048, 1024), Y = (16, 1024, 1024); predictor CD 16, so one
+    # group of two, class 2: X -> K32 (its CD-2 kernel), Y -> K64; X's
+    # isolated kernel is K128.  Roofline 6.87 + 0.27 us < 100: one kernel.
+    # Tile model (per K: max(area/128, perimeter); all direct, no splits:
+    # 16 K tiles):
+    #   K32:  per 160, area 4096:  X 2048 tiles, Y 8 -> 2056 x 167,936 / 512
+    #         slots = 674,369
+    #   K64:  per 128, area 4096:  X 2048, Y 16 -> 2064 x 135,168 / 512 = 544,896
+    #   K128: per 256, area 16384: X 512, Y 8 -> 520 x 278,528 / 512 = 282,880
+    # so X's isolated K128 wins; among the group's own kernels K64 would.
+    t = _table(tmp_path, ctx, ["entry 2 0 0 12 2048 1024 " + " ".join([K128 + "_c0"] + [K32 + "_c0"] * 4),
+                               "entry 2 0 0 4 1024 1024 " + " ".join([K64 + "_c0"] * 5)])
+    p = t.plan([desc(4096, 2048, 1024, 0), desc(16, 1024, 1024, 1)], mode="selector")
+    assert p["n_groups"] == 1 and p["n_dispatches"] == 1
+    assert [t.variant(x)["name"] for x in p["variant_of"][:2]] == [K128 + "_c0"] * 2
+
+
+def _add(m, n, slot):
+    d = desc(m, n, 0, slot)
+    d.lda = d.ldb = d.ldc = n
+    d.op = 1
+    return d
+
+
+def test_add_takes_a_slot_only_when_comparable(tmp_path, ctx):
+    # Entries name a different kernel per CD class so the bound class shows.
+    # An add C = A + B (M x N bf16) moves 3 x M x N x 2 bytes: roofline at 8 TB/s.
+    #   GEMM (4096, 1024, 1024): MFMA 8.59 GFLOP / 2.5e15 = 3.436 us, bytes
+    #     18.9 MB = 2.36 us -> 3.436 us.  Its add: 25.2 MB = 3.146 us >= 1.718:
+    #     the add takes a slot -> class of 2 GEMMs (index 1) when the GEMM
+    #     prefers CD >= 2.
+    #   GEMM (512, 8192, 8192): 27.49 us (bytes 151 MB: 18.9 us).  Its add
+    #     (512 x 8192): 3.146 us < 13.7: no slot -> class 1 (index 0).
+    classes = [K64 + "_c0", K64 + "_c128", K128 + "_c64", K128 + "_c32", K256 + "_c0"]
+    lines = ["entry 2 0 0 12 1024 1024 " + " ".join(classes), "entry 2 0 0 9 8192 8192 " + " ".join(classes)]
+    for cd_class, big_class, small_class in ((4, 1, 0), (0, 0, 0)):
+        t = _table(tmp_path, ctx, lines, cd_class, name=f"add{cd_class}")
+        for (m, n, k), want in (((4096, 1024, 1024), big_class), ((512, 8192, 8192), small_class)):
+            p = t.plan([_add(m, n, 0), desc(m, n, k, 1)], mode="selector")
+            assert p["n_groups"] == 1 and p["n_dispatches"] == 1 and p["order"][:2] == [1, 0]
+            assert t.variant(p["variant_of"][0])["kind"] == 1 and p["stream_of"][:2] == [-1, -1]
+            name = t.variant(p["variant_of"][1])["name"]
+            assert name == classes[want] or (p["split_of"][1] > 1 and name.startswith(classes[want][:-5])), \
+                (cd_class, m, n, k, name)
+        # several groups (CD 1 for every GEMM): the add joins the first group's first dispatch
+        descs = [desc(512, 8192, 8192, j) for j in range(3)]
+        descs.insert(1, _add(512, 4096, 9))
+        p = t.plan(descs, mode="selector")
+        if cd_class == 0:
+            assert p["n_groups"] == 3 and p["group_size"][:3] == [2, 1, 1]
+        assert p["group_of"][1] == 0 and p["dispatch_of"][1] == p["dispatch_of"][p["order"][0]]

@@ -112,10 +112,27 @@ def test_plan_invariants(descs, mode, forced):
         assert len(gemm_kernels) <= 1, (disp, gemm_kernels)
         assert len({p["group_of"][i] for i in members}) == 1
         assert len(members) <= 16
-    # the workspace holds every split GEMM's planes
-    ws = sum((descs[i].m * descs[i].n * max(descs[i].batch, 1) * p["split_of"][i] * 4 + 255) // 256 * 256
-             for i in live if p["split_of"][i] > 1)
-    assert ws <= 256 << 20
+    # the workspace holds the planes of every group's split GEMMs (groups run
+    # one after another; SEQUENTIAL runs one GEMM at a time)
+    per_group = {}
+    for i in live:
+        if p["split_of"][i] > 1:
+            key = i if mode == "sequential" else p["group_of"][i]
+            per_group[key] = per_group.get(key, 0) + \
+                (descs[i].m * descs[i].n * max(descs[i].batch, 1) * p["split_of"][i] * 4 + 255) // 256 * 256
+    assert all(b <= 256 << 20 for b in per_group.values())
+    # a GEMM's split depends on it and its kernel only: planned alone on the
+    # same variant (FORCED), it splits the same way
+    for i in live:
+        if descs[i].op == 0:
+            alone = gdy.GemmDesc.from_buffer_copy(descs[i])
+            alone.variant = p["variant_of"][i]
+            assert ctx.plan([alone], mode="forced")["split_of"][0] == p["split_of"][i], i
+    # the selector's groups never exceed a member's clamped CD (Sec. 6.7)
+    if mode == "selector" and len(live) > 1:
+        for q in range(p["n_groups"]):
+            members = [i for i in live if p["group_of"][i] == q and descs[i].op == 0]
+            assert all(len(members) <= p["pred_cd"][i] for i in members)
     # fused-dispatch modes: a group's first dispatch runs on the origin stream
     if mode in ("go", "selector", "forced_grouped"):
         first = {}

@@ -71,26 +71,35 @@ def test_written_table_reads_back(tmp_path):
     assert V[c2.isolated_variant(d)]["name"] == names[0]
 
 
-def test_library_rejects_table_naming_unknown_variants(tmp_path):
+def _falls_back(path):
+    """The library does not use the table: the context is created, its plans
+    report fallback = 1, and the last error gives the reason."""
+    ctx = gdy.Context(-1, table=path)
+    assert "GO table not used" in ctx.last_error()
+    d = gdy.GemmDesc()
+    d.m, d.n, d.k = 512, 4096, 1024
+    d.a_type = d.b_type = d.c_type = 2
+    d.lda, d.ldb, d.ldc = 1024, 4096, 4096
+    d.a, d.b, d.c = 1 << 36, 2 << 36, 3 << 36
+    d.scale_a = d.scale_b = 1.0
+    assert ctx.plan([d], mode="selector")["fallback"] == 1
+
+
+def test_library_refuses_table_naming_unknown_variants(tmp_path):
     path = str(tmp_path / "bad.table")
     open(path, "w").write("gdy-go-table 1\ndevice host cus 256\ncatalogue 0123456789abcdef\n"
                           "entry 2 0 0 9 4096 1024 a b c d e\n")
-    with pytest.raises(gdy.GdyError) as e:
-        gdy.Context(-1, table=path)
-    assert e.value.status == 5
+    _falls_back(path)
     open(path, "w").write("not a table\n")
-    with pytest.raises(gdy.GdyError):
-        gdy.Context(-1, table=path)
+    _falls_back(path)
 
 
-def test_library_rejects_the_add_kernel_in_a_gemm_entry(tmp_path):
+def test_library_refuses_the_add_kernel_in_a_gemm_entry(tmp_path):
     """A GO table entry naming the element-wise add for a GEMM shape is refused."""
     path = str(tmp_path / "ew.table")
     open(path, "w").write("gdy-go-table 1\ndevice host cus 256\ncatalogue 0123456789abcdef\n"
                           "entry 2 0 0 9 4096 1024 " + " ".join(["ew_add_bf16_c0"] * 5) + "\n")
-    with pytest.raises(gdy.GdyError) as e:
-        gdy.Context(-1, table=path)
-    assert e.value.status == 5
+    _falls_back(path)
 
 
 def test_shape_sets():
