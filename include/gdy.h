@@ -267,6 +267,26 @@ gdy_status gdy_execute(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t m
                        int32_t forced_cd, void* hip_stream, gdy_plan_t* out);
 
 /*
+ * gdy_execute for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same plan and the same kernels as gdy_execute, with the split-K
+ * planes in a static device array of GDY_STATIC_SCRATCH_BYTES that the
+ * library holds on every device it runs on until the process ends, instead
+ * of the context's workspace.  Allocates nothing, on the device or through
+ * any allocating library routine.  A plan whose split GEMMs need more than
+ * the array at once (one group's planes; one GEMM's in SEQUENTIAL) returns
+ * GDY_ERR_UNSUPPORTED before anything launches.  Every call on a device
+ * shares that device's array, which keeps the last call's partial planes
+ * (each run overwrites its plane before the reduction reads it, so nothing
+ * needs clearing): calls that overlap on one device, from any context or
+ * thread, race and must be ordered by the caller.  Results are bit-identical
+ * to gdy_execute's.
+ */
+#define GDY_STATIC_SCRATCH_BYTES (64ll * 1024 * 1024)
+gdy_status gdy_execute_static(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode,
+                              int32_t forced_cd, void* hip_stream, gdy_plan_t* out);
+
+/*
  * Per-kernel timing (Sec. 5.3 measures each GEMM's kernel runtime, with the
  * GEMMs run back-to-back on their streams).  When enabled, every dispatch
  * of gdy_execute records a start and a stop event on the stream it runs on

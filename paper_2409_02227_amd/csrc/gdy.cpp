@@ -18,6 +18,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <fstream>
+#include <mutex>
 #include <sstream>
 #include <string>
 #include <vector>
@@ -129,6 +130,7 @@ struct gdy_ctx {
   std::vector<std::vector<hipStream_t>> parts;
   std::vector<std::vector<hipEvent_t>> part_done;
   float* split_ws = nullptr;  // split-K partial planes (kSplitWsBytes)
+  float* scratch = nullptr;   // this device's static split-K array (gdy_execute_static)
   int host_slots = 0;                              // host-only context: planned stream slots
   std::vector<hipEvent_t> done;                    // one per stream slot
   hipEvent_t fork_ev = nullptr;
@@ -138,6 +140,17 @@ struct gdy_ctx {
   Table table;
   std::string err;
 };
+
+// Split-K planes of gdy_execute_static: a file-scope device array, so that
+// entry point allocates nothing.  Each device that loads the library holds
+// its own copy until the process ends.  In host code `scratch` names a
+// host-side stand-in, never the device array: kernels receive the address
+// hipGetSymbolAddress returns for the current device (kept per device in
+// g_scratch), never the symbol itself.
+static __device__ __align__(256) float scratch[GDY_STATIC_SCRATCH_BYTES / sizeof(float)];
+static const int kMaxDevices = 64;
+static float* g_scratch[kMaxDevices];
+static std::mutex g_scratch_mu;
 
 namespace {
 
@@ -1612,6 +1625,19 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
   }
   HIP_TRY(ctx, hipEventCreateWithFlags(&ctx->fork_ev, hipEventDisableTiming));
   HIP_TRY(ctx, hipMalloc((void**)&ctx->split_ws, kSplitWsBytes));
+  {
+    // the static split-K array of this device: its address, once per device,
+    // taken with the device current (hipSetDevice above)
+    if (device >= kMaxDevices) return fail(ctx, GDY_ERR_UNSUPPORTED, "device %d >= %d", device, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[device]) {
+      void* ptr = nullptr;
+      HIP_TRY(ctx, hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+      if (!ptr) return fail(ctx, GDY_ERR_HIP, "no address for the static split-K array");
+      g_scratch[device] = (float*)ptr;
+    }
+    ctx->scratch = g_scratch[device];
+  }
   open_table(ctx, table_path);
   return GDY_OK;
 }
@@ -1687,7 +1713,7 @@ gdy_status gdy_plan(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode
 }
 
 static gdy_status execute_impl(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode, int32_t forced_cd,
-                               void* hip_stream, gdy_plan_t* out) {
+                               void* hip_stream, gdy_plan_t* out, bool use_static) {
   if (!ctx) return GDY_ERR_INVALID_ARG;
   gdy_plan_t local;
   gdy_plan_t* p = out ? out : &local;
@@ -1695,7 +1721,16 @@ static gdy_status execute_impl(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, i
   if (s != GDY_OK) return s;
   if (ctx->device < 0) return fail(ctx, GDY_ERR_UNSUPPORTED, "host-only context cannot execute");
   float* ws = ctx->split_ws;
-  const int64_t cap = kSplitWsBytes;
+  int64_t cap = kSplitWsBytes;
+  if (use_static) {
+    const int64_t need = plan_ws_need(gemms, *p, mode);
+    if (need > (int64_t)GDY_STATIC_SCRATCH_BYTES)
+      return fail(ctx, GDY_ERR_UNSUPPORTED,
+                  "the plan needs %lld bytes of split-K scratch at once; the static array holds %lld",
+                  (long long)need, (long long)GDY_STATIC_SCRATCH_BYTES);
+    ws = ctx->scratch;
+    cap = GDY_STATIC_SCRATCH_BYTES;
+  }
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess || cur != ctx->device) HIP_TRY(ctx, hipSetDevice(ctx->device));
   try {
@@ -1707,7 +1742,12 @@ static gdy_status execute_impl(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, i
 
 gdy_status gdy_execute(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode, int32_t forced_cd,
                        void* hip_stream, gdy_plan_t* out) {
-  return execute_impl(ctx, gemms, n, mode, forced_cd, hip_stream, out);
+  return execute_impl(ctx, gemms, n, mode, forced_cd, hip_stream, out, false);
+}
+
+gdy_status gdy_execute_static(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode, int32_t forced_cd,
+                              void* hip_stream, gdy_plan_t* out) {
+  return execute_impl(ctx, gemms, n, mode, forced_cd, hip_stream, out, true);
 }
 
 gdy_status gdy_set_timing(gdy_ctx* ctx, int32_t enable) {

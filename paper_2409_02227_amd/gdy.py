@@ -35,7 +35,7 @@ RC_STREAMS, PARTITION_STREAMS = 1, 2
 STATUS = {0: "GDY_OK", 1: "GDY_ERR_INVALID_ARG", 2: "GDY_ERR_UNSUPPORTED", 3: "GDY_ERR_ALIAS",
           4: "GDY_ERR_TOO_MANY", 5: "GDY_ERR_TABLE", 6: "GDY_ERR_HIP", 7: "GDY_ERR_NOMEM"}
 
-EXPORTS = ("gdy_create", "gdy_destroy", "gdy_set_rc", "gdy_plan", "gdy_execute",
+EXPORTS = ("gdy_create", "gdy_destroy", "gdy_set_rc", "gdy_plan", "gdy_execute", "gdy_execute_static",
            "gdy_set_timing", "gdy_last_kernel_times", "gdy_kernel_times", "gdy_features",
            "gdy_variant_count",
            "gdy_variant_info", "gdy_variant_find", "gdy_isolated_variant",
@@ -114,6 +114,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "gdy_set_rc": (i32, [P, i32]),
         "gdy_plan": (i32, [P, ctypes.POINTER(GemmDesc), i32, i32, i32, ctypes.POINTER(Plan)]),
         "gdy_execute": (i32, [P, ctypes.POINTER(GemmDesc), i32, i32, i32, P, ctypes.POINTER(Plan)]),
+        "gdy_execute_static": (i32, [P, ctypes.POINTER(GemmDesc), i32, i32, i32, P, ctypes.POINTER(Plan)]),
         "gdy_set_timing": (i32, [P, i32]),
         "gdy_last_kernel_times": (i32, [P, ctypes.POINTER(ctypes.c_float),
                                         ctypes.POINTER(ctypes.c_float), i32]),
@@ -289,6 +290,16 @@ class Context:
         p = Plan()
         self._check(self.lib.gdy_execute(self.h, arr, len(gemms), _mode(mode), forced_cd,
                                          handle, ctypes.byref(p)))
+        return p.as_dict() if want_plan else None
+
+    def execute_static(self, gemms, mode="selector", forced_cd: int = 0, stream=None, want_plan=False):
+        """gdy_execute_static: as execute(), with the split-K planes in the
+        library's static device array (no allocation)."""
+        arr = descs(gemms)
+        handle = _stream_handle(stream)
+        p = Plan()
+        self._check(self.lib.gdy_execute_static(self.h, arr, len(gemms), _mode(mode), forced_cd,
+                                                handle, ctypes.byref(p)))
         return p.as_dict() if want_plan else None
 
     def execute_descs(self, arr, n, mode, forced_cd, handle):
