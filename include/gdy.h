@@ -305,6 +305,24 @@ gdy_status gdy_last_kernel_times(gdy_ctx* ctx, float* start_ms, float* end_ms, i
 gdy_status gdy_kernel_times(gdy_ctx* ctx, int32_t back, float* start_ms, float* end_ms,
                             int32_t n);
 
+/*
+ * Dispatch map (host only; works on host-only contexts): plans the
+ * submission as gdy_plan does, builds launch block `dispatch` of the plan
+ * as gdy_execute would, and reports what each of its workgroups computes,
+ * with the kernels' own mapping code.  *grid receives the dispatch's
+ * workgroup count; for workgroup b < min(*grid, max_workgroups),
+ * gemm_of_wg[b] is the submission index of the member it serves (-1: an
+ * idle workgroup) and it runs that member's work items first_item[b],
+ * first_item[b] + item_stride[b], ... below the member's item count.
+ * items_of_gemm (n entries) receives each member's work items in this
+ * dispatch (tiles x batch items x split runs; 0 for GEMMs of other
+ * dispatches).  Lets a caller check on the CPU that every work item of a
+ * dispatch is computed exactly once (XCD placement included).
+ */
+gdy_status gdy_dispatch_map(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode, int32_t forced_cd,
+                            int32_t dispatch, int32_t max_workgroups, int32_t* grid, int32_t* gemm_of_wg,
+                            int32_t* first_item, int32_t* item_stride, int64_t* items_of_gemm);
+
 /* Features of one GEMM (Sec. 4.3): M, N, K, then for each CD class
  * 1, 2, 4, 8, 16 the bound variant's #WGs, occupancy and #waves. */
 gdy_status gdy_features(gdy_ctx* ctx, const gdy_gemm* gemm, double* out_features);

@@ -131,6 +131,7 @@ struct gdy_ctx {
   std::vector<std::vector<hipEvent_t>> part_done;
   float* split_ws = nullptr;  // split-K partial planes (kSplitWsBytes)
   float* scratch = nullptr;   // this device's static split-K array (gdy_execute_static)
+  bool xcd_place = true;      // XCD placement of fused dispatches (GDY_XCD_PLACEMENT=0: off)
   int host_slots = 0;                              // host-only context: planned stream slots
   std::vector<hipEvent_t> done;                    // one per stream slot
   hipEvent_t fork_ev = nullptr;
@@ -1131,6 +1132,9 @@ hipStream_t slot_stream(const gdy_ctx* ctx, int slot) {
   return ctx->pool[slot];
 }
 
+bool place_xcds(const gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, const std::vector<int>& members,
+                KLaunch* L, int* grid);
+
 // Workgroup ranges of one dispatch: each GEMM gets its own grid (tiles, or
 // its cap x occupancy), every range but the last rounded up to a multiple
 // of 8 so each GEMM starts on XCD 0 (the extra workgroups find no tile).
@@ -1168,7 +1172,107 @@ gdy_status build_launch(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p,
   if (wg > INT32_MAX) return fail(ctx, GDY_ERR_UNSUPPORTED, "dispatch grid of %lld workgroups", (long long)wg);
   L->first[L->count] = (int32_t)wg;
   *grid = (int)wg;
+  if (!*split) place_xcds(ctx, g, p, members, L, grid);
   return GDY_OK;
+}
+
+// XCD placement of a fused GEMM dispatch (KLaunch): the hardware deals
+// workgroup b to XCD b % 8, and each XCD's L2 fetches whatever its
+// workgroups read.  Spread over all eight, every member's A is fetched eight
+// times.  Instead, the members' work items are laid out per K length (one
+// line per distinct number of K tiles, longest first) and each line is cut
+// into eight contiguous pieces, one per XCD, whose lengths even out the XCDs'
+// total work (tiles x (K tiles + 1, the store)); cuts keep a tile column's
+// rows together (multiples of min(tile rows, 8) within a member, the rows
+// the tile order groups), so a B panel stays on one XCD.  Each XCD then
+// holds the same mix of long and short tiles as before -- its CUs pack them
+// as well -- from a few members instead of all.  Only GEMM members that
+// neither split nor cap their grid are placed; anything else keeps ranges.
+bool place_xcds(const gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, const std::vector<int>& members,
+                KLaunch* L, int* grid) {
+  const int U = L->count;
+  if (U < 2 || !ctx->xcd_place) return false;
+  std::vector<int64_t> tiles(U), nk(U), unit(U);
+  for (int u = 0; u < U; ++u) {
+    const int i = members[u];
+    const Variant& v = ctx->variants[p.variant_of[i]];
+    const KernelDesc* d = ctx->kernels[v.kernel].d;
+    if (g[i].op != GDY_OP_GEMM || d->ew || p.split_of[i] > 1 || v.cap > 0) return false;
+    tiles[u] = (int64_t)L->g[u].tiles_m * L->g[u].tiles_n * std::max(L->g[u].batch, 1);
+    if (tiles[u] <= 0 || tiles[u] >= (1LL << 29)) return false;
+    nk[u] = (g[i].k + d->bk - 1) / d->bk;
+    unit[u] = std::min<int64_t>(L->g[u].tiles_m, L->g[u].group_m);
+  }
+  std::vector<int64_t> ks(nk.begin(), nk.end());
+  std::sort(ks.begin(), ks.end(), [](int64_t a, int64_t b) { return a > b; });
+  ks.erase(std::unique(ks.begin(), ks.end()), ks.end());
+  double cost_x[kXcds] = {};
+  double cum = 0.0;
+  struct Piece { int u; int64_t tile0, len; };
+  std::vector<std::vector<Piece>> per(kXcds);
+  int n_pieces = 0;
+  for (int64_t kc : ks) {
+    std::vector<int> mem;
+    std::vector<int64_t> start;
+    int64_t n = 0;
+    for (int u = 0; u < U; ++u)
+      if (nk[u] == kc) {
+        mem.push_back(u);
+        start.push_back(n);
+        n += tiles[u];
+      }
+    const double w = (double)(kc + 1);
+    cum += (double)n * w;
+    // each XCD's share of this line evens out the work so far
+    double want[kXcds], sum = 0.0;
+    for (int x = 0; x < kXcds; ++x) {
+      want[x] = std::max(0.0, (cum / kXcds - cost_x[x]) / w);
+      sum += want[x];
+    }
+    int64_t cut[kXcds + 1];
+    cut[0] = 0;
+    cut[kXcds] = n;
+    double acc = 0.0;
+    for (int x = 1; x < kXcds; ++x) {
+      acc += want[x - 1];
+      int64_t c = sum > 0 ? (int64_t)std::llround(acc / sum * (double)n) : n * x / kXcds;
+      size_t m = 0;  // align the cut to the unit of the member it falls in
+      while (m + 1 < mem.size() && c >= start[m + 1]) ++m;
+      const int64_t un = std::max<int64_t>(unit[mem[m]], 1);
+      c = start[m] + (c - start[m] + un / 2) / un * un;
+      c = std::min(std::max(c, cut[x - 1]), std::min(n, start[m] + tiles[mem[m]]));
+      cut[x] = c;
+    }
+    for (int x = 0; x < kXcds; ++x) {
+      cost_x[x] += (double)(cut[x + 1] - cut[x]) * w;
+      for (size_t m = 0; m < mem.size(); ++m) {
+        const int64_t lo = std::max(cut[x], start[m]), hi = std::min(cut[x + 1], start[m] + tiles[mem[m]]);
+        if (lo >= hi) continue;
+        per[x].push_back(Piece{mem[m], lo - start[m], hi - lo});
+        if (++n_pieces > kMaxPieces) return false;
+      }
+    }
+  }
+  int64_t slots = 0;
+  int q = 0;
+  for (int x = 0; x < kXcds; ++x) {
+    L->xcd_first[x] = q;
+    int64_t end = 0;
+    for (const Piece& pc : per[x]) {
+      end += pc.len;
+      L->piece_end[q] = (int32_t)end;
+      L->piece_tile[q] = (int32_t)pc.tile0;
+      L->piece_gemm[q] = (int8_t)pc.u;
+      ++q;
+    }
+    slots = std::max(slots, end);
+  }
+  L->xcd_first[kXcds] = q;
+  if (slots * kXcds > INT32_MAX) return false;
+  for (int u = 0; u < U; ++u) L->g[u].xcd_remap = 0;  // pieces index the plain tile order
+  L->placed = 1;
+  *grid = (int)(slots * kXcds);
+  return true;
 }
 
 // Launch block of the split-K reduction for the split members of one GEMM
@@ -1193,6 +1297,35 @@ void build_reduce(const gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, co
   (void)p;
 }
 
+// Split-K workspace offsets per GEMM (-1: unsplit): consecutive regions per
+// group in launch order (the groups run one after another and reuse the
+// workspace; in SEQUENTIAL each GEMM runs alone on the origin stream and
+// starts at offset 0), as plan_ws_need counts.
+std::vector<int64_t> ws_offsets(const gdy_gemm* g, const gdy_plan_t& p, int mode) {
+  std::vector<int64_t> ws_off(std::max(p.n, 1), -1);
+  int64_t ws = 0;
+  int cur = -1;
+  for (int t = 0; t < GDY_MAX_GEMMS && p.order[t] >= 0; ++t) {
+    const int i = p.order[t];
+    if (p.group_of[i] != cur || mode == GDY_SEQUENTIAL) {
+      cur = p.group_of[i];
+      ws = 0;
+    }
+    if (p.split_of[i] <= 1) continue;
+    ws_off[i] = ws;
+    ws += split_ws_bytes(g[i], p.split_of[i]);
+  }
+  return ws_off;
+}
+
+// Members of dispatch d in launch order.
+std::vector<int> dispatch_members(const gdy_plan_t& p, int d) {
+  std::vector<int> out;
+  for (int t = 0; t < GDY_MAX_GEMMS && p.order[t] >= 0; ++t)
+    if (p.dispatch_of[p.order[t]] == d) out.push_back(p.order[t]);
+  return out;
+}
+
 gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, int mode,
                        hipStream_t origin, float* ws_base, int64_t ws_cap) {
   gdy_status st = GDY_OK;
@@ -1205,24 +1338,7 @@ gdy_status launch_plan(gdy_ctx* ctx, const gdy_gemm* g, const gdy_plan_t& p, int
     return fail(ctx, GDY_ERR_UNSUPPORTED, "no CU partitions: create the context with use_cu_masks & 2");
   auto stream_at = [&](int s) { return parted ? ctx->parts[pr][s] : slot_stream(ctx, s); };
   auto done_at = [&](int s) { return parted ? ctx->part_done[pr][s] : ctx->done[s]; };
-  // split-K workspace: consecutive regions per group in launch order (the
-  // groups run one after another and reuse it; in SEQUENTIAL each GEMM runs
-  // alone on the origin stream and starts at offset 0), as plan_ws_need counts
-  std::vector<int64_t> ws_off(n > 0 ? n : 1, -1);
-  {
-    int64_t ws = 0;
-    int cur = -1;
-    for (int t = 0; t < GDY_MAX_GEMMS && p.order[t] >= 0; ++t) {
-      const int i = p.order[t];
-      if (p.group_of[i] != cur || mode == GDY_SEQUENTIAL) {
-        cur = p.group_of[i];
-        ws = 0;
-      }
-      if (p.split_of[i] <= 1) continue;
-      ws_off[i] = ws;
-      ws += split_ws_bytes(g[i], p.split_of[i]);
-    }
-  }
+  const std::vector<int64_t> ws_off = ws_offsets(g, p, mode);
   int L = 0;
   while (L < GDY_MAX_GEMMS && p.order[L] >= 0) ++L;
   const int D = p.n_dispatches;
@@ -1492,6 +1608,7 @@ static gdy_status create_impl(gdy_ctx* ctx, int device, const char* table_path, 
                               int32_t use_cu_masks) {
   const bool host_only = device < 0;
   ctx->device = device;
+  if (const char* env = std::getenv("GDY_XCD_PLACEMENT")) ctx->xcd_place = std::atoi(env) != 0;
   if (host_only) {
     const char* env = std::getenv("GDY_HOST_CUS");
     ctx->cus = env ? std::atoi(env) : 256;
@@ -1748,6 +1865,42 @@ gdy_status gdy_execute(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t m
 gdy_status gdy_execute_static(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode, int32_t forced_cd,
                               void* hip_stream, gdy_plan_t* out) {
   return execute_impl(ctx, gemms, n, mode, forced_cd, hip_stream, out, true);
+}
+
+gdy_status gdy_dispatch_map(gdy_ctx* ctx, const gdy_gemm* gemms, int32_t n, int32_t mode, int32_t forced_cd,
+                            int32_t dispatch, int32_t max_workgroups, int32_t* grid, int32_t* gemm_of_wg,
+                            int32_t* first_item, int32_t* item_stride, int64_t* items_of_gemm) {
+  if (!ctx || !grid || (max_workgroups > 0 && (!gemm_of_wg || !first_item || !item_stride)) || !items_of_gemm)
+    return GDY_ERR_INVALID_ARG;
+  gdy_plan_t p;
+  gdy_status s = gdy_plan(ctx, gemms, n, mode, forced_cd, &p);
+  if (s != GDY_OK) return s;
+  if (dispatch < 0 || dispatch >= p.n_dispatches) return fail(ctx, GDY_ERR_INVALID_ARG, "no dispatch %d", dispatch);
+  try {
+    const std::vector<int> members = dispatch_members(p, dispatch);
+    const std::vector<int64_t> ws_off = ws_offsets(gemms, p, mode);
+    KLaunch L;
+    int g = 0;
+    bool split = false;
+    // the planes' base is never dereferenced here
+    s = build_launch(ctx, gemms, p, members, ws_off, reinterpret_cast<float*>(256), kSplitWsBytes, &L, &g, &split);
+    if (s != GDY_OK) return s;
+    *grid = g;
+    for (int i = 0; i < n; ++i) items_of_gemm[i] = 0;
+    for (int u = 0; u < L.count; ++u)
+      items_of_gemm[members[u]] = (int64_t)L.g[u].tiles_m * L.g[u].tiles_n * std::max(L.g[u].batch, 1) *
+                                  std::max(L.g[u].split, 1);
+    for (int b = 0; b < std::min(g, max_workgroups); ++b) {
+      int gi = -1, lwg = 0, nwg = 0;
+      locate(L, b, gi, lwg, nwg);
+      gemm_of_wg[b] = gi < 0 ? -1 : members[gi];
+      first_item[b] = gi < 0 ? 0 : lwg;
+      item_stride[b] = gi < 0 ? 0 : nwg;
+    }
+  } catch (...) {
+    return fail(ctx, GDY_ERR_NOMEM, "host allocation failed");
+  }
+  return GDY_OK;
 }
 
 gdy_status gdy_set_timing(gdy_ctx* ctx, int32_t enable) {

@@ -1,6 +1,7 @@
 // gdy_internal.h -- structures shared by the GO-Kernel instantiation units
 // and the host runtime of libgdy (not part of the public C-ABI).
 #pragma once
+#include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace gdy {
@@ -45,12 +46,63 @@ struct KArgs {
 // exactly the same code (and gives the same bits) whether the GEMM runs
 // alone or fused with others.  first[i] is a multiple of 8 for i > 0 so a
 // GEMM's local workgroup index keeps the hardware's XCD round-robin phase.
+//
+// XCD placement (placed != 0; GEMM members that neither split nor cap their
+// grid): the hardware deals workgroup b to XCD b % 8, so b runs as slot
+// b / 8 of XCD x = b % 8.  The slots of XCD x walk its pieces
+// [xcd_first[x], xcd_first[x+1]): piece q covers that XCD's slots up to
+// piece_end[q] (exclusive, counted from the XCD's first slot) with the
+// consecutive work items piece_tile[q], piece_tile[q] + 1, ... of member
+// piece_gemm[q].  Slots past the XCD's last piece are idle.  The host gives
+// each XCD an even share of the dispatch's work built from few members, so
+// each member's A is fetched by few XCDs' L2s.  A work item is computed by
+// the same code wherever it runs: the bits do not change.
 constexpr int kMaxFused = 16;
+constexpr int kXcds = 8;
+constexpr int kMaxPieces = 48;
 struct KLaunch {
   int32_t count;                  // GEMMs in this dispatch, 1..kMaxFused
   int32_t first[kMaxFused + 1];   // workgroup ranges; first[count] = grid size
   KArgs g[kMaxFused];
+  int32_t placed;                 // 1: the piece table below maps workgroups to work
+  int32_t xcd_first[kXcds + 1];
+  int32_t piece_end[kMaxPieces];
+  int32_t piece_tile[kMaxPieces];
+  int8_t piece_gemm[kMaxPieces];
 };
+
+// The member of a range dispatch that owns workgroup b (uniform per
+// workgroup: a short scalar scan of the workgroup ranges).
+__host__ __device__ inline int owner_of(const KLaunch& L, int b) {
+  int i = 0;
+  while (i + 1 < L.count && b >= L.first[i + 1]) ++i;
+  return i;
+}
+
+// Workgroup b's member gi, its first work item lwg and its stride nwg (work
+// items lwg, lwg + nwg, ... of that member).  Range dispatches: the member's
+// workgroup range.  Placed dispatches: one work item from the XCD's piece
+// table (nwg past any item count), or gi = -1 for an idle slot.  The kernels
+// and the host's dispatch map (gdy_dispatch_map) run this same code.
+__host__ __device__ inline void locate(const KLaunch& L, int b, int& gi, int& lwg, int& nwg) {
+  if (L.placed) {
+    const int x = b & (kXcds - 1), j = b / kXcds;
+    const int q0 = L.xcd_first[x], q1 = L.xcd_first[x + 1];
+    int q = q0;
+    while (q < q1 && j >= L.piece_end[q]) ++q;
+    if (q == q1) {
+      gi = -1;
+      return;
+    }
+    gi = L.piece_gemm[q];
+    lwg = L.piece_tile[q] + j - (q == q0 ? 0 : L.piece_end[q - 1]);
+    nwg = 1 << 30;
+    return;
+  }
+  gi = owner_of(L, b);
+  lwg = b - L.first[gi];
+  nwg = L.first[gi + 1] - L.first[gi];
+}
 
 // Compile-time description of one instantiated kernel.
 struct KernelDesc {

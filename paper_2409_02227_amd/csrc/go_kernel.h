@@ -384,13 +384,10 @@ __device__ __forceinline__ void tile_coords(int t, const KArgs& p, int& tm, int&
   tn = in_group / rows_here;
 }
 
-// The GEMM of a fused dispatch that owns this workgroup (uniform per
-// workgroup: a short scalar scan of the workgroup ranges).
-__device__ __forceinline__ int owner_of(const KLaunch& L) {
-  const int b = (int)blockIdx.x;
-  int i = 0;
-  while (i + 1 < L.count && b >= L.first[i + 1]) ++i;
-  return i;
+// owner_of / locate (gdy_internal.h) with this workgroup's index.
+__device__ __forceinline__ int owner_of(const KLaunch& L) { return owner_of(L, (int)blockIdx.x); }
+__device__ __forceinline__ void locate(const KLaunch& L, int& gi, int& lwg, int& nwg) {
+  locate(L, (int)blockIdx.x, gi, lwg, nwg);
 }
 
 // ---------------------------------------------------------------------------
@@ -620,12 +617,12 @@ go_gemm(KLaunch L) {
 
   __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
 
-  const int gi = owner_of(L);
+  int gi, lwg, nwg;
+  locate(L, gi, lwg, nwg);
+  if (gi < 0) return;  // an idle slot of a placed dispatch
   const KArgs& p = L.g[gi];
-  const int wg0 = L.first[gi];
-  const int nwg = L.first[gi + 1] - wg0;
   if (p.ew) {  // an element-wise add fused into this dispatch
-    ew_member<C::NT>(p, (int)blockIdx.x - wg0, nwg);
+    ew_member<C::NT>(p, lwg, nwg);
     return;
   }
 
@@ -648,7 +645,7 @@ go_gemm(KLaunch L) {
   // twin, each in `split` K runs (split innermost)
   const int nsplit = SPLIT ? p.split : 1;
   const int total = ntiles * p.batch * nsplit;
-  for (int tb = (int)blockIdx.x - wg0; tb < total; tb += nwg) {
+  for (int tb = lwg; tb < total; tb += nwg) {
     const int s_run = SPLIT ? tb % nsplit : 0;
     const int tile_all = SPLIT ? tb / nsplit : tb;  // item * ntiles + tile
     const int item = tile_all / ntiles;

@@ -273,12 +273,12 @@ go_gemm_d(KLaunch L) {
   __shared__ __attribute__((aligned(1024))) uint8_t smem_raw[C::LDS];
   lds_u8* smem = (lds_u8*)smem_raw;
 
-  const int gi = owner_of(L);
+  int gi, lwg, nwg;
+  locate(L, gi, lwg, nwg);
+  if (gi < 0) return;  // an idle slot of a placed dispatch
   const KArgs& p = L.g[gi];
-  const int wg0 = L.first[gi];
-  const int nwg = L.first[gi + 1] - wg0;
   if (p.ew) {  // an element-wise add fused into this dispatch
-    ew_member<C::NT>(p, (int)blockIdx.x - wg0, nwg);
+    ew_member<C::NT>(p, lwg, nwg);
     return;
   }
 
@@ -318,7 +318,7 @@ go_gemm_d(KLaunch L) {
   // twin, each in `split` K runs (split innermost)
   const int nsplit = SPLIT ? p.split : 1;
   const int total = ntiles * p.batch * nsplit;
-  for (int tb = (int)blockIdx.x - wg0; tb < total; tb += nwg) {
+  for (int tb = lwg; tb < total; tb += nwg) {
     const int s_run = SPLIT ? tb % nsplit : 0;
     const int tile_all = SPLIT ? tb / nsplit : tb;  // item * ntiles + tile
     const int item = tile_all / ntiles;

@@ -36,7 +36,7 @@ STATUS = {0: "GDY_OK", 1: "GDY_ERR_INVALID_ARG", 2: "GDY_ERR_UNSUPPORTED", 3: "G
           4: "GDY_ERR_TOO_MANY", 5: "GDY_ERR_TABLE", 6: "GDY_ERR_HIP", 7: "GDY_ERR_NOMEM"}
 
 EXPORTS = ("gdy_create", "gdy_destroy", "gdy_set_rc", "gdy_plan", "gdy_execute", "gdy_execute_static",
-           "gdy_set_timing", "gdy_last_kernel_times", "gdy_kernel_times", "gdy_features",
+           "gdy_set_timing", "gdy_last_kernel_times", "gdy_kernel_times", "gdy_features", "gdy_dispatch_map",
            "gdy_variant_count",
            "gdy_variant_info", "gdy_variant_find", "gdy_isolated_variant",
            "gdy_catalogue_hash", "gdy_device_cus", "gdy_status_string", "gdy_last_error")
@@ -121,6 +121,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "gdy_kernel_times": (i32, [P, i32, ctypes.POINTER(ctypes.c_float),
                                    ctypes.POINTER(ctypes.c_float), i32]),
         "gdy_features": (i32, [P, ctypes.POINTER(GemmDesc), ctypes.POINTER(ctypes.c_double)]),
+        "gdy_dispatch_map": (i32, [P, ctypes.POINTER(GemmDesc), i32, i32, i32, i32, i32, ctypes.POINTER(i32),
+                                   ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32),
+                                   ctypes.POINTER(i64)]),
         "gdy_variant_count": (i32, [P]),
         "gdy_variant_info": (i32, [P, i32, ctypes.POINTER(VariantDesc)]),
         "gdy_variant_find": (i32, [P, ctypes.c_char_p]),
@@ -319,6 +322,24 @@ class Context:
         e = (ctypes.c_float * max(n, 1))()
         self._check(self.lib.gdy_kernel_times(self.h, back, s, e, n))
         return list(s[:n]), list(e[:n])
+
+    def dispatch_map(self, gemms, mode="selector", forced_cd: int = 0, dispatch: int = 0,
+                     max_workgroups: int = 1 << 20) -> dict:
+        """gdy_dispatch_map: per workgroup of one dispatch, the member it serves
+        (-1: idle), its first work item and stride; per GEMM its item count."""
+        arr = descs(gemms)
+        n = len(gemms)
+        grid = ctypes.c_int32()
+        cap = max_workgroups
+        gw = (ctypes.c_int32 * cap)()
+        fi = (ctypes.c_int32 * cap)()
+        st = (ctypes.c_int32 * cap)()
+        items = (ctypes.c_int64 * max(n, 1))()
+        self._check(self.lib.gdy_dispatch_map(self.h, arr, n, _mode(mode), forced_cd, dispatch, cap,
+                                              ctypes.byref(grid), gw, fi, st, items))
+        g = min(grid.value, cap)
+        return {"grid": grid.value, "gemm": list(gw[:g]), "first": list(fi[:g]), "stride": list(st[:g]),
+                "items": list(items[:n])}
 
     def features(self, gemm) -> list:
         d = gemm if isinstance(gemm, GemmDesc) else gemm.desc()
