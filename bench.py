@@ -347,12 +347,8 @@ def het_compare(table, count, steps, torch):
     each timed in sequential, selector (GOLDYLOC) and GO mode and at its best
     CD (Sec. 5.5 'Oracle').  Returns per-submission flops, times and CDs."""
     from paper_2409_02227_amd import gdy, inputs
-    subs = inputs.config4(count=count)
-    a_elems, b_elems = 600 << 20, 1200 << 20          # 1.2 GB and 2.4 GB of bf16
-    placed = inputs.pool_specs(subs, a_elems, b_elems, seed=4)
-    gen = torch.Generator(device="cuda").manual_seed(44)
-    a_pool = (torch.rand(a_elems, device="cuda", generator=gen) * 2 - 1).to(torch.bfloat16)
-    b_pool = (torch.randn(b_elems, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+    placed = inputs.het_placed(count)
+    a_pool, b_pool = inputs.het_pools(torch)
     ctx = gdy.Context(0, table=table, max_streams=16)
     handle = gdy._stream_handle(None)
     res = {"flops": [], "gemms": [], "sequential": [], "selector": [], "go": [], "best_cd": [], "best_cd_of": [],

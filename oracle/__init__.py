@@ -41,12 +41,27 @@ def build(force: bool = True) -> str:
     return _LIB
 
 
+def build_sanitized() -> str:
+    """liboracle_san.so: the oracle built with clang's AddressSanitizer and
+    UndefinedBehaviorSanitizer (load with ORACLE_LIBRARY=<path> in a process
+    whose LD_PRELOAD starts with clang's ASan runtime)."""
+    out = os.path.join(_HERE, "liboracle_san.so")
+    clang = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "llvm", "bin", "clang")
+    llvm_lib = os.path.join(os.path.dirname(os.path.dirname(clang)), "lib")
+    cmd = [clang, "-O1", "-g", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-fno-omit-frame-pointer",
+           "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-Wall", "-Wextra",
+           "-o", out, _SRC, "-lm", f"-L{llvm_lib}", f"-Wl,-rpath,{llvm_lib}"]
+    subprocess.run(cmd, check=True)
+    return out
+
+
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        path = os.environ.get("ORACLE_LIBRARY") or _LIB
+        if path == _LIB and (not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC)):
             build(force=True)
-        lib = ctypes.CDLL(_LIB)
+        lib = ctypes.CDLL(path)
         i64, i32, dbl, vp = ctypes.c_int64, ctypes.c_int, ctypes.c_double, ctypes.c_void_p
         lib.orc_decode.argtypes = [i32, vp, i64, vp]
         lib.orc_decode.restype = i32

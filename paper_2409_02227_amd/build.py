@@ -59,5 +59,36 @@ def build(jobs: int | None = None) -> str:
     return LIB
 
 
+def build_sanitized() -> str:
+    """_build_san/libgdy_san.so: the host runtime (planner, launcher, C-ABI)
+    built with clang's AddressSanitizer and UndefinedBehaviorSanitizer on the
+    host side only, linked with the kernel objects of the last build().  Load
+    it with GDY_LIBRARY=<path> in a process whose LD_PRELOAD starts with the
+    ASan runtime (the runtime resolves the sanitizer calls)."""
+    san = os.path.join(HERE, "_build_san")
+    os.makedirs(san, exist_ok=True)
+    obj = os.path.join(san, "gdy.o")
+    host_san = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer"]
+    flags = [f for f in FLAGS if f != "-O3"] + ["-O1", "-g"]
+    cmd = [_hipcc(), "-x", "hip", *flags, *host_san, "-c", os.path.join(CSRC, "gdy.cpp"), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for the sanitizer build:\n{r.stderr}")
+    objs = [os.path.join(BUILD, os.path.splitext(x)[0] + ".o") for x in SOURCES if x != "gdy.cpp"]
+    missing = [o for o in objs if not os.path.exists(o)]
+    if missing:
+        raise RuntimeError(f"run build() first: missing {missing}")
+    lib = os.path.join(san, "libgdy_san.so")
+    r = subprocess.run([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", lib, obj, *objs],
+                       capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed:\n{r.stderr}")
+    return lib
+
+
 if __name__ == "__main__":
-    print(build())
+    if "--sanitize" in sys.argv:
+        print(build_sanitized())
+    else:
+        print(build())

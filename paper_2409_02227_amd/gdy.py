@@ -99,11 +99,13 @@ class GdyError(RuntimeError):
 _lib = None
 
 
-def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Load libgdy.so (raises if it is missing: no fallback exists)."""
+def load_library(path: str = None) -> ctypes.CDLL:
+    """Load libgdy.so (raises if it is missing: no fallback exists).
+    GDY_LIBRARY names another build of it (the sanitizer build)."""
     global _lib
     if _lib is not None:
         return _lib
+    path = path or os.environ.get("GDY_LIBRARY") or LIB_PATH
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with paper_2409_02227_amd.build.build()")
     lib = ctypes.CDLL(path)

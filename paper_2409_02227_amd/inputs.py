@@ -336,6 +336,25 @@ def materialize(spec: GemmSpec, device="cuda", keep_host=True) -> Materialized:
     return Materialized(spec, a, b, c, cfull, sa, sb, host)
 
 
+HET_A_ELEMS, HET_B_ELEMS = 600 << 20, 1200 << 20  # 1.2 GB and 2.4 GB of bf16
+
+
+def het_pools(torch, device="cuda"):
+    """The heterogeneous submissions' device operand pools, bf16: A ~ U[-1, 1]
+    (activations) and B ~ N(0, 0.02) (weights), from a seeded device
+    generator; each GEMM reads a window of each (pool_specs)."""
+    gen = torch.Generator(device=device).manual_seed(44)
+    a = (torch.rand(HET_A_ELEMS, device=device, generator=gen) * 2 - 1).to(torch.bfloat16)
+    b = (torch.randn(HET_B_ELEMS, device=device, generator=gen) * 0.02).to(torch.bfloat16)
+    return a, b
+
+
+def het_placed(count: int = 200) -> list:
+    """The first `count` heterogeneous submissions with their pool windows:
+    per submission a list of (GemmSpec, A offset, B offset) in elements."""
+    return pool_specs(config4(count=count), HET_A_ELEMS, HET_B_ELEMS, seed=4)
+
+
 def pool_specs(subs: list, a_pool_elems: int, b_pool_elems: int, seed: int) -> list:
     """Assign each GEMM of each submission a window (element offset) in the
     A and B pools: consecutive GEMMs of a submission take disjoint windows

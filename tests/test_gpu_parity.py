@@ -139,29 +139,12 @@ def test_config1_and_config2_full(ctx, mode):
             check(m, label=mode)
 
 
-def test_config3_sampled(ctx):
-    mats = [inputs.materialize(s) for s in inputs.config3()]
-    for mode in ("sequential", "selector"):
-        _run(ctx, mats, mode)
-        for m in mats:
-            check(m, samples=6, label=mode)
-
-
 def test_config5_fp8_sampled(ctx):
     mats = [inputs.materialize(s) for s in inputs.config5()]
     for mode in ("sequential", "default"):
         _run(ctx, mats, mode)
         for m in mats:
             check(m, samples=4, label=mode)
-
-
-def test_config4_first_submissions_sampled(ctx):
-    subs = inputs.config4(count=3)
-    for sub in subs:
-        mats = [inputs.materialize(s) for s in sub]
-        _run(ctx, mats, "selector")
-        for m in mats:
-            check(m, samples=3, label="selector")
 
 
 def test_validation_errors(ctx):
