@@ -53,13 +53,16 @@ def parse_table(path: str) -> dict:
     t = {"entries": [], "lr": None, "lr_by_type": {}}
     blocks = {0: {}}
     cur = 0
+    version = 1
     with open(path) as f:
         for raw in f:
             line = raw.strip()
             if not line or line.startswith("#"):
                 continue
             tok = line.split()
-            if tok[0] == "device":
+            if tok[0] == "gdy-go-table":
+                version = int(tok[1])
+            elif tok[0] == "device":
                 t["arch"], t["cus"] = tok[1], int(tok[3])
             elif tok[0] == "catalogue":
                 t["catalogue"] = int(tok[1], 16)
@@ -72,11 +75,13 @@ def parse_table(path: str) -> dict:
                 blocks[cur]["lr_w"] = np.array([float(x) for x in tok[1:]]).reshape(
                     N_FEATURES, len(CD_CLASSES))
             elif tok[0] == "entry":
+                # version 2 adds the tuned batch items after K
+                items, rest = (int(tok[7]), tok[8:]) if version >= 2 else (1, tok[7:])
                 t["entries"].append({"dtype": int(tok[1]), "ta": int(tok[2]), "tb": int(tok[3]),
                                      "mlog": int(tok[4]), "n": int(tok[5]), "k": int(tok[6]),
-                                     "variants": tok[7:12],
+                                     "items": items, "variants": rest[:5],
                                      # best kernels under 128, 64, 32 CUs (CU partitions)
-                                     "partition": tok[12:15] if len(tok) >= 15 else None})
+                                     "partition": rest[5:8] if len(rest) >= 8 else None})
     for d, lr in blocks.items():
         if len(lr) == 4:
             model = {"xmin": lr["lr_min"], "xmax": lr["lr_max"], "w": lr["lr_w"], "b": lr["lr_b"]}
@@ -94,11 +99,13 @@ def predictor_for(table: dict, dtype: int):
 
 def tuned_entry(table: dict, g: dict):
     """The table's entry for g's own shape (dtype, layout, ceil(log2 M), N,
-    K) or None: the oracle only speaks for shapes the table tuned."""
+    K, batch items) or None: the oracle only speaks for shapes the table
+    tuned."""
     mlog = max(0, math.ceil(math.log2(max(g["m"], 1))))
+    items = max(g.get("batch", 0), 1)
     for e in table["entries"]:
-        if (e["dtype"], e["ta"], e["tb"], e["mlog"], e["n"], e["k"]) == (
-                g["a_type"], g["trans_a"], g["trans_b"], mlog, g["n"], g["k"]):
+        if (e["dtype"], e["ta"], e["tb"], e["mlog"], e["n"], e["k"], e["items"]) == (
+                g["a_type"], g["trans_a"], g["trans_b"], mlog, g["n"], g["k"], items):
             return e
     return None
 

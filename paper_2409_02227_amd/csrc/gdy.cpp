@@ -60,6 +60,8 @@ struct TableEntry {
   int dtype, ta, tb, mlog;
   int64_t n, k;
   double ln, lk;  // log2(n), log2(k)
+  int64_t items = 1;  // batch items of the tuned shape (a B-GEMM's count; 1: a single GEMM)
+  double li = 0.0;    // log2(items)
   int v[GDY_N_CD];
   int rc[3] = {-1, -1, -1};  // best kernel tuned under kRcBudgets[r] CUs (-1: not in the table)
 };
@@ -250,11 +252,13 @@ int nearest_entry(const gdy_ctx* ctx, const gdy_gemm& g) {
   const int mlog = ceil_log2(std::max<int64_t>(g.m, 1));
   const double ln = std::log2((double)std::max<int64_t>(g.n, 1));
   const double lk = std::log2((double)std::max<int64_t>(g.k, 1));
+  const double li = std::log2((double)std::max(g.batch, 1));
   int best = -1;
   double best_d = 0;
   for (int i : t.by_layout[g.a_type][g.trans_a & 1][g.trans_b & 1]) {
     const TableEntry& e = t.entries[i];
-    const double d = std::fabs((double)(e.mlog - mlog)) + std::fabs(e.ln - ln) + std::fabs(e.lk - lk);
+    const double d = std::fabs((double)(e.mlog - mlog)) + std::fabs(e.ln - ln) + std::fabs(e.lk - lk) +
+                     std::fabs(e.li - li);
     if (best < 0 || d < best_d) {
       best = i;
       best_d = d;
@@ -1439,14 +1443,14 @@ gdy_status load_table(gdy_ctx* ctx, const char* path) {
   int cur = 0;
   int have[5][4] = {};  // min, max, w, b seen per block
   bool header = false;
+  int version = 0;
   while (std::getline(f, line)) {
     if (line.empty() || line[0] == '#') continue;
     std::istringstream in(line);
     in >> tag;
     if (tag == "gdy-go-table") {
-      int ver = 0;
-      in >> ver;
-      if (ver != 1) return fail(ctx, GDY_ERR_TABLE, "GO table version %d unsupported", ver);
+      in >> version;
+      if (version != 1 && version != 2) return fail(ctx, GDY_ERR_TABLE, "GO table version %d unsupported", version);
       header = true;
     } else if (tag == "device") {
       std::string arch, cus_tag;
@@ -1483,7 +1487,9 @@ gdy_status load_table(gdy_ctx* ctx, const char* path) {
     } else if (tag == "entry") {
       TableEntry e;
       in >> e.dtype >> e.ta >> e.tb >> e.mlog >> e.n >> e.k;
-      if (!in || e.n <= 0 || e.k <= 0) return fail(ctx, GDY_ERR_TABLE, "bad entry line: %s", line.c_str());
+      if (version >= 2) in >> e.items;  // version 2 entries name the tuned batch items
+      if (!in || e.n <= 0 || e.k <= 0 || e.items <= 0)
+        return fail(ctx, GDY_ERR_TABLE, "bad entry line: %s", line.c_str());
       for (int c = 0; c < GDY_N_CD; ++c) {
         std::string name;
         in >> name;
@@ -1512,6 +1518,7 @@ gdy_status load_table(gdy_ctx* ctx, const char* path) {
       if (e.rc[0] >= 0 && e.rc[2] < 0) return fail(ctx, GDY_ERR_TABLE, "bad entry line: %s", line.c_str());
       e.ln = std::log2((double)e.n);
       e.lk = std::log2((double)e.k);
+      e.li = std::log2((double)e.items);
       if (e.dtype < 1 || e.dtype > 4 || (e.ta & ~1) || (e.tb & ~1))
         return fail(ctx, GDY_ERR_TABLE, "bad entry line: %s", line.c_str());
       t.by_layout[e.dtype][e.ta][e.tb].push_back((int)t.entries.size());

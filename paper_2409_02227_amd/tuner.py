@@ -272,7 +272,7 @@ def _lr_lines(lr) -> list:
 def write_table(path, ctx, records, lr=None, lr_by_type=None):
     """GO table: header, the shared predictor, one predictor block per input
     type that has its own ("lr_dtype <code>" then its four lines), entries."""
-    lines = ["gdy-go-table 1",
+    lines = ["gdy-go-table 2",
              f"# written by paper_2409_02227_amd.tuner on {time.strftime('%Y-%m-%d %H:%M:%S')}",
              f"device gfx950 cus {ctx.cus()}",
              f"catalogue {ctx.catalogue_hash():016x}"]
@@ -290,7 +290,8 @@ def write_table(path, ctx, records, lr=None, lr_by_type=None):
         rc = r.get("rc_best", {})
         if all(str(b) in rc for b in RCS[1:]):
             names += [rc[str(b)][0] for b in RCS[1:]]
-        lines.append(f"entry {DT_CODE[dtype]} {ta} {tb} {mlog} {n} {k} " + " ".join(names))
+        items = r["shape"][6] if len(r["shape"]) > 6 and r["shape"][6] > 0 else 1  # B-GEMM items
+        lines.append(f"entry {DT_CODE[dtype]} {ta} {tb} {mlog} {n} {k} {items} " + " ".join(names))
     with open(path, "w") as f:
         f.write("\n".join(lines) + "\n")
 
@@ -463,12 +464,13 @@ def knn_records(records, variants, frac: float, seed: int = 0, k: int = KNN_K):
     return out, stats
 
 
-def label_of(speedup: dict, tol: float = LABEL_TOL) -> int:
+def label_of(speedup: dict, tol: float = None) -> int:
     """Sec. 4.3 label with the Sec. 5.5 threshold: the CD with the most
     speedup over sequential, or 1 when no CD gains 5%.  Speedups within
     `tol` of the best are treated as ties (run-to-run spread of the timings
     on one MI355X is a few percent) and ties go to the largest CD: a GEMM
     indifferent to the degree then does not split a heterogeneous set."""
+    tol = LABEL_TOL if tol is None else tol
     best = max(speedup.values())
     if best < BEST_CD_GAIN:
         return 1
@@ -515,9 +517,13 @@ def main(argv=None):
                     help="no timing: from --records, keep this fraction as exhaustively tuned and "
                          "predict the other shapes' GO-Kernels by preferred-RC KNN (Sec. 7.5)")
     ap.add_argument("--knn-seed", type=int, default=0)
+    ap.add_argument("--label-tol", type=float, default=None,
+                    help=f"speedups within this fraction of the best count as ties (default {LABEL_TOL})")
     ap.add_argument("--max-seconds", type=float, default=0.0,
                     help="start no new shape after this many seconds (resume later from --records)")
     args = ap.parse_args(argv)
+    if args.label_tol is not None:
+        globals()["LABEL_TOL"] = args.label_tol  # label_of's default
 
     import torch
     from paper_2409_02227_amd import gdy

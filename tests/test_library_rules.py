@@ -342,3 +342,25 @@ def test_add_takes_a_slot_only_when_comparable(tmp_path, ctx):
         if cd_class == 0:
             assert p["n_groups"] == 3 and p["group_size"][:3] == [2, 1, 1]
         assert p["group_of"][1] == 0 and p["dispatch_of"][1] == p["dispatch_of"][p["order"][0]]
+
+
+def test_nearest_tuned_shape_counts_batch_items(tmp_path, ctx):
+    # version 2 entries name the tuned batch items: (256, 256, 64) as a single
+    # GEMM -> K64, as a batch of 64 items -> K128.  Distance adds
+    # |log2 items - log2 entry items|: a batch of 48 is 0.415 from 64 and
+    # 5.585 from 1; a single GEMM is 0 from 1.
+    b = ["0.0"] * 5
+    b[4] = "50.0"
+    lines = ["gdy-go-table 2", "device host cus 256", f"catalogue {ctx.catalogue_hash():016x}",
+             "lr_min " + " ".join(["0.0"] * 18), "lr_max " + " ".join(["1.0"] * 18),
+             "lr_w " + " ".join(["0.0"] * 90), "lr_b " + " ".join(b),
+             "entry 2 0 0 8 256 64 1 " + " ".join([K64 + "_c0"] * 5),
+             "entry 2 0 0 8 256 64 64 " + " ".join([K128 + "_c0"] * 5)]
+    path = tmp_path / "v2.table"
+    path.write_text("\n".join(lines) + "\n")
+    t = gdy.Context(-1, table=str(path))
+    iso = lambda d: t.variant(t.isolated_variant(d))["name"]  # noqa: E731
+    assert iso(desc(256, 256, 64, 0)) == K64 + "_c0"
+    assert iso(desc(256, 256, 64, 0, batch=64)) == K128 + "_c0"
+    assert iso(desc(256, 256, 64, 0, batch=48)) == K128 + "_c0"
+    assert t.plan([desc(256, 256, 64, 0)], mode="sequential")["fallback"] == 0
