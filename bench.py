@@ -224,8 +224,11 @@ def clock_snapshot():
 
 
 def clock_under_load(ctx, arr, n, mode, handle, torch, seconds=2.0):
-    """GPU clocks sampled by amd-smi while the submission runs back to back
-    for about `seconds` (the idle snapshots show the boost clock only)."""
+    """GPU clocks sampled by amd-smi (three samples, one every `seconds`/9)
+    while the submission runs back to back for about `seconds` (the idle
+    snapshots show the boost clock only)."""
+    if NO_CLOCKS:
+        return None
     from paper_2409_02227_amd import gdy
     m = gdy.MODES[mode]
     for _ in range(5):
@@ -233,7 +236,12 @@ def clock_under_load(ctx, arr, n, mode, handle, torch, seconds=2.0):
     torch.cuda.synchronize()
     box = {}
     import threading
-    th = threading.Thread(target=lambda: (time.sleep(seconds / 3), box.setdefault("c", clock_snapshot())))
+
+    def sample():
+        for i in range(3):
+            time.sleep(seconds / 9)
+            box[f"sample_{i}"] = clock_snapshot()
+    th = threading.Thread(target=sample)
     th.start()
     t0 = time.perf_counter()
     while time.perf_counter() - t0 < seconds or th.is_alive():
@@ -243,7 +251,9 @@ def clock_under_load(ctx, arr, n, mode, handle, torch, seconds=2.0):
         if time.perf_counter() - t0 > seconds + 30:
             break
     th.join(timeout=30)
-    return box.get("c")
+    # keep each sample's current clocks (gfx per XCD, memory), not their limits
+    return {k: {name: v for name, v in (c or {}).items() if name.endswith("/clk")}
+            for k, c in sorted(box.items())} or None
 
 
 def cpu_model() -> str:

@@ -118,7 +118,8 @@ def test_heterogeneous_submissions_all_200(wctx, het_pools, chunk):
         torch.cuda.synchronize()
         for (g, oa, ob), c in zip(placed[s_idx], outs):
             ii, jj = _sample(g.m, g.n, 8, 8, rng)
-            got = oracle.decode(c.view(torch.int16).cpu().numpy().view(np.uint16)[ii, jj], "bf16")
+            sel = c.view(torch.int16)[torch.from_numpy(ii).cuda(), torch.from_numpy(jj).cuda()]
+            got = oracle.decode(sel.cpu().numpy().view(np.uint16), "bf16")
             ref, bound = oracle.gemm_entries(g.m, g.n, g.k, a_host[oa:oa + g.m * g.k], "bf16", g.k,
                                              b_host[ob:ob + g.k * g.n], "bf16", g.n, ii, jj)
             ok, worst = oracle.accept(got, ref, bound, TAU["bf16"])
