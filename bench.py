@@ -62,22 +62,12 @@ WORKLOADS = {
 PARTITION_SHAPES = ((4096, 1024, 1024), (8192, 1024, 512), (2048, 2048, 2048), (4096, 4096, 1024),
                     (1024, 4096, 4096), (512, 8192, 8192), (256, 4096, 4096), (64, 8192, 2048))
 TRAFFIC = os.path.join(ROOT, "profiles", "hbm_traffic.json")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2409_02227_amd", "csrc", f)
-                  for f in ("go_kernel.h", "go_kernel_d.h")]
-
-
-def kernel_source_hash() -> str:
-    import hashlib
-    h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
-        h.update(open(f, "rb").read())
-    return h.hexdigest()[:16]
-
 
 def recorded_traffic(workload, kernel, gemm):
     """HBM bytes per launch of the dominant kernel from the committed
     FETCH_SIZE/WRITE_SIZE counter runs, scaled by the copy calibration;
     None when no record matches or the kernels changed since."""
+    from paper_2409_02227_amd.profiling import kernel_source_hash
     if not os.path.exists(TRAFFIC):
         return None
     for r in json.load(open(TRAFFIC)).get("records", []):
@@ -266,7 +256,7 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def dominant_kernel(ctx, mats, plan, steps):
+def dominant_kernel(ctx, mats, plan, steps, gemms, mode):
     """Kernel dispatch (a variant over the GEMMs it runs) with the largest
     total time over the timed steps; returns its name, the GEMMs it covers,
     per-dispatch algorithmic flops and bytes, and the mean duration from the
@@ -288,16 +278,9 @@ def dominant_kernel(ctx, mats, plan, steps):
     idx = members[d]
     v = ctx.variant(plan["variant_of"][idx[0]])
     specs = [mats[i].spec for i in idx]
-    # workgroups of the dispatch (to find it in a profiler trace): each GEMM
-    # its tiles or cap x occupancy, all but the last rounded up to 8
-    grid = 0
-    for u, i in enumerate(idx):
-        w = ctx.variant(plan["variant_of"][i])
-        s = mats[i].spec
-        wg = -(-s.m // w["bm"]) * -(-s.n // w["bn"]) * s.items
-        if w["grid_cap_cus"]:
-            wg = min(wg, w["grid_cap_cus"] * max(w["occupancy"], 1))
-        grid += -(-wg // 8) * 8 if u + 1 < len(idx) else wg
+    # workgroups of the dispatch (to find it in a profiler trace), as the
+    # library launches it
+    grid = ctx.dispatch_map(gemms, mode=mode, dispatch=d, max_workgroups=0)["grid"]
     return {"variant": v["name"], "shape": [[s.m, s.n, s.k] + ([s.batch] if s.batch else []) for s in specs], "grid": grid,
             "launches": len(per[d]), "mean_ms": float(np.mean(per[d])),
             "flops": sum(s.flops for s in specs),
@@ -670,7 +653,7 @@ def main():
     t_mode = time_steps(ctx, arr, n, args.mode, args.steps, args.warmup, handle, torch)
     # per-dispatch events in a pass of their own (event records cost host time)
     time_steps(ctx, arr, n, args.mode, args.steps, 1, handle, torch, timing=True)
-    dom = dominant_kernel(ctx, mats, plan, args.steps)
+    dom = dominant_kernel(ctx, mats, plan, args.steps, gemms, args.mode)
     latency = step_latency(ctx, arr, n, args.mode, max(args.latency_steps, args.steps), handle, torch)
     t_best, cd_best = best_cd_time(ctx, arr, n, args.steps, args.warmup, handle, torch)
     clocks_load = clock_under_load(ctx, arr, n, args.mode, handle, torch)
@@ -683,6 +666,7 @@ def main():
             "frac": round(ach / peak, 4),
             "traffic": recorded_traffic(args.workload, dom["variant"], dom["shape"]),
             "kernel": dom["variant"], "gemms": dom["shape"], "workgroups": dom["grid"],
+            "algorithmic_bytes": int(dom["bytes"]),
             "launches": dom["launches"],
             "mean_ms": round(dom["mean_ms"], 4)}
     ai = dom["flops"] / dom["bytes"]

@@ -14,8 +14,17 @@ Every child runs as `rocprofv3 ... -- python3 <committed script>`: the
 profiler's preloaded library starts the GPU before the program, so the
 program itself follows `--` directly (no shell or env hop).
 
+Two more outputs: `trace` writes a kernel-trace summary of a bench run (the
+kernels with the largest total time, and the dominant dispatch's mean beside
+the one bench.py measured with HIP events in the same run), and `collect
+--traffic-record` stores the scaled FETCH_SIZE + WRITE_SIZE bytes of a
+workload's dominant dispatch in the record file bench.py reports as the
+roofline's `traffic` while the kernel sources hash the same.
+
 Usage, on a GPU machine:
-  python3 -m paper_2409_02227_amd.profiling collect --workload tp8_layer_share --out profiles/x.md
+  python3 -m paper_2409_02227_amd.profiling trace --workload tp8_layer_share --out profiles/x.md
+  python3 -m paper_2409_02227_amd.profiling collect --workload tp8_layer_share --out profiles/x.md \
+      --traffic-record profiles/hbm_traffic.json
   python3 -m paper_2409_02227_amd.profiling collect --gemm 4096x4096x4096 --kernel iso --out ...
   python3 -m paper_2409_02227_amd.profiling collect --gemm 4096x4096x4096 --kernel hipblaslt --out ...
   python3 -m paper_2409_02227_amd.profiling run-gemm 4096x4096x4096 iso 10   (the child of --gemm)
@@ -49,17 +58,29 @@ PASSES = {
     "write": ["WRITE_SIZE"],
 }
 COPY_BYTES = 1 << 30
+# what the kernels' HBM traffic depends on: the kernels, the launch block and
+# work mapping they share with the host, and the planner that fills it
+KERNEL_SOURCES = [os.path.join(HERE, "csrc", f) for f in ("go_kernel.h", "go_kernel_d.h", "gdy_internal.h",
+                                                         "gdy.cpp")]
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def _python() -> str:
     return sys.executable or "python3"
 
 
-def target_cmd(args) -> list:
+def target_cmd(args, warmup: int = 1) -> list:
     """The profiled program (a committed script and its arguments)."""
     if args.workload:
         return [_python(), os.path.join(ROOT, "bench.py"), "--workload", args.workload, "--mode", args.mode,
-                "--steps", str(args.steps), "--warmup", "1", "--cpu-seconds", "0", "--submissions", "0",
+                "--steps", str(args.steps), "--warmup", str(warmup), "--cpu-seconds", "0", "--submissions", "0",
                 "--no-clocks"]
     return [_python(), "-m", "paper_2409_02227_amd.profiling", "run-gemm", args.gemm, args.kernel,
             str(args.steps), args.dtype]
@@ -114,14 +135,30 @@ def read_counters(d: str) -> list:
 
 
 def read_trace(d: str) -> list:
+    """Per-dispatch rows in dispatch order: {"kernel", "grid" (threads),
+    "wg" (threads per workgroup), "ns"}."""
     out = []
     for f in glob.glob(os.path.join(d, "*kernel_trace.csv")):
         with open(f) as fh:
             for r in csv.DictReader(fh):
                 grid = int(r.get("Grid_Size") or r.get("Grid_Size_X") or 0)
-                out.append({"kernel": r["Kernel_Name"], "grid": grid,
+                wg = int(r.get("Workgroup_Size") or r.get("Workgroup_Size_X") or 0)
+                out.append({"kernel": r["Kernel_Name"], "grid": grid, "wg": wg, "id": int(r["Dispatch_Id"]),
                             "ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"])})
+    out.sort(key=lambda r: r["id"])
     return out
+
+
+def bench_line(log_path: str):
+    """The JSON line a profiled bench.py run printed (None if it printed none)."""
+    line = None
+    if os.path.exists(log_path):
+        with open(log_path) as f:
+            for raw in f:
+                raw = raw.strip()
+                if raw.startswith("{") and '"metric"' in raw:
+                    line = raw
+    return json.loads(line) if line else None
 
 
 def is_gemm_kernel(name: str) -> bool:
@@ -161,7 +198,7 @@ def collect(args) -> None:
     key = dominant(trace)
     durs = [r["ns"] for r in trace if (r["kernel"], r["grid"]) == key]
     res = {"kernel": key[0], "grid": key[1], "dispatches": len(durs), "mean_us": sum(durs) / len(durs) / 1e3}
-    vals = {}
+    vals, counted = {}, {}
     for name, counters in PASSES.items():
         if args.passes and name not in args.passes.split(","):
             continue
@@ -174,6 +211,7 @@ def collect(args) -> None:
             v = mean_of(rows, k, c)
             if v is not None:
                 vals[c] = v
+                counted[c] = [r for r in rows if (r["kernel"], r["grid"]) == k]
     cal = {}
     if "FETCH_SIZE" in vals or "WRITE_SIZE" in vals:
         for name, c in (("copy_fetch", "FETCH_SIZE"), ("copy_write", "WRITE_SIZE")):
@@ -188,14 +226,117 @@ def collect(args) -> None:
     res["counters"] = vals
     res["calibration"] = cal
     res["derived"] = derived(vals, cal)
+    res["dispatches_counted"] = {c: sum(1 for r in counted.get(c, []) if c in r) for c in ("FETCH_SIZE", "WRITE_SIZE")}
     res["command"] = " ".join(shlex.quote(x) for x in ["python3", "-m", "paper_2409_02227_amd.profiling",
                                                          *sys.argv[1:]])
-    res["target"] = " ".join(shlex.quote(os.path.relpath(x, ROOT) if x.startswith(ROOT) else x) for x in cmd)
+    res["target"] = " ".join(["python3"] + [shlex.quote(os.path.relpath(x, ROOT) if x.startswith(ROOT) else x)
+                               for x in cmd[1:]])
     with open(os.path.join(out_dir, "summary.json"), "w") as f:
         json.dump(res, f, indent=1)
+    if args.traffic_record:
+        write_traffic_record(args.traffic_record, args.workload, res, bench_line(os.path.join(out_dir, "trace.log")))
     if args.out:
         write_summary(args.out, res, args)
     print(json.dumps(res["derived"]), flush=True)
+
+
+def write_traffic_record(path: str, workload: str, res: dict, line) -> None:
+    """Store the dominant dispatch's HBM bytes (FETCH_SIZE and WRITE_SIZE
+    means, each scaled by the copy calibration) under the workload, the
+    variant, its member shapes and the current kernel source hash, replacing
+    an earlier record of the same workload and variant."""
+    v, cal = res["counters"], res["calibration"]
+    if line is None or "roofline" not in line:
+        raise RuntimeError("the profiled bench run printed no roofline")
+    if not (v.get("FETCH_SIZE") and v.get("WRITE_SIZE") and cal.get("FETCH_SIZE") and cal.get("WRITE_SIZE")):
+        raise RuntimeError("--traffic-record needs the fetch and write passes and their calibration")
+    roof = line["roofline"]
+    fetch_f = round(cal["FETCH_SIZE"], 3)
+    write_f = round(cal["WRITE_SIZE"], 3)
+    rec = {"workload": workload, "kernel": roof["kernel"], "gemm": roof["gemms"],
+           "workgroups": roof["workgroups"], "kernel_source_hash": kernel_source_hash(),
+           "fetch_kib_per_dispatch": round(v["FETCH_SIZE"], 1), "write_kib_per_dispatch": round(v["WRITE_SIZE"], 1),
+           "dispatches_counted": [res["dispatches_counted"]["FETCH_SIZE"], res["dispatches_counted"]["WRITE_SIZE"]],
+           "fetch_factor": fetch_f, "write_factor": write_f,
+           "bytes_per_launch": int(v["FETCH_SIZE"] * 1024 * fetch_f + v["WRITE_SIZE"] * 1024 * write_f),
+           "algorithmic_bytes_per_launch": roof.get("algorithmic_bytes"),
+           "command": res["command"]}
+    data = {"note": "HBM-side bytes per dispatch from rocprofv3 FETCH_SIZE / WRITE_SIZE runs, scaled by the "
+                    "same counters on a 1 GiB device copy", "records": []}
+    if os.path.exists(path):
+        with open(path) as f:
+            data = json.load(f)
+    data["records"] = [r for r in data.get("records", [])
+                       if not (r.get("workload") == workload and r.get("kernel") == rec["kernel"])] + [rec]
+    with open(path, "w") as f:
+        json.dump(data, f, indent=1)
+    print(f"traffic record: {rec['bytes_per_launch'] / 1e6:.1f} MB per launch "
+          f"({rec['algorithmic_bytes_per_launch']} algorithmic bytes)", flush=True)
+
+
+def trace(args) -> None:
+    """Kernel-trace summary of one bench.py run: the kernels (symbol and
+    workgroup count) with the largest total time, and the dominant one's
+    trace mean and median beside the mean the bench measured itself with HIP
+    events."""
+    out_dir = os.path.abspath(args.raw)
+    os.makedirs(out_dir, exist_ok=True)
+    cmd = target_cmd(args, warmup=args.warmup)
+    d = run_pass(out_dir, "trace", None, cmd, args.timeout)
+    rows = read_trace(d)
+    line = bench_line(os.path.join(out_dir, "trace.log"))
+    if not args.keep_raw:
+        prune(d)
+    # the same command without the profiler, whose per-launch host work
+    # lengthens the event-timed span of launch-bound dispatches
+    print(f"== unprofiled: {' '.join(shlex.quote(x) for x in cmd)}", flush=True)
+    with open(os.path.join(out_dir, "unprofiled.log"), "w") as log:
+        r = subprocess.run(["timeout", "-s", "KILL", str(args.timeout)] + cmd, stdout=log,
+                           stderr=subprocess.STDOUT, cwd=ROOT)
+    if r.returncode != 0:
+        raise RuntimeError(f"unprofiled run failed with {r.returncode}; see {out_dir}/unprofiled.log")
+    plain = bench_line(os.path.join(out_dir, "unprofiled.log"))
+    groups = {}
+    for r in rows:
+        k = (r["kernel"], r["grid"] // max(r["wg"], 1))
+        groups.setdefault(k, []).append(r["ns"] / 1e3)
+    top = sorted(groups.items(), key=lambda kv: -sum(kv[1]))[:args.top]
+    cmdline = " ".join(shlex.quote(x) for x in ["python3", "-m", "paper_2409_02227_amd.profiling", *sys.argv[1:]])
+    target = " ".join(["python3"] + [shlex.quote(os.path.relpath(x, ROOT) if x.startswith(ROOT) else x)
+                               for x in cmd[1:]])
+    lines = [f"# Kernel trace: {args.workload} workload, {args.mode} mode", "",
+             "Command (on the GPU box, from the repository root):", "", f"    {cmdline}", "",
+             f"which runs `rocprofv3 --kernel-trace --stats` over `{target}`.", "",
+             "The bench times the set in default, GO, sequential and the chosen mode, runs a pass with "
+             "per-dispatch events, a latency pass and the best-CD search; durations are End - Start "
+             "timestamps of the kernel trace, grouped by kernel symbol and workgroup count.", "",
+             "| kernel | workgroups | calls | avg us | min us | max us | total ms |",
+             "|---|---|---|---|---|---|---|"]
+    for (name, wgs), ds in top:
+        lines.append(f"| `{short(name)}` | {wgs} | {len(ds)} | {sum(ds) / len(ds):.1f} | {min(ds):.1f} | "
+                     f"{max(ds):.1f} | {sum(ds) / 1e3:.2f} |")
+    if line and "roofline" in line:
+        roof = line["roofline"]
+        lines += ["", f"Dominant dispatch as the bench reports it: variant `{roof['kernel']}`, "
+                      f"{roof['workgroups']} workgroups, members {roof['gemms']}; "
+                      f"mean {roof['mean_ms'] * 1e3:.1f} us over {roof['launches']} launches from HIP events "
+                      f"on the dispatch's own stream, in this profiled run."]
+        wg = roof["workgroups"]
+        same = [ds for (name, w), ds in groups.items() if w == wg and "go_gemm" in name]
+        if same:
+            ds = sorted(max(same, key=len))
+            lines.append(f"Kernel trace, the same workgroup count: {len(ds)} dispatches over every pass "
+                         f"(all modes that launch it), mean {sum(ds) / len(ds):.1f} us, median "
+                         f"{ds[len(ds) // 2]:.1f} us.")
+        lines.append(f"Bench line: value {line['value']} {line['unit']}, ms_per_step {line['ms_per_step']}.")
+    if plain and "roofline" in plain:
+        roof = plain["roofline"]
+        lines += ["", f"The same command without the profiler: dominant dispatch mean {roof['mean_ms'] * 1e3:.1f} us "
+                      f"from HIP events ({roof['launches']} launches), value {plain['value']} {plain['unit']}, "
+                      f"ms_per_step {plain['ms_per_step']}, roofline frac {roof['frac']}."]
+    with open(args.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines[-4:]), flush=True)
 
 
 def derived(v: dict, cal: dict) -> dict:
@@ -298,6 +439,17 @@ def main():
     c.add_argument("--out", help="write the text summary here (profiles/...)")
     c.add_argument("--timeout", type=int, default=150)
     c.add_argument("--keep-raw", action="store_true", help="keep the per-dispatch CSVs of every pass")
+    c.add_argument("--traffic-record", help="store the dispatch's HBM bytes in this record file (--workload)")
+    t = sub.add_parser("trace")
+    t.add_argument("--workload", required=True)
+    t.add_argument("--mode", default="selector")
+    t.add_argument("--steps", type=int, default=20)
+    t.add_argument("--warmup", type=int, default=5)
+    t.add_argument("--top", type=int, default=5)
+    t.add_argument("--raw", default="gpurun_out/profiling_trace")
+    t.add_argument("--out", required=True)
+    t.add_argument("--timeout", type=int, default=240)
+    t.add_argument("--keep-raw", action="store_true")
     r = sub.add_parser("run-gemm")
     r.add_argument("spec")
     r.add_argument("kernel")
@@ -306,8 +458,12 @@ def main():
     args = ap.parse_args()
     if args.cmd == "run-gemm":
         return run_gemm(args.spec, args.kernel, args.reps, args.dtype)
+    if args.cmd == "trace":
+        return trace(args)
     if bool(args.workload) == bool(args.gemm):
         raise SystemExit("give one of --workload or --gemm")
+    if args.traffic_record and not args.workload:
+        raise SystemExit("--traffic-record needs --workload")
     t0 = time.time()
     collect(args)
     print(f"profiling done in {time.time() - t0:.0f} s", flush=True)

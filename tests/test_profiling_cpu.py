@@ -1,0 +1,87 @@
+"""Host logic of the profiling harness (no profiler, no GPU): reading the
+profiler's CSVs, choosing the dominant dispatch, the derived metrics, and the
+HBM traffic record bench.py reads back."""
+import csv
+import json
+import os
+
+import pytest
+
+from paper_2409_02227_amd import profiling
+
+
+def _write_csv(path, rows):
+    with open(path, "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=list(rows[0]))
+        w.writeheader()
+        w.writerows(rows)
+
+
+def test_trace_rows_and_dominant(tmp_path):
+    rows = []
+    for i, (name, grid, ns) in enumerate([("gdy::go_gemm_d<A>", 560 * 512, 480_000),
+                                          ("void at::fill_kernel", 1024, 900_000),
+                                          ("gdy::go_gemm_d<A>", 560 * 512, 470_000),
+                                          ("gdy::go_gemm_d<B>", 192 * 256, 300_000)]):
+        rows.append({"Dispatch_Id": 10 - i, "Kernel_Name": name, "Grid_Size_X": grid, "Workgroup_Size_X":
+                     512 if "<A>" in name else 256, "Start_Timestamp": 1000, "End_Timestamp": 1000 + ns})
+    _write_csv(tmp_path / "p_kernel_trace.csv", rows)
+    tr = profiling.read_trace(str(tmp_path))
+    assert [r["id"] for r in tr] == [7, 8, 9, 10]  # dispatch order
+    # the fill kernel is longer but is not a GEMM; A's total (950 us) beats B's
+    assert profiling.dominant(tr) == ("gdy::go_gemm_d<A>", 560 * 512)
+
+
+def test_counters_summed_per_dispatch(tmp_path):
+    rows = []
+    for disp, ctr, val in [(1, "FETCH_SIZE", 100.0), (1, "FETCH_SIZE", 50.0), (2, "FETCH_SIZE", 210.0)]:
+        rows.append({"Dispatch_Id": disp, "Kernel_Name": "gdy::go_gemm_d<A>", "Grid_Size": 4096,
+                     "Start_Timestamp": 0, "End_Timestamp": 10, "Counter_Name": ctr, "Counter_Value": val})
+    _write_csv(tmp_path / "p_counter_collection.csv", rows)
+    got = profiling.read_counters(str(tmp_path))
+    assert sorted(r["FETCH_SIZE"] for r in got) == [150.0, 210.0]  # per-dimension values add up
+    assert profiling.mean_of(got, ("gdy::go_gemm_d<A>", 4096), "FETCH_SIZE") == 180.0
+
+
+def test_derived_metrics():
+    v = {"MfmaUtil": 44.123, "SQ_WAVE_CYCLES": 1000.0, "SQ_WAIT_INST_ANY": 470.0, "SQ_LDS_BANK_CONFLICT": 30.0,
+         "SQ_INSTS_LDS": 60.0, "TCC_HIT_sum": 695.0, "TCC_MISS_sum": 305.0, "FETCH_SIZE": 1000.0}
+    d = profiling.derived(v, {"FETCH_SIZE": 2.0})
+    assert d["mfma_util_pct"] == 44.12 and d["wait_inst_any_per_wave_cycle"] == 0.47
+    assert d["lds_bank_conflict_cycles_per_lds_inst"] == 0.5 and d["l2_hit_pct"] == 69.5
+    assert d["hbm_read_bytes"] == 1000 * 1024 * 2
+
+
+def test_bench_line_takes_the_last_metric_line(tmp_path):
+    log = tmp_path / "trace.log"
+    log.write_text('noise\n{"metric": "m", "value": 1}\n{"other": 2}\n{"metric": "m", "value": 2}\ntail\n')
+    assert profiling.bench_line(str(log))["value"] == 2
+    assert profiling.bench_line(str(tmp_path / "none.log")) is None
+
+
+def test_traffic_record_replaces_and_matches_bench(tmp_path, monkeypatch):
+    path = tmp_path / "traffic.json"
+    old = {"note": "n", "records": [{"workload": "w", "kernel": "k", "gemm": [[1, 2, 3]], "bytes_per_launch": 1},
+                                    {"workload": "other", "kernel": "k", "bytes_per_launch": 7}]}
+    path.write_text(json.dumps(old))
+    res = {"counters": {"FETCH_SIZE": 1000.0, "WRITE_SIZE": 500.0}, "calibration": {"FETCH_SIZE": 2.0,
+           "WRITE_SIZE": 1.0}, "dispatches_counted": {"FETCH_SIZE": 12, "WRITE_SIZE": 11}, "command": "c"}
+    line = {"roofline": {"kernel": "k", "gemms": [[512, 6144, 12288]], "workgroups": 560,
+                         "algorithmic_bytes": 999}}
+    profiling.write_traffic_record(str(path), "w", res, line)
+    recs = json.loads(path.read_text())["records"]
+    assert [r["workload"] for r in recs] == ["other", "w"]
+    r = recs[-1]
+    assert r["bytes_per_launch"] == (1000 * 2 + 500) * 1024
+    assert r["dispatches_counted"] == [12, 11] and r["kernel_source_hash"] == profiling.kernel_source_hash()
+    # bench.py finds it under the same workload, kernel and member shapes
+    import importlib.util
+    spec = importlib.util.spec_from_file_location(
+        "bench_mod", os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "bench.py"))
+    bench = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(bench)
+    monkeypatch.setattr(bench, "TRAFFIC", str(path))
+    assert bench.recorded_traffic("w", "k", [[512, 6144, 12288]]) == r["bytes_per_launch"]
+    assert bench.recorded_traffic("w", "k", [[512, 6144, 6144]]) is None
+    with pytest.raises(RuntimeError):
+        profiling.write_traffic_record(str(path), "w", dict(res, counters={"FETCH_SIZE": 1.0}), line)
