@@ -231,12 +231,14 @@ class AddInputs:
     c: object
     c_full: object
     host: dict
+    c_guard: object = None        # GUARD_ROWS rows of ld elements right after c_full (NaN)
 
 
 def materialize_add(m: int, n: int, dtype: str = "bf16", seed: int = 0, pad: int = 0,
                     device="cuda") -> AddInputs:
     """A, B ~ U[-1, 1] of the given type with leading dimension n + pad;
-    C (same type) prefilled with NaN, its padding columns included."""
+    C (same type) prefilled with NaN, its padding columns and guard rows
+    included."""
     import torch
     ld = n + pad
     rng = np.random.default_rng([seed, 7])
@@ -245,8 +247,10 @@ def materialize_add(m: int, n: int, dtype: str = "bf16", seed: int = 0, pad: int
     b_codes = encode(_draw(rng, u, m * ld), dtype)
     a = _device_tensor(a_codes, dtype, m, ld, n, device)
     b = _device_tensor(b_codes, dtype, m, ld, n, device)
-    cfull = torch.full((m, ld), float("nan"), dtype=getattr(torch, _TORCH_CODE[dtype]), device=device)
-    return AddInputs(m, n, dtype, ld, a, b, cfull[:, :n], cfull, {"a": a_codes, "b": b_codes})
+    buf = torch.full(((m + GUARD_ROWS) * ld,), float("nan"), dtype=getattr(torch, _TORCH_CODE[dtype]),
+                     device=device)
+    cfull = buf[:m * ld].view(m, ld)
+    return AddInputs(m, n, dtype, ld, a, b, cfull[:, :n], cfull, {"a": a_codes, "b": b_codes}, buf[m * ld:])
 
 
 def gemm_add_pairs(seed: int = 7) -> list:
@@ -279,6 +283,23 @@ class Materialized:
     scale_a: float = 1.0
     scale_b: float = 1.0
     host: dict = field(default_factory=dict)  # flat codes of a and b when kept
+    c_guard: object = None        # GUARD_ROWS rows of ldc elements right after c_full (NaN)
+
+
+GUARD_ROWS = 4
+
+
+def _output(spec: GemmSpec, device):
+    """C's ldc-wide buffer (items x M x ldc, or M x ldc) with GUARD_ROWS rows
+    of NaN behind it in the same allocation: writes past C's last row land
+    there and show."""
+    import torch
+    odt = getattr(torch, _TORCH_CODE[OUT[spec.dtype]])
+    ldc = spec.ld("c")
+    shape = (spec.batch, spec.m, ldc) if spec.batch > 0 else (spec.m, ldc)
+    body = int(np.prod(shape))
+    buf = torch.full((body + GUARD_ROWS * ldc,), float("nan"), dtype=odt, device=device)
+    return buf[:body].view(shape), buf[body:]
 
 
 def _device_tensor(codes: np.ndarray, dtype: str, rows: int, ld: int, cols: int, device):
@@ -299,16 +320,14 @@ def from_codes(spec: GemmSpec, a_codes: np.ndarray, b_codes: np.ndarray, scale_a
                scale_b: float = 1.0, device="cuda") -> Materialized:
     """Device operands from given flat codes in the stored layouts of `spec`
     (for inputs with a chosen structure, e.g. all-subnormal operands)."""
-    import torch
     ar, ac = spec.stored_shape("a")
     br, bc = spec.stored_shape("b")
     assert a_codes.size == ar * spec.ld("a") and b_codes.size == br * spec.ld("b")
     a = _device_tensor(a_codes, spec.dtype, ar, spec.ld("a"), ac, device)
     b = _device_tensor(b_codes, spec.dtype, br, spec.ld("b"), bc, device)
-    odt = getattr(torch, _TORCH_CODE[OUT[spec.dtype]])
-    cfull = torch.full((spec.m, spec.ld("c")), float("nan"), dtype=odt, device=device)
+    cfull, guard = _output(spec, device)
     return Materialized(spec, a, b, cfull[:, :spec.n], cfull, scale_a, scale_b,
-                        {"a": a_codes, "b": b_codes})
+                        {"a": a_codes, "b": b_codes}, guard)
 
 
 def materialize(spec: GemmSpec, device="cuda", keep_host=True) -> Materialized:
@@ -317,23 +336,21 @@ def materialize(spec: GemmSpec, device="cuda", keep_host=True) -> Materialized:
     br, bc = spec.stored_shape("b")
     a_codes, sa = operand_codes(spec, "a")
     b_codes, sb = operand_codes(spec, "b")
-    odt = getattr(torch, _TORCH_CODE[OUT[spec.dtype]])
+    cfull, guard = _output(spec, device)
     if spec.batch > 0:
         tdt = getattr(torch, _TORCH_CODE[spec.dtype])
         flat_a = torch.from_numpy(a_codes.view(_RAW_VIEW[ELEM[spec.dtype]])).to(device).view(tdt)
         flat_b = torch.from_numpy(b_codes.view(_RAW_VIEW[ELEM[spec.dtype]])).to(device).view(tdt)
         a = _batched(flat_a, spec, "a", ar, ac)
         b = _batched(flat_b, spec, "b", br, bc)
-        cfull = torch.full((spec.batch, spec.m, spec.ld("c")), float("nan"), dtype=odt, device=device)
         c = cfull[:, :, :spec.n]
         host = {"a": a_codes, "b": b_codes} if keep_host else {}
-        return Materialized(spec, a, b, c, cfull, sa, sb, host)
+        return Materialized(spec, a, b, c, cfull, sa, sb, host, guard)
     a = _device_tensor(a_codes, spec.dtype, ar, spec.ld("a"), ac, device)
     b = _device_tensor(b_codes, spec.dtype, br, spec.ld("b"), bc, device)
-    cfull = torch.full((spec.m, spec.ld("c")), float("nan"), dtype=odt, device=device)
     c = cfull[:, :spec.n]
     host = {"a": a_codes, "b": b_codes} if keep_host else {}
-    return Materialized(spec, a, b, c, cfull, sa, sb, host)
+    return Materialized(spec, a, b, c, cfull, sa, sb, host, guard)
 
 
 HET_A_ELEMS, HET_B_ELEMS = 600 << 20, 1200 << 20  # 1.2 GB and 2.4 GB of bf16

@@ -38,6 +38,7 @@ def check(mat, rng=None, samples=8, label=""):
         for i in range(s.batch):
             item = _item(mat, i)
             worst = max(worst, check(item, rng, samples, f"{label} item {i}"))
+        assert_untouched(mat, label)
         return worst
     dt = ORC[s.dtype]
     got = decode_out(mat)
@@ -59,11 +60,19 @@ def check(mat, rng=None, samples=8, label=""):
         ok, worst = oracle.accept(got[ii, jj], ref, bound, TAU[s.dtype])
     assert ok, f"{label} {s.name} ({s.m},{s.n},{s.k},{s.dtype},t{s.trans_a}{s.trans_b}): " \
                f"outside bound, worst ratio {worst:.3g}"
-    # columns between n and ldc must be untouched (they were NaN)
-    if s.pad_c:
-        pad = mat.c_full[:, s.n:].float()
-        assert torch.isnan(pad).all().item(), f"{label} {s.name}: wrote into C padding"
+    assert_untouched(mat, label)
     return worst
+
+
+def assert_untouched(mat, label=""):
+    """C's padding columns (between n and ldc) and the guard rows behind C's
+    last row still hold the NaN they were filled with."""
+    s = mat.spec
+    if s.pad_c:
+        pad = mat.c_full[..., s.n:].float()
+        assert torch.isnan(pad).all().item(), f"{label} {s.name}: wrote into C padding"
+    if mat.c_guard is not None:
+        assert torch.isnan(mat.c_guard.float()).all().item(), f"{label} {s.name}: wrote past C's last row"
 
 
 def _item(mat, i):
@@ -76,6 +85,7 @@ def _item(mat, i):
         r, _ = s.stored_shape(w)
         off = i * s.item_stride(w)
         host[w] = mat.host[w][off:off + r * s.ld(w)]
+    # an item's guard is the next item's rows: the whole batch's guard is checked once
     return inputs.Materialized(single, mat.a[i], mat.b[i], mat.c[i], mat.c_full[i], mat.scale_a,
                                mat.scale_b, host)
 
@@ -89,6 +99,8 @@ def gemm_of(mat, variant=-1):
 def reset_outputs(mats):
     for m in mats:
         m.c_full.fill_(float("nan"))
+        if m.c_guard is not None:
+            m.c_guard.fill_(float("nan"))
 
 
 def check_add(x, label=""):
@@ -104,4 +116,6 @@ def check_add(x, label=""):
     assert ok, f"{label} add ({x.m},{x.n},{x.dtype}): outside bound, worst ratio {worst:.3g}"
     if x.ld > x.n:
         assert torch.isnan(x.c_full[:, x.n:].float()).all().item(), f"{label}: wrote into C padding"
+    if x.c_guard is not None:
+        assert torch.isnan(x.c_guard.float()).all().item(), f"{label}: wrote past C's last row"
     return worst

@@ -22,7 +22,7 @@ torch = pytest.importorskip("torch")
 
 import oracle  # noqa: E402
 from paper_2409_02227_amd import gdy, inputs  # noqa: E402
-from tests.gpu_helpers import ORC, TAU, decode_out, gemm_of, out_codes, reset_outputs  # noqa: E402
+from tests.gpu_helpers import ORC, TAU, assert_untouched, decode_out, gemm_of, out_codes, reset_outputs  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 TABLE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
@@ -64,6 +64,7 @@ def test_layer_share_every_element_every_mode(wctx):
         for i, (m, (ref, bound)) in enumerate(zip(mats, refs)):
             ok, worst = oracle.accept(decode_out(m), ref, bound, TAU["bf16"])
             assert ok, f"{mode} {m.spec.name}: worst ratio {worst:.3g}"
+            assert_untouched(m, mode)
             key = (i, wctx.variant(plan["variant_of"][i])["name"].rsplit("_c", 1)[0])
             codes = out_codes(m)
             if key in bits:
@@ -92,6 +93,7 @@ def test_fp8_tenants(wctx, mode):
                                              m.scale_a, m.scale_b)
             ok, worst = oracle.accept(got[ii, jj], ref, bound, TAU["fp8"])
         assert ok, f"{mode} {s.name} ({s.m},{s.n},{s.k}): worst ratio {worst:.3g}"
+        assert_untouched(m, mode)
 
 
 @pytest.fixture(scope="module")
@@ -107,13 +109,15 @@ def test_heterogeneous_submissions_all_200(wctx, het_pools, chunk):
     a_pool, b_pool, a_host, b_host, placed = het_pools
     rng = np.random.default_rng(400 + chunk)
     for s_idx in range(20 * chunk, 20 * chunk + 20):
-        gemms, outs = [], []
+        gemms, outs, guards = [], [], []
         for g, oa, ob in placed[s_idx]:
             a = a_pool[oa:oa + g.m * g.k].view(g.m, g.k)
             b = b_pool[ob:ob + g.k * g.n].view(g.k, g.n)
-            c = torch.full((g.m, g.n), float("nan"), dtype=torch.bfloat16, device="cuda")
+            buf = torch.full(((g.m + inputs.GUARD_ROWS) * g.n,), float("nan"), dtype=torch.bfloat16, device="cuda")
+            c = buf[:g.m * g.n].view(g.m, g.n)
             gemms.append(gdy.Gemm(a, b, c))
             outs.append(c)
+            guards.append(buf[g.m * g.n:])
         wctx.execute(gemms, mode="selector")
         torch.cuda.synchronize()
         for (g, oa, ob), c in zip(placed[s_idx], outs):
@@ -124,4 +128,5 @@ def test_heterogeneous_submissions_all_200(wctx, het_pools, chunk):
                                              b_host[ob:ob + g.k * g.n], "bf16", g.n, ii, jj)
             ok, worst = oracle.accept(got, ref, bound, TAU["bf16"])
             assert ok, f"submission {s_idx} ({g.m},{g.n},{g.k}): worst ratio {worst:.3g}"
+        assert all(torch.isnan(gd.float()).all().item() for gd in guards), f"submission {s_idx}: wrote past C"
     print(f"submissions {20 * chunk}-{20 * chunk + 19}: sampled rows and columns within the bound", flush=True)
