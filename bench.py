@@ -56,8 +56,9 @@ WORKLOADS = {
                               "(CU-masked streams) and unpartitioned"),
     "knn_tuning": ("knn", "CD copies (CD = 2, 4, 8, 16) of 40 bf16 shapes whose GO-Kernels a KNN "
                           "table predicts from the 20% of shapes tuned exhaustively"),
-    "selector_accuracy": ("acc", "n copies (n = 2, 4, 8, 16) of untuned bf16 shapes drawn like the "
-                                 "heterogeneous submissions'; selector CD against the best CD"),
+    "selector_accuracy": ("acc", "n copies (n = 2, 4, 8, 16) of bf16 shapes (untuned ones drawn like the "
+                                 "heterogeneous submissions', or --accuracy-set tuned); selector CD against "
+                                 "the best CD, selector and GO against default"),
 }
 PARTITION_SHAPES = ((4096, 1024, 1024), (8192, 1024, 512), (2048, 2048, 2048), (4096, 4096, 1024),
                     (1024, 4096, 4096), (512, 8192, 8192), (256, 4096, 4096), (64, 8192, 2048))
@@ -108,7 +109,10 @@ def parse():
                          "het_submissions block of the default run; 0 skips that block)")
     ap.add_argument("--no-clocks", action="store_true", help="do not sample GPU clocks with amd-smi")
     ap.add_argument("--accuracy-shapes", type=int, default=30,
-                    help="selector_accuracy workload: number of untuned shapes")
+                    help="selector_accuracy workload: number of shapes")
+    ap.add_argument("--accuracy-set", default="untuned", choices=("untuned", "tuned"),
+                    help="selector_accuracy workload: shapes drawn like the heterogeneous submissions' "
+                         "(none tuned), or a seeded sample of the GO table's bf16 NN shapes")
     ap.add_argument("--latency-steps", type=int, default=50,
                     help="steps of the event-timed pass that gives the p10/p50/p90 step latency")
     ap.add_argument("--knn-table", default=KNN_TABLE,
@@ -417,14 +421,29 @@ def accuracy_bench(args, desc):
     heterogeneous submissions' (none of them a tuned shape), each set timed
     at every CD to find the best one (Sec. 5.5 'Oracle', 5% rule) and under
     the selector.  Per n: how often the selector's CD equals the best CD, and
-    the geomean of best-CD time over selector time (1.0 = as fast)."""
+    the geomean of best-CD time over selector time (1.0 = as fast).
+    Sec. 6.4: the same sets in default mode (every GEMM on its own stream,
+    isolated kernels) and in sequential mode (one stream, isolated kernels);
+    the shares of sets the selector and GO make faster than each by more than
+    BENEFIT_BAND, leave within it, or make slower by more than it.  Default's
+    times include its per-stream fork/join on the host, which for sets of
+    short GEMMs is most of its step."""
     import torch
     from paper_2409_02227_amd import gdy, inputs
     table = args.table if args.table and os.path.exists(args.table) else None
     ctx = gdy.Context(0, table=table, max_streams=16)
     handle = gdy._stream_handle(None)
     shapes, seen = [], set()
-    for sub in inputs.config4(seed=46, count=40):
+    if args.accuracy_set == "tuned":
+        # the table's own bf16 NN shapes (M = 2^ceil(log2 M) of the entry)
+        tuned = []
+        for line in open(table):
+            tok = line.split()
+            if tok and tok[0] == "entry" and tok[1:4] == ["2", "0", "0"] and tok[7] == "1":
+                tuned.append((1 << int(tok[4]), int(tok[5]), int(tok[6])))
+        order = np.random.default_rng(46).permutation(len(tuned))
+        shapes = [tuned[i] for i in order[:args.accuracy_shapes]]
+    for sub in inputs.config4(seed=46, count=40) if args.accuracy_set == "untuned" else []:
         for g in sub:
             key = (g.m, g.n, g.k)
             if key not in seen and len(shapes) < args.accuracy_shapes:
@@ -432,8 +451,12 @@ def accuracy_bench(args, desc):
                 shapes.append(key)
     gen = torch.Generator(device="cuda").manual_seed(46)
     res, tot_f, tot_t = {}, 0.0, 0.0
+    vs_default = {"selector": [], "go": []}
+    vs_seq = {"selector": [], "go": []}
     for n in (2, 4, 8, 16):
         hit, rel, rel_go = [], [], []
+        sp = {"selector": [], "go": []}
+        sq = {"selector": [], "go": []}
         for (m, nn, k) in shapes:
             a = (torch.rand(n, m, k, device="cuda", generator=gen) * 2 - 1).to(torch.bfloat16)
             b = (torch.randn(n, k, nn, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
@@ -443,6 +466,12 @@ def accuracy_bench(args, desc):
             t_best, cd_best = best_cd_time(ctx, arr, n, args.steps, 2, handle, torch)
             t_sel = time_steps(ctx, arr, n, "selector", args.steps, 2, handle, torch)
             t_go = time_steps(ctx, arr, n, "go", args.steps, 2, handle, torch)
+            t_def = time_steps(ctx, arr, n, "default", args.steps, 2, handle, torch)
+            t_seq = time_steps(ctx, arr, n, "sequential", args.steps, 2, handle, torch)
+            sp["selector"].append(t_def / t_sel)
+            sp["go"].append(t_def / t_go)
+            sq["selector"].append(t_seq / t_sel)
+            sq["go"].append(t_seq / t_go)
             cd_sel = ctx.plan(gemms, mode="selector")["cd"]
             hit.append(cd_sel == cd_best)
             rel.append(t_best / t_sel)
@@ -452,17 +481,42 @@ def accuracy_bench(args, desc):
             del a, b, c, gemms, arr
         res[n] = {"accuracy": round(float(np.mean(hit)), 4),
                   "best_cd_over_selector_geomean": round(float(np.exp(np.mean(np.log(rel)))), 4),
-                  "go_over_selector_geomean": round(float(np.exp(np.mean(np.log(rel_go)))), 4)}
+                  "go_over_selector_geomean": round(float(np.exp(np.mean(np.log(rel_go)))), 4),
+                  "vs_default": {m: benefit_shares(v) for m, v in sp.items()},
+                  "vs_sequential": {m: benefit_shares(v) for m, v in sq.items()}}
+        for m in vs_default:
+            vs_default[m] += sp[m]
+            vs_seq[m] += sq[m]
+        print(f"selector_accuracy: {len(shapes)} sets of {n} GEMMs timed", file=sys.stderr, flush=True)
     value = tot_f / tot_t / 1e12
     out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
            "steps": args.steps, "warmup": 2, "ms_per_step": round(1e3 * tot_t / (4 * len(shapes)), 4),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic (seeded device draws; A ~ U[-1,1], B ~ N(0, 0.02))",
            "config": {"workload": f"selector_accuracy: {desc}", "mode": "selector", "shapes": len(shapes),
+                      "shape_set": args.accuracy_set,
                       "table": os.path.relpath(table, ROOT) if table else None},
            "per_available_gemms": res,
+           "vs_default_all": {m: benefit_shares(v) for m, v in vs_default.items()},
+           "vs_sequential_all": {m: benefit_shares(v) for m, v in vs_seq.items()},
+           "benefit_band": BENEFIT_BAND,
            "pct_mfma_peak": round(100 * value / PEAK_TFLOPS["bf16"], 2)}
     print(json.dumps(out), flush=True)
+
+
+BENEFIT_BAND = 0.05  # speedups within 5% of 1 count as unchanged (the 5% of Sec. 5.5's Oracle rule)
+
+
+def benefit_shares(speedups) -> dict:
+    """Sec. 6.4's distribution: shares of cases improved, unchanged and
+    degraded against default (speedup = default time / mode time), plus the
+    geomean and the extremes."""
+    v = np.array(speedups, dtype=float)
+    return {"cases": int(v.size), "improved": round(float(np.mean(v > 1 + BENEFIT_BAND)), 4),
+            "unchanged": round(float(np.mean(np.abs(v - 1) <= BENEFIT_BAND)), 4),
+            "degraded": round(float(np.mean(v < 1 - BENEFIT_BAND)), 4),
+            "geomean": round(float(np.exp(np.mean(np.log(v)))), 4),
+            "min": round(float(v.min()), 4), "max": round(float(v.max()), 4)}
 
 
 def pairs_bench(args, desc):

@@ -44,12 +44,30 @@ def _compile(src: str) -> str:
     return obj
 
 
+CEILINGS = os.path.join(HERE, "ceilings")
+
+
+def build_ceilings() -> str:
+    """The stand-alone chip-ceiling probe (csrc/ceilings.hip) as an executable
+    next to this file; the profiling harness runs it."""
+    tmp = CEILINGS + ".tmp"
+    cmd = [_hipcc(), *[f for f in FLAGS if f != "-fPIC"], os.path.join(CSRC, "ceilings.hip"), "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for ceilings.hip:\n{r.stderr}")
+    os.replace(tmp, CEILINGS)
+    return CEILINGS
+
+
 def build(jobs: int | None = None) -> str:
-    """Compile every source and link libgdy.so (always rebuilds)."""
+    """Compile every source and link libgdy.so (always rebuilds), and build
+    the ceiling probe."""
     os.makedirs(BUILD, exist_ok=True)
     jobs = jobs or min(len(SOURCES), os.cpu_count() or 1)
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
+        probe = ex.submit(build_ceilings)
         objs = list(ex.map(_compile, SOURCES))
+        probe.result()
     tmp = LIB + ".tmp"
     cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -22,6 +22,7 @@ workload's dominant dispatch in the record file bench.py reports as the
 roofline's `traffic` while the kernel sources hash the same.
 
 Usage, on a GPU machine:
+  python3 -m paper_2409_02227_amd.profiling ceilings --out profiles/ceilings_gfx950.md
   python3 -m paper_2409_02227_amd.profiling trace --workload tp8_layer_share --out profiles/x.md
   python3 -m paper_2409_02227_amd.profiling collect --workload tp8_layer_share --out profiles/x.md \
       --traffic-record profiles/hbm_traffic.json
@@ -144,6 +145,7 @@ def read_trace(d: str) -> list:
                 grid = int(r.get("Grid_Size") or r.get("Grid_Size_X") or 0)
                 wg = int(r.get("Workgroup_Size") or r.get("Workgroup_Size_X") or 0)
                 out.append({"kernel": r["Kernel_Name"], "grid": grid, "wg": wg, "id": int(r["Dispatch_Id"]),
+                            "start": int(r["Start_Timestamp"]), "end": int(r["End_Timestamp"]),
                             "ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"])})
     out.sort(key=lambda r: r["id"])
     return out
@@ -240,6 +242,19 @@ def collect(args) -> None:
     print(json.dumps(res["derived"]), flush=True)
 
 
+def split_spans(rows: list, wgs: int) -> list:
+    """For each split-K GEMM dispatch with `wgs` workgroups, the time from its
+    start to the end of the first split_reduce dispatch after it (us)."""
+    out = []
+    for i, r in enumerate(rows):
+        if "go_gemm" in r["kernel"] and "true>" in r["kernel"] and r["grid"] // max(r["wg"], 1) == wgs:
+            for q in rows[i + 1:i + 64]:
+                if "split_reduce" in q["kernel"] and q["start"] >= r["end"]:
+                    out.append((q["end"] - r["start"]) / 1e3)
+                    break
+    return out
+
+
 def write_traffic_record(path: str, workload: str, res: dict, line) -> None:
     """Store the dominant dispatch's HBM bytes (FETCH_SIZE and WRITE_SIZE
     means, each scaled by the copy calibration) under the workload, the
@@ -328,6 +343,13 @@ def trace(args) -> None:
             lines.append(f"Kernel trace, the same workgroup count: {len(ds)} dispatches over every pass "
                          f"(all modes that launch it), mean {sum(ds) / len(ds):.1f} us, median "
                          f"{ds[len(ds) // 2]:.1f} us.")
+            # a split dispatch's events also cover the plane reduction that follows it
+            spans = split_spans(rows, wg)
+            if spans:
+                spans.sort()
+                lines.append(f"With the split-K reduction that follows each of them (reduction end - GEMM "
+                             f"start, what the bench's events span): {len(spans)} dispatches, mean "
+                             f"{sum(spans) / len(spans):.1f} us, median {spans[len(spans) // 2]:.1f} us.")
         lines.append(f"Bench line: value {line['value']} {line['unit']}, ms_per_step {line['ms_per_step']}.")
     if plain and "roofline" in plain:
         roof = plain["roofline"]
@@ -337,6 +359,46 @@ def trace(args) -> None:
     with open(args.out, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines[-4:]), flush=True)
+
+
+def ceilings(args) -> None:
+    """Run the chip-ceiling probe (built by build.py from csrc/ceilings.hip)
+    `args.repeat` times and write the per-probe medians: shader clock under
+    each load, LDS bytes per clock per CU, MFMA utilisation and the bf16 rate
+    that utilisation gives at that clock."""
+    exe = os.path.join(HERE, "ceilings")
+    if not os.path.exists(exe):
+        raise SystemExit(f"{exe} is missing: run the build first")
+    runs = {}
+    for rep in range(args.repeat):
+        r = subprocess.run(["timeout", "-s", "KILL", "60", exe], capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"ceilings run {rep} failed ({r.returncode}): {r.stderr[-400:]}")
+        for line in r.stdout.splitlines():
+            if line.startswith("{"):
+                d = json.loads(line)
+                runs.setdefault(d["probe"], []).append(d)
+        print(f"ceilings run {rep + 1}/{args.repeat} done", flush=True)
+    med = lambda xs: sorted(xs)[len(xs) // 2]
+    cmdline = " ".join(shlex.quote(x) for x in ["python3", "-m", "paper_2409_02227_amd.profiling", *sys.argv[1:]])
+    lines = ["# Chip ceilings measured on the device", "", "Command (on the GPU box, from the repository root):", "",
+             f"    {cmdline}", "",
+             f"which runs `paper_2409_02227_amd/ceilings` (built from `csrc/ceilings.hip`) {args.repeat} times; "
+             "medians over the runs.  One block per CU (128 KiB of LDS each), no global traffic in the timed "
+             "loops; the clock is shader cycles (s_memtime) over the wall time of the launch.", "",
+             "| probe | what it runs | clock GHz | LDS B/clk/CU | MFMA util | bf16 TFLOP/s at that clock |",
+             "|---|---|---|---|---|---|"]
+    what = {"mfma": "1 wave/SIMD, independent 32x32x16 bf16 MFMAs",
+            "lds": "8 waves/CU of conflict-free ds_read_b128",
+            "mix_w2x4": "8 waves of 128x64: 8 MFMAs + 6 KiB of reads per wave per K step",
+            "mix_w2x2": "4 waves of 128x128: 16 MFMAs + 8 KiB of reads per wave per K step"}
+    for name, rs in runs.items():
+        lines.append(f"| {name} | {what.get(name, '')} | {med([r['clock_ghz'] for r in rs]):.3f} | "
+                     f"{med([r['lds_bytes_per_clk_cu'] for r in rs]):.1f} | {med([r['mfma_util'] for r in rs]):.4f} | "
+                     f"{med([r['bf16_tflops_at_clock'] for r in rs]):.1f} |")
+    with open(args.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines[-len(runs):]), flush=True)
 
 
 def derived(v: dict, cal: dict) -> dict:
@@ -450,6 +512,9 @@ def main():
     t.add_argument("--out", required=True)
     t.add_argument("--timeout", type=int, default=240)
     t.add_argument("--keep-raw", action="store_true")
+    e = sub.add_parser("ceilings")
+    e.add_argument("--repeat", type=int, default=5)
+    e.add_argument("--out", required=True)
     r = sub.add_parser("run-gemm")
     r.add_argument("spec")
     r.add_argument("kernel")
@@ -460,6 +525,8 @@ def main():
         return run_gemm(args.spec, args.kernel, args.reps, args.dtype)
     if args.cmd == "trace":
         return trace(args)
+    if args.cmd == "ceilings":
+        return ceilings(args)
     if bool(args.workload) == bool(args.gemm):
         raise SystemExit("give one of --workload or --gemm")
     if args.traffic_record and not args.workload:

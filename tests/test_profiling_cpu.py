@@ -85,3 +85,15 @@ def test_traffic_record_replaces_and_matches_bench(tmp_path, monkeypatch):
     assert bench.recorded_traffic("w", "k", [[512, 6144, 6144]]) is None
     with pytest.raises(RuntimeError):
         profiling.write_traffic_record(str(path), "w", dict(res, counters={"FETCH_SIZE": 1.0}), line)
+
+
+def test_split_spans_pair_each_split_dispatch_with_its_reduction():
+    def row(i, name, wgs, start, end):
+        return {"kernel": name, "grid": wgs * 256, "wg": 256, "id": i, "start": start, "end": end, "ns": end - start}
+    main = "gdy::go_gemm_d<3, 0, 0, 128, 128, 2, 2, 2, 128, true>"
+    rows = [row(1, main, 3584, 0, 240_000), row(2, "gdy::split_reduce<2>", 64, 241_000, 262_000),
+            row(3, "gdy::go_gemm_d<3, 0, 0, 128, 128, 2, 2, 2, 128, false>", 3584, 300_000, 500_000),
+            row(4, main, 3584, 600_000, 840_000), row(5, "other", 1, 841_000, 842_000),
+            row(6, "gdy::split_reduce<2>", 64, 843_000, 860_000)]
+    assert profiling.split_spans(rows, 3584) == [262.0, 260.0]
+    assert profiling.split_spans(rows, 512) == []
