@@ -387,6 +387,9 @@ def het_summary(r) -> dict:
     return {"submissions": len(seq), "gemms": int(sum(r["gemms"])),
             "geomean_speedup_vs_sequential": {m: gm(r[m]) for m in ("selector", "go", "best_cd")},
             "selector_speedup_min_max": [round(float(sp.min()), 3), round(float(sp.max()), 3)],
+            # Sec. 6.4's distribution over the submissions, and the ones the selector slows down
+            "selector_vs_sequential": benefit_shares(sp),
+            "degraded_submissions": [int(i) for i in np.nonzero(sp < 1 - BENEFIT_BAND)[0]],
             "selector_over_go_geomean": round(float(np.exp(np.mean(np.log(np.array(r["go"]) / sel)))), 4),
             "selector_over_best_cd_geomean": round(float(np.exp(np.mean(np.log(np.array(r["best_cd"]) / sel)))), 4),
             "best_cd_chosen": {str(c): int(np.sum(np.array(r["best_cd_of"]) == c))
