@@ -9,6 +9,8 @@ columns whose offsets are largest (the last rows and columns), plus a seeded
 sample of the rest, on direct and register-staged kernels.  One element past
 the limit is refused before anything launches.
 """
+import os
+
 import numpy as np
 import pytest
 
@@ -33,11 +35,15 @@ def max_rows(ld, es=2):
     return (LIMIT - 1025) // (ld * es) - 256
 
 
+TABLE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                     "paper_2409_02227_amd", "tables", "gfx950.table")
+
+
 @pytest.fixture(scope="module")
 def lctx():
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
-    c = gdy.Context(0, max_streams=16)
+    c = gdy.Context(0, table=TABLE if os.path.exists(TABLE) else None, max_streams=16)
     yield c
     c.close()
 
@@ -199,3 +205,27 @@ def test_one_row_past_the_limit_is_refused(lctx):
         with pytest.raises(gdy.GdyError, match="extent"):
             lctx.execute([d], mode="sequential")
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("mode", ["sequential", "default", "go", "selector"])
+def test_largest_submission(lctx, mode):
+    """GDY_MAX_GEMMS = 256 independent GEMMs in one submission (seeded ragged
+    shapes, M, N, K in [1, 300], padded leading dimensions for a quarter of
+    them): every element of every output within the oracle's bound, C's
+    padding and guard rows untouched; 257 are refused."""
+    from tests.gpu_helpers import check, gemm_of
+    rng = np.random.default_rng(256)
+    specs = [inputs.GemmSpec(int(rng.integers(1, 301)), int(rng.integers(1, 301)), int(rng.integers(1, 301)),
+                             "bf16", seed=12000 + i, name=f"s{i}",
+                             pad_a=int(rng.integers(0, 9)) if i % 4 == 0 else 0,
+                             pad_c=int(rng.integers(0, 9)) if i % 4 == 1 else 0)
+             for i in range(gdy.MAX_GEMMS)]
+    mats = [inputs.materialize(s) for s in specs]
+    plan = lctx.execute([gemm_of(m) for m in mats], mode=mode, want_plan=True)
+    torch.cuda.synchronize()
+    assert sum(1 for v in plan["variant_of"][:gdy.MAX_GEMMS] if v >= 0) == gdy.MAX_GEMMS
+    for m in mats:
+        check(m, label=f"{mode} 256")
+    print(f"{mode}: {plan['n_groups']} groups, {plan['n_dispatches']} dispatches", flush=True)
+    with pytest.raises(gdy.GdyError):
+        lctx.execute([gemm_of(m) for m in mats] + [gemm_of(mats[0])], mode=mode)
