@@ -52,16 +52,61 @@ def check(mat, rng=None, samples=8, label=""):
         cols = rng.choice(s.n, size=min(samples, s.n), replace=False)
         if s.m <= 32:
             rows = np.arange(s.m)
-        ii = np.concatenate([np.repeat(rows, s.n), np.tile(np.arange(s.m), len(cols))])
-        jj = np.concatenate([np.tile(np.arange(s.n), len(rows)), np.repeat(cols, s.m)])
-        ref, bound = oracle.gemm_entries(s.m, s.n, s.k, mat.host["a"], dt, s.ld("a"),
-                                         mat.host["b"], dt, s.ld("b"), ii, jj, s.trans_a,
-                                         s.trans_b, mat.scale_a, mat.scale_b)
-        ok, worst = oracle.accept(got[ii, jj], ref, bound, TAU[s.dtype])
+        ok, worst = accept_rows_cols(got[rows], got[:, cols], s.m, s.n, s.k, mat.host["a"], dt, s.ld("a"),
+                                     mat.host["b"], dt, s.ld("b"), rows, cols, TAU[s.dtype], s.trans_a,
+                                     s.trans_b, mat.scale_a, mat.scale_b)
     assert ok, f"{label} {s.name} ({s.m},{s.n},{s.k},{s.dtype},t{s.trans_a}{s.trans_b}): " \
                f"outside bound, worst ratio {worst:.3g}"
     assert_untouched(mat, label)
     return worst
+
+
+def rows_cols_ref(m, n, k, a, a_dt, lda, b, b_dt, ldb, rows, cols, ta=0, tb=0, sa=1.0, sb=1.0):
+    """Oracle values and bounds of the full rows `rows` (len(rows) x n) and
+    the full columns `cols` (m x len(cols)) of C = op(A) op(B).  Each part is
+    the oracle's own GEMM over a copy of the stored rows or columns of A or B
+    those outputs read (the codes are copied, not changed: every element is
+    still the oracle's k-ascending sum), which streams the operands instead
+    of walking a column of B per output."""
+    rows = np.asarray(rows, dtype=np.int64)
+    cols = np.asarray(cols, dtype=np.int64)
+    a2 = np.asarray(a).reshape(-1)
+    b2 = np.asarray(b).reshape(-1)
+    a_st, b_st = _stored(a2, lda), _stored(b2, ldb)
+    if ta == 0:  # op(A) row i is stored row i
+        ar, lda_r = a_st[rows, :k], k
+    else:        # op(A) row i is stored column i of a K x M operand
+        ar, lda_r = a_st[:k, rows], len(rows)
+    if tb == 0:  # op(B) column j is stored column j of a K x N operand
+        bc, ldb_c = b_st[:k, cols], len(cols)
+    else:        # op(B) column j is stored row j
+        bc, ldb_c = b_st[cols, :k], k
+    ref_r, bd_r = oracle.gemm(len(rows), n, k, np.ascontiguousarray(ar).reshape(-1), a_dt, lda_r, b2, b_dt, ldb,
+                              ta, tb, sa, sb)
+    ref_c, bd_c = oracle.gemm(m, len(cols), k, a2, a_dt, lda, np.ascontiguousarray(bc).reshape(-1), b_dt, ldb_c,
+                              ta, tb, sa, sb)
+    return ref_r, bd_r, ref_c, bd_c
+
+
+def _stored(flat, ld):
+    """A flat operand as its stored rows of ld elements (a last partial row,
+    as a minimal extent ends, is completed with zero codes that no index
+    below reaches)."""
+    if flat.size % ld:
+        full = np.zeros(-(-flat.size // ld) * ld, dtype=flat.dtype)
+        full[:flat.size] = flat
+        flat = full
+    return flat.reshape(-1, ld)
+
+
+def accept_rows_cols(got_rows, got_cols, m, n, k, a, a_dt, lda, b, b_dt, ldb, rows, cols, tau, ta=0, tb=0,
+                     sa=1.0, sb=1.0):
+    """oracle.accept over full rows (got_rows: len(rows) x n decoded values)
+    and full columns (got_cols: m x len(cols)) of a result."""
+    ref_r, bd_r, ref_c, bd_c = rows_cols_ref(m, n, k, a, a_dt, lda, b, b_dt, ldb, rows, cols, ta, tb, sa, sb)
+    ok_r, w_r = oracle.accept(got_rows, ref_r, bd_r, tau)
+    ok_c, w_c = oracle.accept(got_cols, ref_c, bd_c, tau)
+    return ok_r and ok_c, max(w_r, w_c)
 
 
 def assert_untouched(mat, label=""):

@@ -8,8 +8,11 @@ tau = 2^-7 for bf16, 2^-3 for fp8):
   * the two fp8 tenants under the selector and GO: every element of the
     GEMMs with M <= 256, 16 full rows and 16 full columns of the M = 2048 ones;
   * all 200 heterogeneous submissions the bench times (its device operand
-    pools and windows) under the selector: 8 full rows and 8 full columns of
-    every GEMM, every element of GEMMs with M <= 32.
+    pools and windows) under the selector: 16 full rows and 16 full columns
+    of every GEMM, every element of GEMMs with M <= 32.
+
+Sampled rows and columns are checked against the oracle's full GEMM over the
+stored rows of A and columns of B they read (tests.gpu_helpers.rows_cols_ref).
 """
 import os
 
@@ -22,7 +25,8 @@ torch = pytest.importorskip("torch")
 
 import oracle  # noqa: E402
 from paper_2409_02227_amd import gdy, inputs  # noqa: E402
-from tests.gpu_helpers import ORC, TAU, assert_untouched, decode_out, gemm_of, out_codes, reset_outputs  # noqa: E402
+from tests.gpu_helpers import (ORC, TAU, accept_rows_cols, assert_untouched, decode_out, gemm_of,  # noqa: E402
+                               out_codes, reset_outputs)
 
 pytestmark = pytest.mark.gpu
 TABLE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
@@ -45,12 +49,10 @@ def _full_ref(mat):
 
 
 def _sample(m, n, rows, cols, rng):
-    """Row and column indices: `rows` full rows (all when m <= 32) and `cols` full columns."""
+    """`rows` full rows (all when m <= 32) and `cols` full columns to check."""
     r = np.arange(m) if m <= 32 else rng.choice(m, size=min(rows, m), replace=False)
     c = rng.choice(n, size=min(cols, n), replace=False)
-    ii = np.concatenate([np.repeat(r, n), np.tile(np.arange(m), len(c))])
-    jj = np.concatenate([np.tile(np.arange(n), len(r)), np.repeat(c, m)])
-    return ii, jj
+    return r, c
 
 
 def test_layer_share_every_element_every_mode(wctx):
@@ -87,11 +89,10 @@ def test_fp8_tenants(wctx, mode):
             ref, bound = _full_ref(m)
             ok, worst = oracle.accept(got, ref, bound, TAU["fp8"])
         else:
-            ii, jj = _sample(s.m, s.n, 16, 16, rng)
-            ref, bound = oracle.gemm_entries(s.m, s.n, s.k, m.host["a"], "e4m3fn", s.ld("a"), m.host["b"],
-                                             "e4m3fn", s.ld("b"), ii, jj, s.trans_a, s.trans_b,
-                                             m.scale_a, m.scale_b)
-            ok, worst = oracle.accept(got[ii, jj], ref, bound, TAU["fp8"])
+            rows, cols = _sample(s.m, s.n, 16, 16, rng)
+            ok, worst = accept_rows_cols(got[rows], got[:, cols], s.m, s.n, s.k, m.host["a"], "e4m3fn",
+                                         s.ld("a"), m.host["b"], "e4m3fn", s.ld("b"), rows, cols, TAU["fp8"],
+                                         s.trans_a, s.trans_b, m.scale_a, m.scale_b)
         assert ok, f"{mode} {s.name} ({s.m},{s.n},{s.k}): worst ratio {worst:.3g}"
         assert_untouched(m, mode)
 
@@ -121,12 +122,13 @@ def test_heterogeneous_submissions_all_200(wctx, het_pools, chunk):
         wctx.execute(gemms, mode="selector")
         torch.cuda.synchronize()
         for (g, oa, ob), c in zip(placed[s_idx], outs):
-            ii, jj = _sample(g.m, g.n, 8, 8, rng)
-            sel = c.view(torch.int16)[torch.from_numpy(ii).cuda(), torch.from_numpy(jj).cuda()]
-            got = oracle.decode(sel.cpu().numpy().view(np.uint16), "bf16")
-            ref, bound = oracle.gemm_entries(g.m, g.n, g.k, a_host[oa:oa + g.m * g.k], "bf16", g.k,
-                                             b_host[ob:ob + g.k * g.n], "bf16", g.n, ii, jj)
-            ok, worst = oracle.accept(got, ref, bound, TAU["bf16"])
+            rows, cols = _sample(g.m, g.n, 16, 16, rng)
+            # only the checked rows and columns come back to the host
+            c16 = c.view(torch.int16)
+            got_r = oracle.decode(c16[torch.from_numpy(rows).cuda()].cpu().numpy().view(np.uint16), "bf16")
+            got_c = oracle.decode(c16[:, torch.from_numpy(cols).cuda()].cpu().numpy().view(np.uint16), "bf16")
+            ok, worst = accept_rows_cols(got_r, got_c, g.m, g.n, g.k, a_host[oa:oa + g.m * g.k], "bf16", g.k,
+                                         b_host[ob:ob + g.k * g.n], "bf16", g.n, rows, cols, TAU["bf16"])
             assert ok, f"submission {s_idx} ({g.m},{g.n},{g.k}): worst ratio {worst:.3g}"
         assert all(torch.isnan(gd.float()).all().item() for gd in guards), f"submission {s_idx}: wrote past C"
     print(f"submissions {20 * chunk}-{20 * chunk + 19}: sampled rows and columns within the bound", flush=True)
