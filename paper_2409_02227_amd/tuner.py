@@ -48,6 +48,7 @@ RCS = (0, 128, 64, 32)  # whole GPU, then CU-masked budgets
 DT_CODE = {"f16": 1, "bf16": 2, "fp8": 3, "f32": 4}
 BEST_CD_GAIN = 1.05     # Sec. 5.5: sequential unless a CD gives >= 5%
 LABEL_TOL = 0.03        # CDs within 3% of the best speedup count as equally good
+KERNEL_TOL = 0.0        # CD-step kernels within this fraction of the fastest count as ties (0: fastest)
 MIN_TYPE_RECORDS = 20   # an input type gets its own predictor from this many tuned shapes
 KNN_K = 3               # neighbours of the preferred-RC vote (Sec. 7.5)
 
@@ -243,8 +244,10 @@ def tune_shape(ctx, bench, torch, variants, shape, rounds=3):
         n_g = cd * rounds
         t_seq = bench.time(submission(ops, cd, rounds, best_iso, ta, tb), "forced", 1) / n_g
         best, best_t = None, None
+        rec.setdefault("conc_all", {})[str(cd)] = {}
         for vid in pool:
             t = bench.time(submission(ops, cd, rounds, vid, ta, tb), "forced_grouped", cd) / n_g
+            rec["conc_all"][str(cd)][variants[vid]["name"]] = t
             if best_t is None or t < best_t:
                 best, best_t = vid, t
         rec["seq"][str(cd)] = t_seq
@@ -269,6 +272,52 @@ def _lr_lines(lr) -> list:
             "lr_b " + " ".join(repr(float(x)) for x in lr["b"])]
 
 
+def kernel_of(name: str) -> str:
+    """A variant's kernel (its name without the grid cap): the GEMMs of a
+    group that bind variants of one kernel run as one fused dispatch."""
+    return name.rsplit("_c", 1)[0]
+
+
+def consistent_go(records, tol: float) -> dict:
+    """CD-step kernels with ties broken toward agreement.  For each input
+    type, layout and CD, a shape's acceptable kernels are those whose fastest
+    variant is within `tol` of the shape's fastest time; each shape takes the
+    acceptable kernel that the most shapes of its kind find acceptable (ties:
+    the faster one), with that kernel's fastest variant.  A mixed group then
+    more often binds one kernel and runs as one dispatch instead of several
+    forked ones.  Returns {record index: {cd: variant name}}; records without
+    per-candidate times keep their fastest kernels."""
+    out = {}
+    for i, r in enumerate(records):
+        out[i] = {str(cd): r["go"][str(cd)] for cd in CDS}
+    if tol <= 0:
+        return out
+    for cd in CDS[1:]:
+        groups = {}
+        for i, r in enumerate(records):
+            if str(cd) in r.get("conc_all", {}):
+                key = (r["shape"][0], r["shape"][1], r["shape"][2])
+                groups.setdefault(key, []).append(i)
+        for idx in groups.values():
+            ok, votes = {}, {}
+            for i in idx:
+                times = records[i]["conc_all"][str(cd)]
+                best = min(times.values())
+                per_kernel = {}
+                for name, t in times.items():
+                    k = kernel_of(name)
+                    if k not in per_kernel or t < times[per_kernel[k]]:
+                        per_kernel[k] = name
+                ok[i] = {k: nm for k, nm in per_kernel.items() if times[nm] <= best * (1.0 + tol)}
+                for k in ok[i]:
+                    votes[k] = votes.get(k, 0) + 1
+            for i in idx:
+                times = records[i]["conc_all"][str(cd)]
+                k = max(sorted(ok[i]), key=lambda k: (votes[k], -times[ok[i][k]]))
+                out[i][str(cd)] = ok[i][k]
+    return out
+
+
 def write_table(path, ctx, records, lr=None, lr_by_type=None):
     """GO table: header, the shared predictor, one predictor block per input
     type that has its own ("lr_dtype <code>" then its four lines), entries."""
@@ -281,10 +330,11 @@ def write_table(path, ctx, records, lr=None, lr_by_type=None):
     for code, model in sorted((lr_by_type or {}).items()):
         lines.append(f"lr_dtype {int(code)}")
         lines += _lr_lines(model)
-    for r in records:
+    go = consistent_go(records, KERNEL_TOL)
+    for i, r in enumerate(records):
         dtype, ta, tb, m, n, k = r["shape"][:6]
         mlog = max(0, math.ceil(math.log2(max(m, 1))))
-        names = [r["go"][str(cd)] for cd in CDS]
+        names = [go[i][str(cd)] for cd in CDS]
         # the best kernel under each resource constraint: the kernels of the
         # CU-Partition modes (a partition of 2, 4, 8 holds 128, 64, 32 CUs)
         rc = r.get("rc_best", {})
@@ -519,11 +569,16 @@ def main(argv=None):
     ap.add_argument("--knn-seed", type=int, default=0)
     ap.add_argument("--label-tol", type=float, default=None,
                     help=f"speedups within this fraction of the best count as ties (default {LABEL_TOL})")
+    ap.add_argument("--kernel-tol", type=float, default=None,
+                    help="CD-step kernels within this fraction of the fastest count as ties, broken toward "
+                         f"the kernel most shapes of the kind accept (default {KERNEL_TOL}: the fastest)")
     ap.add_argument("--max-seconds", type=float, default=0.0,
                     help="start no new shape after this many seconds (resume later from --records)")
     args = ap.parse_args(argv)
     if args.label_tol is not None:
         globals()["LABEL_TOL"] = args.label_tol  # label_of's default
+    if args.kernel_tol is not None:
+        globals()["KERNEL_TOL"] = args.kernel_tol  # write_table's
 
     import torch
     from paper_2409_02227_amd import gdy

@@ -118,3 +118,31 @@ def test_shape_sets():
         assert n in (512, 1024, 2048, 4096, 8192, 16384) and k in (512, 1024, 2048, 4096, 8192, 16384)
         assert m * n <= 168 * 2 ** 20 and m * n * k <= 8192 ** 3
     assert tuner.shape_set("large") == large  # seeded
+
+
+def test_consistent_go_breaks_ties_toward_agreement():
+    """Three bf16 NN shapes at CD 2.  Hand-worked with tol 3%:
+      s0: A 100, B 102, C 110 -> acceptable {A, B}
+      s1: A 100, B 101        -> acceptable {A, B}
+      s2: B 100, A 104        -> acceptable {B} (A is 4% slower)
+    votes: A 2, B 3 -> every shape takes B (s0 and s1 trade up to 2% for it);
+    tol 0 keeps each shape's fastest (A, A, B).  Grid-capped variants of one
+    kernel count as one kernel and the faster variant is written."""
+    from paper_2409_02227_amd import tuner
+
+    def rec(times):
+        go = {"1": "bf16_nn_iso_c0"}
+        go.update({str(cd): min(times, key=times.get) for cd in tuner.CDS[1:]})
+        return {"shape": ["bf16", 0, 0, 64, 1024, 1024], "go": go,
+                "conc_all": {str(cd): dict(times) for cd in tuner.CDS[1:]}}
+    recs = [rec({"bf16_A_c0": 100.0, "bf16_B_c0": 103.0, "bf16_B_c64": 102.0, "bf16_C_c0": 110.0}),
+            rec({"bf16_A_c0": 100.0, "bf16_B_c0": 101.0}),
+            rec({"bf16_B_c0": 100.0, "bf16_A_c0": 104.0})]
+    got = tuner.consistent_go(recs, 0.03)
+    assert [got[i]["2"] for i in range(3)] == ["bf16_B_c64", "bf16_B_c0", "bf16_B_c0"]
+    assert all(got[i]["1"] == "bf16_nn_iso_c0" for i in range(3))  # the isolated kernel is untouched
+    got0 = tuner.consistent_go(recs, 0.0)
+    assert [got0[i]["2"] for i in range(3)] == ["bf16_A_c0", "bf16_A_c0", "bf16_B_c0"]
+    # a record without per-candidate times keeps its own kernels
+    plain = {"shape": ["bf16", 0, 0, 64, 2048, 1024], "go": {str(cd): "bf16_X_c0" for cd in tuner.CDS}}
+    assert tuner.consistent_go(recs + [plain], 0.03)[3]["2"] == "bf16_X_c0"
