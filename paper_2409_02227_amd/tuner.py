@@ -330,7 +330,21 @@ def write_table(path, ctx, records, lr=None, lr_by_type=None):
     for code, model in sorted((lr_by_type or {}).items()):
         lines.append(f"lr_dtype {int(code)}")
         lines += _lr_lines(model)
+    lines += entry_lines(records)
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def entry_key(line: str) -> tuple:
+    """(dtype, ta, tb, ceil(log2 M), N, K, items) of an entry line."""
+    return tuple(int(x) for x in line.split()[1:8])
+
+
+def entry_lines(records) -> list:
+    """One "entry" line per record: the shape key, then the GO-Kernel of each
+    CD class and, when tuned, the best kernel under each CU budget."""
     go = consistent_go(records, KERNEL_TOL)
+    out = []
     for i, r in enumerate(records):
         dtype, ta, tb, m, n, k = r["shape"][:6]
         mlog = max(0, math.ceil(math.log2(max(m, 1))))
@@ -341,9 +355,25 @@ def write_table(path, ctx, records, lr=None, lr_by_type=None):
         if all(str(b) in rc for b in RCS[1:]):
             names += [rc[str(b)][0] for b in RCS[1:]]
         items = r["shape"][6] if len(r["shape"]) > 6 and r["shape"][6] > 0 else 1  # B-GEMM items
-        lines.append(f"entry {DT_CODE[dtype]} {ta} {tb} {mlog} {n} {k} {items} " + " ".join(names))
+        out.append(f"entry {DT_CODE[dtype]} {ta} {tb} {mlog} {n} {k} {items} " + " ".join(names))
+    return out
+
+
+def extend_table(base: str, records, path: str) -> int:
+    """A table with everything of `base` (header, predictors, entries) plus
+    an entry for each record whose shape key `base` has no entry for; the
+    predictors are not retrained.  Returns the number of entries added."""
+    lines = open(base).read().rstrip("\n").split("\n")
+    have = {entry_key(l) for l in lines if l.startswith("entry ")}
+    added = []
+    for line in entry_lines(records):
+        key = entry_key(line)
+        if key not in have:
+            have.add(key)
+            added.append(line)
     with open(path, "w") as f:
-        f.write("\n".join(lines) + "\n")
+        f.write("\n".join(lines + added) + "\n")
+    return len(added)
 
 
 def feature_rows(ctx, records):
@@ -572,6 +602,9 @@ def main(argv=None):
     ap.add_argument("--kernel-tol", type=float, default=None,
                     help="CD-step kernels within this fraction of the fastest count as ties, broken toward "
                          f"the kernel most shapes of the kind accept (default {KERNEL_TOL}: the fastest)")
+    ap.add_argument("--extend", default=None,
+                    help="no timing: write --out as this table plus entries for the --records shapes it "
+                         "lacks (its predictors kept)")
     ap.add_argument("--max-seconds", type=float, default=0.0,
                     help="start no new shape after this many seconds (resume later from --records)")
     args = ap.parse_args(argv)
@@ -580,6 +613,12 @@ def main(argv=None):
     if args.kernel_tol is not None:
         globals()["KERNEL_TOL"] = args.kernel_tol  # write_table's
 
+    if args.extend:
+        if not args.records:
+            raise SystemExit("--extend needs --records")
+        recs = [json.loads(line) for line in open(args.records)]
+        print(f"{extend_table(args.extend, recs, args.out)} entries added", flush=True)
+        return
     import torch
     from paper_2409_02227_amd import gdy
     ctx = gdy.Context(0, max_streams=16, use_cu_masks=gdy.RC_STREAMS)
