@@ -335,6 +335,14 @@ def write_table(path, ctx, records, lr=None, lr_by_type=None):
         f.write("\n".join(lines) + "\n")
 
 
+def open_records(path: str):
+    """A records file (JSONL, or gzip-compressed JSONL ending in .gz) as text lines."""
+    if path.endswith(".gz"):
+        import gzip
+        return gzip.open(path, "rt")
+    return open(path)
+
+
 def entry_key(line: str) -> tuple:
     """(dtype, ta, tb, ceil(log2 M), N, K, items) of an entry line."""
     return tuple(int(x) for x in line.split()[1:8])
@@ -613,10 +621,12 @@ def main(argv=None):
     if args.kernel_tol is not None:
         globals()["KERNEL_TOL"] = args.kernel_tol  # write_table's
 
+    if args.records and args.records.endswith(".gz") and not (args.retrain or args.knn or args.extend):
+        raise SystemExit("compressed records are read only: tune into a .jsonl file")
     if args.extend:
         if not args.records:
             raise SystemExit("--extend needs --records")
-        recs = [json.loads(line) for line in open(args.records)]
+        recs = [json.loads(line) for line in open_records(args.records)]
         print(f"{extend_table(args.extend, recs, args.out)} entries added", flush=True)
         return
     import torch
@@ -626,7 +636,7 @@ def main(argv=None):
     bench = Bench(ctx, torch)
     records, done = [], set()
     if args.records and os.path.exists(args.records):
-        for line in open(args.records):
+        for line in open_records(args.records):
             r = json.loads(line)
             records.append(r)
             done.add(tuple(r["shape"]))
