@@ -57,7 +57,7 @@ KNN_K = 3               # neighbours of the preferred-RC vote (Sec. 7.5)
 # tuning shape sets
 # ---------------------------------------------------------------------------
 
-LARGE_SET = 1072  # the paper's tuning set size (Sec. 5.4)
+LARGE_SET = 1072  # the paper's tuning set size (Sec. 4.3, Sec. 5.2)
 
 
 def shape_set(kind: str) -> list:
@@ -95,7 +95,7 @@ def shape_set(kind: str) -> list:
     if kind == "large":
         shapes = shape_set("full")
         # the paper tunes 1072 GEMMs over outputs of 32K-168M elements and K up
-        # to 20K (Sec. 5.4); draw bf16 shapes to that count: M log-uniform in
+        # to 20K (Sec. 4.3, Sec. 5.2); draw bf16 shapes to that count: M log-uniform in
         # [1, 8192], N and K from 512 to 16384, outputs at most 168M elements
         # and at most 2 * 8192^3 flops (a bound on tuning time)
         rng = np.random.default_rng(2409)
