@@ -348,15 +348,23 @@ void uncap_mixed_group(const gdy_ctx* ctx, const gdy_gemm* g, const std::vector<
 // geomeans of 2.02, 2.06 and 2.07 over sequential), every GEMM is rebound to
 // the one kernel that all of them can run at the least estimated cost,
 // uncapped: one dispatch, no fork.  The candidates are the kernels the group
-// binds, then each member's isolated kernel (first listed wins a tie): a
+// binds, then each member's isolated kernel: a
 // group bound only to small-tile kernels tuned for its skinny members would
 // otherwise put its large members on them too.  The estimate extends the isolated
 // heuristic's tile model over the group: a work item (a tile, or one K run
 // of it when the GEMM splits) costs max(tile area / 128, tile perimeter) per
 // K plus its area once (the stores, which dominate at small K); the group
 // takes the larger of its items packed into CUs x occupancy slots and its
-// longest item; direct kernels count 1.5x faster.
+// longest item; direct kernels count 1.5x faster.  The model cannot tell
+// kernels of one tile apart and misjudges tiles run two to a CU, so among
+// the candidates within kUnifyTie of the cheapest estimate the group takes
+// the kernel its GEMMs were bound to for the most flops (the tuned choice of
+// its heaviest members): on the layer share under a table whose QKV,
+// out-projection and FFN shapes bind three kernels, the estimates of the
+// 128 x 128 and the 256 x 256 kernels differ by 1%, and the flops rule picks
+// the latter, which runs the set 1.18x faster.
 const double kUnifyUs = 100.0;
+const double kUnifyTie = 0.05;
 double roofline_s(const gdy_gemm& g);
 int split_for(const gdy_ctx* ctx, int vid, const gdy_gemm& g);
 bool active(const gdy_gemm& g);
@@ -397,7 +405,7 @@ void unify_short_group(const gdy_ctx* ctx, const gdy_gemm* g, const std::vector<
     const int v = ctx->variants[iso].uncapped;
     if (std::find(cand.begin(), cand.end(), v) == cand.end()) cand.push_back(v);
   }
-  int best = -1;
+  std::vector<std::pair<int, double>> runnable_cost;
   double best_f = 0.0;
   for (int v : cand) {
     bool ok = true;
@@ -405,12 +413,26 @@ void unify_short_group(const gdy_ctx* ctx, const gdy_gemm* g, const std::vector<
       if (g[i].op != GDY_OP_ADD && (!variant_fits(ctx, v, g[i]) || !direct_ok(ctx, v, g[i]))) ok = false;
     if (!ok) continue;
     const double f = group_cost(ctx, v, g, grp);
-    if (best < 0 || f < best_f) {
-      best = v;
-      best_f = f;
+    if (runnable_cost.empty() || f < best_f) best_f = f;
+    runnable_cost.emplace_back(v, f);
+  }
+  if (runnable_cost.empty()) return;
+  // within kUnifyTie of the cheapest estimate, the kernel the group's GEMMs
+  // bound for the most flops
+  int best = -1;
+  double best_bound = -1.0, best_cost = 0.0;
+  for (const auto& vc : runnable_cost) {
+    if (vc.second > best_f * (1.0 + kUnifyTie)) continue;
+    double bound = 0.0;
+    for (int i : grp)
+      if (g[i].op != GDY_OP_ADD && ctx->variants[p->variant_of[i]].uncapped == vc.first)
+        bound += 2.0 * (double)g[i].m * (double)g[i].n * (double)g[i].k * (double)std::max(g[i].batch, 1);
+    if (best < 0 || bound > best_bound || (bound == best_bound && vc.second < best_cost)) {
+      best = vc.first;
+      best_bound = bound;
+      best_cost = vc.second;
     }
   }
-  if (best < 0) return;
   for (int i : grp)
     if (g[i].op != GDY_OP_ADD) p->variant_of[i] = best;
 }

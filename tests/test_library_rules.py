@@ -279,12 +279,14 @@ def test_short_group_threshold(tmp_path, ctx):
     #         Y 256 x (3072 x 512 + 65536) = 973,078,528 / 256 slots = 3,801,088
     #   K128: per 256, area 16384; X 1024 x (4096 x 256 + 16384) +
     #         Y 1024 x (3072 x 256 + 16384) = 1,912,602,624 / 512 = 3,735,552
-    # so K128 (uncapped).
+    # K256's estimate is within 5% of K128's (1.8% above), so the flops each
+    # kernel was bound for decide: K256 for X's 137.4 GFLOP, K128 for Y's
+    # 103.1 GFLOP: K256 (uncapped).
     t = _table(tmp_path, ctx, ["entry 2 0 0 12 4096 4096 " + " ".join([K256 + "_c0"] * 5),
                                "entry 2 0 0 12 4096 3072 " + " ".join([K128 + "_c0"] * 5),
                                "entry 2 0 0 12 4096 3584 " + " ".join([K128 + "_c0"] * 5)])
     p = t.plan([desc(4096, 4096, 4096, 0), desc(4096, 4096, 3072, 1)], mode="selector")
-    assert p["n_dispatches"] == 1 and [t.variant(x)["name"] for x in p["variant_of"][:2]] == [K128 + "_c0"] * 2
+    assert p["n_dispatches"] == 1 and [t.variant(x)["name"] for x in p["variant_of"][:2]] == [K256 + "_c0"] * 2
     p = t.plan([desc(4096, 4096, 4096, 0), desc(4096, 4096, 3584, 1)], mode="selector")
     assert p["n_dispatches"] == 2
     assert [t.variant(x)["name"] for x in p["variant_of"][:2]] == [K256 + "_c0", K128 + "_c0"]
@@ -306,6 +308,34 @@ def test_short_group_weighs_members_isolated_kernels(tmp_path, ctx):
     p = t.plan([desc(4096, 2048, 1024, 0), desc(16, 1024, 1024, 1)], mode="selector")
     assert p["n_groups"] == 1 and p["n_dispatches"] == 1
     assert [t.variant(x)["name"] for x in p["variant_of"][:2]] == [K128 + "_c0"] * 2
+
+
+def test_short_group_tie_goes_to_the_heaviest_binding(tmp_path, ctx):
+    # The layer share (QKV (512, 4608, 12288), out-proj (512, 12288, 1536),
+    # FFN-up (512, 6144, 12288), FFN-down (512, 12288, 6144), two each) under
+    # a table that binds QKV to K128, the out-projection to K64 and the FFN
+    # GEMMs to K256 (every CD class).  Roofline 184 us < 100 us x 2 extra
+    # kernels: one kernel.  Tile model (all direct; K tile 64):
+    #   K256: per 512, area 65536; tiles 36, 96, 48, 96 per pair member:
+    #         2 x (36 x 6,356,992 + 96 x 851,968 + 48 x 6,356,992 + 96 x 3,211,264)
+    #         = 1,848,115,200 / 256 slots = 7,219,200 (longest 6,356,992)
+    #   K128: per 256, area 16384; tiles 144, 384, 192, 384:
+    #         2 x (144 x 3,162,112 + 384 x 409,600 + 192 x 3,162,112 + 384 x 1,589,248)
+    #         = 3,660,054,528 / 512 slots = 7,148,544
+    #   K64:  per 128, area 4096; tiles 576, 1536, 768, 1536:
+    #         2 x (576 x 1,576,960 + 1536 x 200,704 + 768 x 1,576,960 + 1536 x 790,528)
+    #         = 7,283,933,184 / 512 = 14,226,432
+    # K128 is cheapest; K256 is 1.0% above it (within 5%), K64 twice it.  Of
+    # the two, the GEMMs were bound to K256 for 309.2 GFLOP (the four FFN
+    # GEMMs, 77.3 each) and to K128 for 116.0 (the two QKV): K256.  Without
+    # the tie rule K128 would win.
+    ent = lambda n, k, kern: f"entry 2 0 0 9 {n} {k} " + " ".join([kern + "_c0"] * 5)  # noqa: E731
+    t = _table(tmp_path, ctx, [ent(4608, 12288, K128), ent(12288, 1536, K64), ent(6144, 12288, K256),
+                               ent(12288, 6144, K256)], cd_class=3)
+    shapes = [(512, 4608, 12288), (512, 12288, 1536), (512, 6144, 12288), (512, 12288, 6144)] * 2
+    p = t.plan([desc(m, n, k, j) for j, (m, n, k) in enumerate(shapes)], mode="selector")
+    assert p["n_groups"] == 1 and p["n_dispatches"] == 1
+    assert {t.variant(x)["name"] for x in p["variant_of"][:8]} == {K256 + "_c0"}
 
 
 def _add(m, n, slot):
