@@ -38,17 +38,17 @@ RECORDS = os.path.join(ROOT, "paper_2409_02227_amd", "tables", "gfx950_records.j
 KNN_TABLE = os.path.join(ROOT, "paper_2409_02227_amd", "tables", "gfx950_knn.table")
 
 WORKLOADS = {
-    "tp8_layer_share": (3, "8 bf16 GEMMs: QKV (512,4608,12288), out-proj (512,12288,1536), "
+    "tp8_layer_share": ("layer_share", "8 bf16 GEMMs: QKV (512,4608,12288), out-proj (512,12288,1536), "
                            "FFN-up (512,6144,12288), FFN-down (512,12288,6144) x 2 microbatches"),
-    "lstm_gates": (2, "4 bf16 GEMMs (64,4096,1024): LSTM-step gate projections at batch 64"),
-    "square_fp16": (1, "2 fp16 GEMMs (256,256,256)"),
-    "two_tenant_fp8": (5, "2 tenants x 16 fp8 e4m3 GEMMs, M in {1,32,256,2048}, N=K in {4096,8192}"),
-    "het_submissions": (4, "seeded submissions of 2-16 bf16 GEMMs, M log-uniform in [16,4096], "
+    "lstm_gates": ("lstm_gates", "4 bf16 GEMMs (64,4096,1024): LSTM-step gate projections at batch 64"),
+    "square_fp16": ("square_fp16", "2 fp16 GEMMs (256,256,256)"),
+    "two_tenant_fp8": ("fp8_tenants", "2 tenants x 16 fp8 e4m3 GEMMs, M in {1,32,256,2048}, N=K in {4096,8192}"),
+    "het_submissions": ("het", "seeded submissions of 2-16 bf16 GEMMs, M log-uniform in [16,4096], "
                            "N,K in {1024,2048,4096,8192}, operands windows of device pools"),
-    "tp8_layer_share_nt": ("3nt", "the 8 bf16 GEMMs of tp8_layer_share with each weight stored N x K "
+    "tp8_layer_share_nt": ("layer_share_nt", "the 8 bf16 GEMMs of tp8_layer_share with each weight stored N x K "
                                   "(linear-layer layout) and used transposed"),
-    "tp8_layer_share_f32": ("3f32", "the 8 GEMMs of tp8_layer_share in fp32 (full precision)"),
-    "attn_bgemm_4p": ("attn", "4 heterogeneous strided batched bf16 GEMMs: attention scores Q K^T "
+    "tp8_layer_share_f32": ("layer_share_f32", "the 8 GEMMs of tp8_layer_share in fp32 (full precision)"),
+    "attn_bgemm_4p": ("attention_bgemms", "4 heterogeneous strided batched bf16 GEMMs: attention scores Q K^T "
                               "(SL x SL x 64, K transposed) for SL 128/256/384/512, 64 items each"),
     "gemm_add_pairs": ("pairs", "8 submissions of one bf16 GEMM and an element-wise add sized like its "
                                 "output (2P GEMM + non-GEMM co-runs)"),
@@ -446,7 +446,7 @@ def accuracy_bench(args, desc):
                 tuned.append((1 << int(tok[4]), int(tok[5]), int(tok[6])))
         order = np.random.default_rng(46).permutation(len(tuned))
         shapes = [tuned[i] for i in order[:args.accuracy_shapes]]
-    for sub in inputs.config4(seed=46, count=40) if args.accuracy_set == "untuned" else []:
+    for sub in inputs.het_submissions(seed=46, count=40) if args.accuracy_set == "untuned" else []:
         for g in sub:
             key = (g.m, g.n, g.k)
             if key not in seen and len(shapes) < args.accuracy_shapes:
@@ -668,25 +668,23 @@ def main():
     import torch
     from paper_2409_02227_amd import gdy, inputs
 
-    cfg_id, desc = WORKLOADS[args.workload]
-    if cfg_id == 4:
+    kind, desc = WORKLOADS[args.workload]
+    if kind == "het":
         return het_bench(args, desc)
-    if cfg_id == "pairs":
+    if kind == "pairs":
         return pairs_bench(args, desc)
-    if cfg_id == "parts":
+    if kind == "parts":
         return partition_bench(args, desc)
-    if cfg_id == "knn":
+    if kind == "knn":
         return knn_bench(args, desc)
-    if cfg_id == "acc":
+    if kind == "acc":
         return accuracy_bench(args, desc)
-    if cfg_id == "3nt":
-        specs = inputs.config3(trans_b=1)
-    elif cfg_id == "3f32":
-        specs = inputs.config3(dtype="f32")
-    elif cfg_id == "attn":
-        specs = inputs.config_attn()
-    else:
-        specs = inputs.CONFIGS[cfg_id]()
+    if kind == "layer_share_nt":
+        specs = inputs.layer_share(trans_b=1)
+    elif kind == "layer_share_f32":
+        specs = inputs.layer_share(dtype="f32")
+    else:  # the generator of that name
+        specs = getattr(inputs, kind)()
     mats = [inputs.materialize(s, "cuda:0", keep_host=True) for s in specs]
     table = args.table if args.table and os.path.exists(args.table) else None
     ctx = gdy.Context(0, table=table, max_streams=16)

@@ -145,34 +145,34 @@ def operand_codes(spec: GemmSpec, which: str) -> tuple:
 # the five workloads
 # ---------------------------------------------------------------------------
 
-def config1(seed: int = 1) -> list:
+def square_fp16(seed: int = 1) -> list:
     u = ("uniform", -1.0, 1.0)
     return [GemmSpec(256, 256, 256, "f16", a_dist=u, b_dist=u, seed=seed * 1000 + i,
                      name=f"sq256_{i}") for i in range(2)]
 
 
-def config2(seed: int = 2) -> list:
+def lstm_gates(seed: int = 2) -> list:
     return [GemmSpec(64, 4096, 1024, "bf16", seed=seed * 1000 + i, name=f"lstm_gate_{i}")
             for i in range(4)]
 
 
-CONFIG3_SHAPES = (("qkv", 512, 4608, 12288), ("out", 512, 12288, 1536),
+LAYER_SHARE_SHAPES = (("qkv", 512, 4608, 12288), ("out", 512, 12288, 1536),
                   ("up", 512, 6144, 12288), ("down", 512, 12288, 6144))
 
 
-def config3(seed: int = 3, dtype: str = "bf16", trans_b: int = 0) -> list:
+def layer_share(seed: int = 3, dtype: str = "bf16", trans_b: int = 0) -> list:
     """The tensor-sliced layer share; `dtype` f32 gives its full-precision
     form, `trans_b` 1 stores each weight N x K (the layout of a linear
     layer's weight) and uses it transposed."""
     out = []
     for mb in range(2):
-        for j, (nm, m, n, k) in enumerate(CONFIG3_SHAPES):
+        for j, (nm, m, n, k) in enumerate(LAYER_SHARE_SHAPES):
             out.append(GemmSpec(m, n, k, dtype, 0, trans_b, seed=seed * 1000 + 10 * mb + j,
                                 name=f"{nm}_mb{mb}"))
     return out
 
 
-def config4(seed: int = 4, count: int = 200) -> list:
+def het_submissions(seed: int = 4, count: int = 200) -> list:
     """List of submissions, each a list of GemmSpec (without pool offsets)."""
     rng = np.random.default_rng([seed, 4])
     subs = []
@@ -190,7 +190,7 @@ def config4(seed: int = 4, count: int = 200) -> list:
     return subs
 
 
-def config5(seed: int = 5) -> list:
+def fp8_tenants(seed: int = 5) -> list:
     rng = np.random.default_rng([seed, 5])
     tenants = []
     for t in range(2):
@@ -209,7 +209,7 @@ def config5(seed: int = 5) -> list:
     return out
 
 
-def config_attn(seed: int = 6, items: int = 64) -> list:
+def attention_bgemms(seed: int = 6, items: int = 64) -> list:
     """Heterogeneous strided batched GEMMs (B-GEMMs, Sec. 6.7): the attention
     scores Q K^T of four sequence-length buckets (128, 256, 384, 512 tokens),
     each a batch of 16 heads x 4 sequences with head dimension 64; K is
@@ -263,7 +263,6 @@ def gemm_add_pairs(seed: int = 7) -> list:
             for i, (m, n, k) in enumerate(shapes)]
 
 
-CONFIGS = {1: config1, 2: config2, 3: config3, 5: config5}
 
 
 # ---------------------------------------------------------------------------
@@ -369,7 +368,7 @@ def het_pools(torch, device="cuda"):
 def het_placed(count: int = 200) -> list:
     """The first `count` heterogeneous submissions with their pool windows:
     per submission a list of (GemmSpec, A offset, B offset) in elements."""
-    return pool_specs(config4(count=count), HET_A_ELEMS, HET_B_ELEMS, seed=4)
+    return pool_specs(het_submissions(count=count), HET_A_ELEMS, HET_B_ELEMS, seed=4)
 
 
 def pool_specs(subs: list, a_pool_elems: int, b_pool_elems: int, seed: int) -> list:

@@ -21,7 +21,7 @@ the one bench.py measured with HIP events in the same run), and `collect
 workload's dominant dispatch in the record file bench.py reports as the
 roofline's `traffic` while the kernel sources hash the same.
 
-Usage, on a GPU machine:
+Usage, on an MI355X (from the repository root):
   python3 -m paper_2409_02227_amd.profiling ceilings --out profiles/ceilings_gfx950.md
   python3 -m paper_2409_02227_amd.profiling trace --workload tp8_layer_share --out profiles/x.md
   python3 -m paper_2409_02227_amd.profiling collect --workload tp8_layer_share --out profiles/x.md \
@@ -320,7 +320,7 @@ def trace(args) -> None:
     target = " ".join(["python3"] + [shlex.quote(os.path.relpath(x, ROOT) if x.startswith(ROOT) else x)
                                for x in cmd[1:]])
     lines = [f"# Kernel trace: {args.workload} workload, {args.mode} mode", "",
-             "Command (on the GPU box, from the repository root):", "", f"    {cmdline}", "",
+             "Command (on the MI355X, from the repository root):", "", f"    {cmdline}", "",
              f"which runs `rocprofv3 --kernel-trace --stats` over `{target}`.", "",
              "The bench times the set in default, GO, sequential and the chosen mode, runs a pass with "
              "per-dispatch events, a latency pass and the best-CD search; durations are End - Start "
@@ -381,7 +381,7 @@ def ceilings(args) -> None:
         print(f"ceilings run {rep + 1}/{args.repeat} done", flush=True)
     med = lambda xs: sorted(xs)[len(xs) // 2]
     cmdline = " ".join(shlex.quote(x) for x in ["python3", "-m", "paper_2409_02227_amd.profiling", *sys.argv[1:]])
-    lines = ["# Chip ceilings measured on the device", "", "Command (on the GPU box, from the repository root):", "",
+    lines = ["# Chip ceilings measured on the device", "", "Command (on the MI355X, from the repository root):", "",
              f"    {cmdline}", "",
              f"which runs `paper_2409_02227_amd/ceilings` (built from `csrc/ceilings.hip`) {args.repeat} times; "
              "medians over the runs.  One block per CU (128 KiB of LDS each), no global traffic in the timed "
@@ -428,7 +428,7 @@ def derived(v: dict, cal: dict) -> dict:
 
 def write_summary(path: str, res: dict, args) -> None:
     lines = [f"# Counters: {args.workload or args.gemm + ' on ' + args.kernel}", "",
-             "Command (on the GPU box, from the repository root):", "",
+             "Command (on the MI355X, from the repository root):", "",
              f"    {res['command']}", "",
              f"Each counter pass profiles: `{res['target']}`", "",
              f"Dominant dispatch: `{short(res['kernel'])}`, grid {res['grid']} threads, "
@@ -497,7 +497,7 @@ def main():
     c.add_argument("--dtype", default="bf16", choices=("bf16", "fp8"))
     c.add_argument("--steps", type=int, default=5)
     c.add_argument("--passes", default="", help="comma-separated subset of " + ",".join(PASSES))
-    c.add_argument("--raw", default="gpurun_out/profiling", help="directory for the raw profiler output")
+    c.add_argument("--raw", default="profiling_raw/collect", help="directory for the raw profiler output")
     c.add_argument("--out", help="write the text summary here (profiles/...)")
     c.add_argument("--timeout", type=int, default=150)
     c.add_argument("--keep-raw", action="store_true", help="keep the per-dispatch CSVs of every pass")
@@ -508,7 +508,7 @@ def main():
     t.add_argument("--steps", type=int, default=20)
     t.add_argument("--warmup", type=int, default=5)
     t.add_argument("--top", type=int, default=5)
-    t.add_argument("--raw", default="gpurun_out/profiling_trace")
+    t.add_argument("--raw", default="profiling_raw/trace")
     t.add_argument("--out", required=True)
     t.add_argument("--timeout", type=int, default=240)
     t.add_argument("--keep-raw", action="store_true")

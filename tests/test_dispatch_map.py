@@ -70,7 +70,7 @@ def test_layer_share_is_placed_on_few_xcds():
     GEMM's tiles on at most 4 of the 8 XCDs (all 8 before placement), and
     every XCD holds the same work (tiles x (K tiles + 1)) within 1%."""
     ctx = gdy.Context(-1, table=TABLE if os.path.exists(TABLE) else None)
-    specs = inputs.config3()
+    specs = inputs.layer_share()
     descs = [_desc(s.m, s.n, s.k, 2, i) for i, s in enumerate(specs)]
     for mode in ("selector", "go"):
         p, placed = _check_cover(ctx, descs, mode)

@@ -130,8 +130,8 @@ def test_concurrent_equals_isolated_bitwise(ctx):
 
 
 @pytest.mark.parametrize("mode", ["sequential", "default", "go", "selector"])
-def test_config1_and_config2_full(ctx, mode):
-    for specs in (inputs.config1(), inputs.config2()):
+def test_square_fp16_and_lstm_gates_full(ctx, mode):
+    for specs in (inputs.square_fp16(), inputs.lstm_gates()):
         mats = [inputs.materialize(s) for s in specs]
         plan = _run(ctx, mats, mode)
         assert sorted(plan["order"]) == list(range(len(specs)))
@@ -139,8 +139,8 @@ def test_config1_and_config2_full(ctx, mode):
             check(m, label=mode)
 
 
-def test_config5_fp8_sampled(ctx):
-    mats = [inputs.materialize(s) for s in inputs.config5()]
+def test_fp8_tenants_sampled(ctx):
+    mats = [inputs.materialize(s) for s in inputs.fp8_tenants()]
     for mode in ("sequential", "default"):
         _run(ctx, mats, mode)
         for m in mats:

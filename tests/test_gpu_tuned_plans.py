@@ -53,7 +53,7 @@ def run_and_check(ctx, mats, label, samples=3, mode="selector"):
 
 def test_heterogeneous_submissions_selector(tctx):
     plans = []
-    for s, sub in enumerate(inputs.config4(count=6)):
+    for s, sub in enumerate(inputs.het_submissions(count=6)):
         mats = [inputs.materialize(sp) for sp in sub]
         plans.append(run_and_check(tctx, mats, f"submission {s}"))
         del mats
@@ -64,13 +64,13 @@ def test_heterogeneous_submissions_selector(tctx):
 
 
 def test_attention_bgemms_selector(tctx):
-    mats = [inputs.materialize(sp) for sp in inputs.config_attn()]
+    mats = [inputs.materialize(sp) for sp in inputs.attention_bgemms()]
     plan = run_and_check(tctx, mats, "attention", samples=4)
     assert plan["n_dispatches"] == 1  # a short group on one kernel
 
 
 def test_fp8_tenants_selector(tctx):
-    mats = [inputs.materialize(sp) for sp in inputs.config5()]
+    mats = [inputs.materialize(sp) for sp in inputs.fp8_tenants()]
     run_and_check(tctx, mats, "fp8 tenants", samples=2)
 
 

@@ -56,7 +56,7 @@ def _sample(m, n, rows, cols, rng):
 
 
 def test_layer_share_every_element_every_mode(wctx):
-    mats = [inputs.materialize(s) for s in inputs.config3()]
+    mats = [inputs.materialize(s) for s in inputs.layer_share()]
     refs = [_full_ref(m) for m in mats]
     bits = {}
     for mode in ("sequential", "default", "go", "selector"):
@@ -77,7 +77,7 @@ def test_layer_share_every_element_every_mode(wctx):
 
 @pytest.mark.parametrize("mode", ["selector", "go"])
 def test_fp8_tenants(wctx, mode):
-    mats = [inputs.materialize(s) for s in inputs.config5()]
+    mats = [inputs.materialize(s) for s in inputs.fp8_tenants()]
     reset_outputs(mats)
     wctx.execute([gemm_of(m) for m in mats], mode=mode)
     torch.cuda.synchronize()

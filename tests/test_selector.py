@@ -268,7 +268,7 @@ def test_paper_parts_match_oracle_on_the_tuned_table():
     table = sel.parse_table(TABLE)
     if table["lr"] is None and not table["lr_by_type"]:
         pytest.skip("table has no predictor")
-    for specs in (inputs.config1(), inputs.config2(), inputs.config3(), inputs.config5()):
+    for specs in (inputs.square_fp16(), inputs.lstm_gates(), inputs.layer_share(), inputs.fp8_tenants()):
         _check_paper_parts(ctx, table, _specs_descs(specs))
 
 
