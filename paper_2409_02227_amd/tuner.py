@@ -261,6 +261,31 @@ def tune_shape(ctx, bench, torch, variants, shape, rounds=3):
     return rec
 
 
+def relabel_shape(bench, torch, variants, rec, rounds=3):
+    """Re-time a tuned shape's CD step with the current library, keeping its
+    kernels: per CD, the copies one after another on its isolated kernel
+    (SEQUENTIAL's launch) and as one group on its recorded GO-Kernel; the
+    speedups give a new label.  Returns the updated record."""
+    dtype, ta, tb, m, n, k = rec["shape"][:6]
+    batch = rec["shape"][6] if len(rec["shape"]) > 6 else 0
+    by_name = {v["name"]: i for i, v in enumerate(variants)}
+    ops = operands(torch, dtype, ta, tb, m, n, k, 16, rounds, batch)
+    iso = by_name[rec["go"]["1"]]
+    out = dict(rec)
+    out["seq"], out["conc"] = {}, {}
+    for cd in CDS[1:]:
+        n_g = cd * rounds
+        out["seq"][str(cd)] = bench.time(submission(ops, cd, rounds, iso, ta, tb), "sequential", 0) / n_g
+        vid = by_name[rec["go"][str(cd)]]
+        out["conc"][str(cd)] = bench.time(submission(ops, cd, rounds, vid, ta, tb), "forced_grouped", cd) / n_g
+    sp = {cd: out["seq"][str(cd)] / out["conc"][str(cd)] for cd in CDS[1:]}
+    out["speedup"] = {str(c): sp[c] for c in sp}
+    out["label"] = label_of(sp)
+    out["relabelled"] = True
+    del ops
+    return out
+
+
 # ---------------------------------------------------------------------------
 # table writing and predictor training
 # ---------------------------------------------------------------------------
@@ -610,6 +635,9 @@ def main(argv=None):
     ap.add_argument("--kernel-tol", type=float, default=None,
                     help="CD-step kernels within this fraction of the fastest count as ties, broken toward "
                          f"the kernel most shapes of the kind accept (default {KERNEL_TOL}: the fastest)")
+    ap.add_argument("--relabel", default=None,
+                    help="re-time the CD step of every --records shape on its recorded kernels with the "
+                         "current library, write the relabelled records here and retrain")
     ap.add_argument("--extend", default=None,
                     help="no timing: write --out as this table plus entries for the --records shapes it "
                          "lacks (its predictors kept)")
@@ -643,10 +671,24 @@ def main(argv=None):
     shapes = shape_set(args.shapes)
     if args.limit:
         shapes = shapes[:args.limit]
-    if args.retrain or args.knn:
+    if args.retrain or args.knn or args.relabel:
         if not records:
-            raise SystemExit("--retrain / --knn need --records with tuned shapes")
+            raise SystemExit("--retrain / --knn / --relabel need --records with tuned shapes")
         shapes = [tuple(r["shape"]) for r in records]
+    if args.relabel:
+        t0 = time.time()
+        relabelled, old_labels = [], [r["label"] for r in records]
+        for i, r in enumerate(records):
+            relabelled.append(relabel_shape(bench, torch, variants, r))
+            torch.cuda.empty_cache()
+            if i % 20 == 19:
+                print(f"relabelled {i + 1}/{len(records)} ({time.time() - t0:.0f} s)", flush=True)
+        records = relabelled
+        with open(args.relabel, "w") as f:
+            for r in records:
+                f.write(json.dumps(r) + "\n")
+        changed = sum(1 for a, r in zip(old_labels, records) if a != r["label"])
+        print(f"relabelled {len(records)} records, {changed} labels changed", flush=True)
     t0 = time.time()
     for i, s in enumerate(shapes):
         if tuple(s) in done:
