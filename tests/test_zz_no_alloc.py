@@ -2,7 +2,9 @@
 in the library's static device array) against gdy_execute, through the
 C-ABI: the same plans and bit-identical outputs, both within the oracle's
 bound, on two calls in a row (the second smaller), and a clear refusal of a
-plan that needs more than the array holds."""
+plan that needs more than the array holds; and the entry point captured in a
+HIP graph (torch.cuda.CUDAGraph on a side stream), every replay bit-identical
+to the eager call, with eager work and synchronisations between replays."""
 import os
 
 import numpy as np
@@ -81,3 +83,41 @@ def test_static_entry_refuses_a_plan_beyond_the_array(sctx):
     p = sctx.execute_static(gemms, mode="forced_grouped", forced_cd=2, want_plan=True)
     torch.cuda.synchronize()
     assert p["n_groups"] == 3 and all(torch.count_nonzero(c).item() == 0 for c in cs)
+
+
+@pytest.mark.parametrize("mode", ["selector", "default"])
+def test_static_entry_in_a_captured_graph(sctx, mode):
+    specs = [GemmSpec(16, 1024, 8192, "bf16", seed=9800, name="g0"),    # splits
+             GemmSpec(32, 2048, 8192, "bf16", seed=9801, name="g1"),    # splits
+             GemmSpec(512, 1024, 1024, "bf16", seed=9802, name="g2"),
+             GemmSpec(1024, 4096, 4096, "bf16", seed=9803, name="g3")]  # another kernel
+    mats = [inputs.materialize(s) for s in specs]
+    gemms = [gemm_of(m) for m in mats]
+    reset_outputs(mats)
+    plan = sctx.execute_static(gemms, mode=mode, want_plan=True)
+    torch.cuda.synchronize()
+    print(f"{mode}: {plan['n_groups']} groups, {plan['n_dispatches']} dispatches, splits {plan['split_of'][:4]}",
+          flush=True)
+    assert any(s > 1 for s in plan["split_of"][:4])
+    ref = [out_codes(m).copy() for m in mats]
+    for m in mats:
+        check(m, samples=4, label=f"eager {mode}")
+    side = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    reset_outputs(mats)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, stream=side):
+        sctx.execute_static(gemms, mode=mode, stream=side)
+    torch.cuda.synchronize()
+    other = inputs.materialize(GemmSpec(256, 256, 256, "bf16", seed=9810, name="eager"))
+    for rep in range(3):
+        reset_outputs(mats)              # a fill kernel per buffer, eager
+        sctx.execute([gemm_of(other)], mode="sequential")  # eager library work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for m, r in zip(mats, ref):
+            assert np.array_equal(out_codes(m), r), f"replay {rep}: {m.spec.name} differs from the eager call"
+    check(other, label="eager between replays")
+    del graph
+    torch.cuda.synchronize()
