@@ -59,9 +59,25 @@ def build_ceilings() -> str:
     return CEILINGS
 
 
+EXAMPLE = os.path.join(HERE, "examples", "gemm_set")
+
+
+def build_example() -> str:
+    """examples/gemm_set: a C++ program that drives libgdy through its C-ABI
+    alone (no Python), linked against the in-tree library."""
+    tmp = EXAMPLE + ".tmp"
+    cmd = [_hipcc(), *[f for f in FLAGS if f != "-fPIC"], os.path.join(HERE, "examples", "gemm_set.cpp"),
+           "-L", HERE, "-lgdy", "-Wl,-rpath,$ORIGIN/..", "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for examples/gemm_set.cpp:\n{r.stderr}")
+    os.replace(tmp, EXAMPLE)
+    return EXAMPLE
+
+
 def build(jobs: int | None = None) -> str:
-    """Compile every source and link libgdy.so (always rebuilds), and build
-    the ceiling probe."""
+    """Compile every source and link libgdy.so (always rebuilds), then build
+    the ceiling probe and the C-ABI example program."""
     os.makedirs(BUILD, exist_ok=True)
     jobs = jobs or min(len(SOURCES), os.cpu_count() or 1)
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
@@ -74,6 +90,7 @@ def build(jobs: int | None = None) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
     os.replace(tmp, LIB)
+    build_example()
     return LIB
 
 
