@@ -169,10 +169,17 @@ class Add:
     def desc(self) -> GemmDesc:
         a, b, c = self.a, self.b, self.c
         batch = c.shape[0] if c.dim() == 3 else 0
+        if batch and any(t.dim() == 3 and t.shape[0] != batch for t in (a, b)):
+            raise ValueError("batched operands disagree on the batch size")
+        if not batch and (a.dim() == 3 or b.dim() == 3):
+            raise ValueError("a batched A or B needs a batched C")
 
         def mat(t):
             return (t[0], t.stride(0)) if t.dim() == 3 else (t, 0)
         (a2, sa), (b2, sb), (c2, sc) = mat(a), mat(b), mat(c)
+        for t in (a2, b2, c2):
+            if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1):
+                raise ValueError("operands must be 2-D (or 3-D batches) with a contiguous last dimension")
         m, n = c2.shape
         if tuple(a2.shape) != (m, n) or tuple(b2.shape) != (m, n):
             raise ValueError("add operands must have C's shape")
@@ -221,11 +228,15 @@ class Gemm:
                 return t[0], t.stride(0)
             return t, 0
         (a2, sa), (b2, sb), (c2, sc) = mat(a), mat(b), mat(c)
-        m, n = c2.shape
-        k = a2.shape[0] if self.trans_a else a2.shape[1]
         for t in (a2, b2, c2):
             if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1):
                 raise ValueError("operands must be 2-D (or 3-D batches) with a contiguous last dimension")
+        m, n = c2.shape
+        k = a2.shape[0] if self.trans_a else a2.shape[1]
+        am = a2.shape[1] if self.trans_a else a2.shape[0]
+        bk, bn = (b2.shape[1], b2.shape[0]) if self.trans_b else (b2.shape[0], b2.shape[1])
+        if am != m or bn != n or bk != k:
+            raise ValueError(f"shapes disagree: op(A) {am}x{k}, op(B) {bk}x{bn}, C {m}x{n}")
         d = GemmDesc()
         d.m, d.n, d.k = m, n, k
         d.a_type, d.b_type, d.c_type = _dtype_code(a), _dtype_code(b), _dtype_code(c)

@@ -76,3 +76,31 @@ def test_binding_layouts_equal_the_c_compilers(tmp_path):
         assert got[(cname, "size")] == ctypes.sizeof(py), cname
         for f, _ in py._fields_:
             assert got[(cname, f)] == getattr(py, f).offset, (cname, f)
+
+
+def test_binding_rejects_operands_that_disagree():
+    """Gemm and Add descriptors are built from tensors only when their shapes,
+    batch sizes and last-dimension strides agree: a B of the wrong shape would
+    otherwise hand the library extents past its allocation.  CPU tensors:
+    building a descriptor touches no device."""
+    torch = pytest.importorskip("torch")
+    bf = torch.bfloat16
+    a, b, c = torch.zeros(8, 16, dtype=bf), torch.zeros(16, 4, dtype=bf), torch.zeros(8, 4, dtype=bf)
+    d = gdy.Gemm(a, b, c).desc()
+    assert (d.m, d.n, d.k, d.lda, d.ldb, d.ldc) == (8, 4, 16, 16, 4, 4)
+    d = gdy.Gemm(a, b.t().contiguous(), c, 0, 1).desc()  # B stored N x K
+    assert (d.k, d.ldb, d.trans_b) == (16, 16, 1)
+    bad = [gdy.Gemm(a, torch.zeros(15, 4, dtype=bf), c),            # K differs
+           gdy.Gemm(a, torch.zeros(16, 5, dtype=bf), c),            # N differs
+           gdy.Gemm(torch.zeros(9, 16, dtype=bf), b, c),            # M differs
+           gdy.Gemm(a, b, c, 0, 1),                                 # B^T would be 4 x 16
+           gdy.Gemm(a, torch.zeros(4, 16, dtype=bf).t(), c),        # last dimension strided
+           gdy.Gemm(torch.zeros(2, 8, 16, dtype=bf), torch.zeros(3, 16, 4, dtype=bf),
+                    torch.zeros(3, 8, 4, dtype=bf)),                # batch sizes differ
+           gdy.Add(c, c.t().contiguous().t(), torch.zeros(8, 4, dtype=bf)),  # strided add operand
+           gdy.Add(torch.zeros(2, 8, 4, dtype=bf), c, torch.zeros(3, 8, 4, dtype=bf))]
+    for g in bad:
+        with pytest.raises(ValueError):
+            g.desc()
+    e = gdy.Add(c, c, torch.zeros(8, 4, dtype=bf)).desc()
+    assert (e.m, e.n, e.k, e.op) == (8, 4, 0, gdy.ADD)
