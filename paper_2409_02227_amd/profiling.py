@@ -57,6 +57,9 @@ PASSES = {
     "l2": ["TCC_HIT_sum", "TCC_MISS_sum", "TCC_REQ_sum", "TCC_EA0_RDREQ_sum"],
     "fetch": ["FETCH_SIZE"],
     "write": ["WRITE_SIZE"],
+    # GRBM_COUNT ticks once per graphics clock in each XCD's GRBM and is summed
+    # over the XCDs: over the dispatch's own duration it gives the clock held
+    "clock": ["GRBM_COUNT", "GRBM_GUI_ACTIVE"],
 }
 COPY_BYTES = 1 << 30
 # what the kernels' HBM traffic depends on: the kernels, the launch block and
@@ -135,6 +138,16 @@ def read_counters(d: str) -> list:
     return list(rows.values())
 
 
+def num_xcc(d: str):
+    """XCDs of the profiled GPU, from rocprofv3's agent table (None if absent)."""
+    for f in glob.glob(os.path.join(d, "*agent_info.csv")):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r.get("Agent_Type") == "GPU" and int(r.get("Num_Xcc") or 0) > 0:
+                    return int(r["Num_Xcc"])
+    return None
+
+
 def read_trace(d: str) -> list:
     """Per-dispatch rows in dispatch order: {"kernel", "grid" (threads),
     "wg" (threads per workgroup), "ns"}."""
@@ -206,6 +219,7 @@ def collect(args) -> None:
             continue
         d = run_pass(out_dir, name, counters, cmd, args.timeout)
         rows = read_counters(d)
+        xcc = num_xcc(d)
         if not args.keep_raw:
             prune(d)
         k = key if any((r["kernel"], r["grid"]) == key for r in rows) else dominant(rows)
@@ -214,6 +228,11 @@ def collect(args) -> None:
             if v is not None:
                 vals[c] = v
                 counted[c] = [r for r in rows if (r["kernel"], r["grid"]) == k]
+        per_ns = [r["GRBM_COUNT"] / r["ns"] for r in rows
+                  if (r["kernel"], r["grid"]) == k and "GRBM_COUNT" in r and r["ns"] > 0]
+        if per_ns and xcc:
+            vals["GRBM_COUNT_per_ns"] = sum(per_ns) / len(per_ns)
+            vals["Num_Xcc"] = xcc
     cal = {}
     if "FETCH_SIZE" in vals or "WRITE_SIZE" in vals:
         for name, c in (("copy_fetch", "FETCH_SIZE"), ("copy_write", "WRITE_SIZE")):
@@ -423,6 +442,8 @@ def derived(v: dict, cal: dict) -> dict:
     for c, nm in (("FETCH_SIZE", "hbm_read_bytes"), ("WRITE_SIZE", "hbm_write_bytes")):
         if c in v and cal.get(c):
             d[nm] = int(v[c] * 1024 * cal[c])
+    if v.get("GRBM_COUNT_per_ns") and v.get("Num_Xcc"):
+        d["clock_ghz"] = round(v["GRBM_COUNT_per_ns"] / v["Num_Xcc"], 3)
     return d
 
 

@@ -52,6 +52,21 @@ def test_derived_metrics():
     assert d["hbm_read_bytes"] == 1000 * 1024 * 2
 
 
+def test_clock_from_grbm_count_over_the_dispatch(tmp_path):
+    """GRBM_COUNT summed over the XCDs, over each dispatch's own duration and
+    divided by the XCD count of the agent table, is the clock held."""
+    _write_csv(tmp_path / "p_agent_info.csv", [{"Node_Id": 0, "Agent_Type": "CPU", "Num_Xcc": 1, "Cu_Count": 16},
+                                              {"Node_Id": 1, "Agent_Type": "GPU", "Num_Xcc": 8, "Cu_Count": 256}])
+    assert profiling.num_xcc(str(tmp_path)) == 8
+    assert profiling.num_xcc(str(tmp_path / "missing")) is None
+    # 480 us at 2.0 GHz on 8 XCDs, 400 us at 2.2 GHz: 16.0 and 17.6 counts per ns
+    rows = [{"GRBM_COUNT": 16.0 * 480_000, "ns": 480_000}, {"GRBM_COUNT": 17.6 * 400_000, "ns": 400_000}]
+    per_ns = sum(r["GRBM_COUNT"] / r["ns"] for r in rows) / len(rows)
+    assert profiling.derived({"GRBM_COUNT_per_ns": per_ns, "Num_Xcc": 8}, {})["clock_ghz"] == 2.1
+    assert "clock_ghz" not in profiling.derived({"GRBM_COUNT_per_ns": per_ns}, {})
+    assert profiling.PASSES["clock"] == ["GRBM_COUNT", "GRBM_GUI_ACTIVE"]  # two GRBM counters: one run
+
+
 def test_bench_line_takes_the_last_metric_line(tmp_path):
     log = tmp_path / "trace.log"
     log.write_text('noise\n{"metric": "m", "value": 1}\n{"other": 2}\n{"metric": "m", "value": 2}\ntail\n')
