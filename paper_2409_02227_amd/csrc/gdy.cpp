@@ -74,10 +74,16 @@ struct Predictor {
   double b[GDY_N_CD];
 };
 
+// The coordinates nearest_entry compares, packed for a linear scan.
+struct EntryKey {
+  double mlog, ln, lk, li;
+};
+
 struct Table {
   bool loaded = false;
   std::vector<TableEntry> entries;
   std::vector<int> by_layout[5][2][2];  // entry indices per (dtype, ta, tb), file order
+  std::vector<EntryKey> keys[5][2][2];  // their coordinates, in the same order
   // lr[0]: the predictor for every input type; lr[d]: one trained on input
   // type d alone, used for GEMMs of that type when present
   Predictor lr[5];
@@ -253,14 +259,16 @@ int nearest_entry(const gdy_ctx* ctx, const gdy_gemm& g) {
   const double ln = std::log2((double)std::max<int64_t>(g.n, 1));
   const double lk = std::log2((double)std::max<int64_t>(g.k, 1));
   const double li = std::log2((double)std::max(g.batch, 1));
+  const std::vector<int>& idx = t.by_layout[g.a_type][g.trans_a & 1][g.trans_b & 1];
+  const std::vector<EntryKey>& key = t.keys[g.a_type][g.trans_a & 1][g.trans_b & 1];
+  const double ml = (double)mlog;
   int best = -1;
   double best_d = 0;
-  for (int i : t.by_layout[g.a_type][g.trans_a & 1][g.trans_b & 1]) {
-    const TableEntry& e = t.entries[i];
-    const double d = std::fabs((double)(e.mlog - mlog)) + std::fabs(e.ln - ln) + std::fabs(e.lk - lk) +
-                     std::fabs(e.li - li);
+  for (size_t j = 0; j < key.size(); ++j) {
+    const EntryKey& e = key[j];
+    const double d = std::fabs(e.mlog - ml) + std::fabs(e.ln - ln) + std::fabs(e.lk - lk) + std::fabs(e.li - li);
     if (best < 0 || d < best_d) {
-      best = i;
+      best = idx[j];
       best_d = d;
     }
   }
@@ -387,7 +395,8 @@ double group_cost(const gdy_ctx* ctx, int vid, const gdy_gemm* g, const std::vec
   return std::max(f / slots, longest) / (k.d->direct ? 1.5 : 1.0);
 }
 
-void unify_short_group(const gdy_ctx* ctx, const gdy_gemm* g, const std::vector<int>& grp, gdy_plan_t* p) {
+void unify_short_group(const gdy_ctx* ctx, const gdy_gemm* g, const std::vector<int>& grp,
+                       const std::vector<int>& entry, gdy_plan_t* p) {
   std::vector<int> kern;  // the GEMMs' kernels as uncapped variants, in order of first use
   double t = 0.0;
   for (int i : grp) {
@@ -400,7 +409,7 @@ void unify_short_group(const gdy_ctx* ctx, const gdy_gemm* g, const std::vector<
   std::vector<int> cand = kern;
   for (int i : grp) {
     if (g[i].op == GDY_OP_ADD) continue;
-    const int iso = bind_variant(ctx, g[i], 0, nullptr);
+    const int iso = bind_entry(ctx, g[i], entry[i], 0, nullptr);  // entry[i]: g[i]'s nearest tuned shape
     if (iso < 0) continue;
     const int v = ctx->variants[iso].uncapped;
     if (std::find(cand.begin(), cand.end(), v) == cand.end()) cand.push_back(v);
@@ -1042,7 +1051,7 @@ void make_plan_core(const gdy_ctx* ctx, const gdy_gemm* g, int n, int mode, int 
     std::vector<std::vector<int>> parts;  // their GEMMs
     for (int i : grp) p->variant_of[i] = bind_entry(ctx, g[i], entry[i], ci, &fb);
     uncap_mixed_group(ctx, g, grp, p);
-    unify_short_group(ctx, g, grp, p);
+    unify_short_group(ctx, g, grp, entry, p);
     for (int i : grp) {
       const int k = ctx->variants[p->variant_of[i]].kernel;
       size_t u = 0;
@@ -1544,6 +1553,7 @@ gdy_status load_table(gdy_ctx* ctx, const char* path) {
       if (e.dtype < 1 || e.dtype > 4 || (e.ta & ~1) || (e.tb & ~1))
         return fail(ctx, GDY_ERR_TABLE, "bad entry line: %s", line.c_str());
       t.by_layout[e.dtype][e.ta][e.tb].push_back((int)t.entries.size());
+      t.keys[e.dtype][e.ta][e.tb].push_back(EntryKey{(double)e.mlog, e.ln, e.lk, e.li});
       t.entries.push_back(e);
     } else {
       return fail(ctx, GDY_ERR_TABLE, "unknown GO table line: %s", line.c_str());
