@@ -507,6 +507,46 @@ def run_gemm(spec: str, kernel: str, reps: int, dtype: str = "bf16") -> None:
     print("done", spec, kernel, flush=True)
 
 
+def plan_cost(table: str, count: int, repeat: int) -> dict:
+    """Host time of gdy_plan -- the dynamic logic: features, Eq. 1, grouping,
+    variant binding, dispatch forming -- over the first `count` seeded
+    heterogeneous submissions, on a host-only context (no GPU is touched).
+    Per mode, the best of `repeat` passes over all submissions, in
+    microseconds per submission and per GEMM; each call crosses ctypes."""
+    from paper_2409_02227_amd import gdy, inputs
+    ctx = gdy.Context(-1, table=table)
+    arrs, gemms = [], 0
+    for sub in inputs.het_submissions(count=count):
+        ds = []
+        for j, s in enumerate(sub):
+            d = gdy.GemmDesc()
+            d.m, d.n, d.k = s.m, s.n, s.k
+            d.a_type = d.b_type = d.c_type = gdy.BF16
+            d.lda, d.ldb, d.ldc = s.k, s.n, s.n
+            base = (j + 1) << 40  # distinct, aligned, never dereferenced
+            d.a, d.b, d.c = base, base + (1 << 38), base + (2 << 38)
+            d.scale_a = d.scale_b = 1.0
+            d.variant = -1
+            ds.append(d)
+        arrs.append((gdy.descs(ds), len(ds)))
+        gemms += len(ds)
+    lib, plan = gdy.load_library(), gdy.Plan()
+    out = {"submissions": len(arrs), "gemms_per_submission": round(gemms / max(len(arrs), 1), 2), "us": {}}
+    for mode in ("sequential", "go", "selector"):
+        best = float("inf")
+        for _ in range(repeat):
+            t0 = time.perf_counter()
+            for arr, n in arrs:
+                st = lib.gdy_plan(ctx.h, arr, n, gdy.MODES[mode], 0, plan)
+                if st:
+                    raise RuntimeError(f"gdy_plan returned {st}")
+            best = min(best, time.perf_counter() - t0)
+        per = best / max(len(arrs), 1) * 1e6
+        out["us"][mode] = {"per_submission": round(per, 2), "per_gemm": round(per * len(arrs) / max(gemms, 1), 3)}
+    ctx.close()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -536,6 +576,10 @@ def main():
     e = sub.add_parser("ceilings")
     e.add_argument("--repeat", type=int, default=5)
     e.add_argument("--out", required=True)
+    q = sub.add_parser("plan-cost", help="host time of gdy_plan over the heterogeneous submissions (no GPU)")
+    q.add_argument("--table", default=TABLE)
+    q.add_argument("--submissions", type=int, default=200)
+    q.add_argument("--repeat", type=int, default=20)
     r = sub.add_parser("run-gemm")
     r.add_argument("spec")
     r.add_argument("kernel")
@@ -548,6 +592,9 @@ def main():
         return trace(args)
     if args.cmd == "ceilings":
         return ceilings(args)
+    if args.cmd == "plan-cost":
+        print(json.dumps(plan_cost(args.table, args.submissions, args.repeat)), flush=True)
+        return None
     if bool(args.workload) == bool(args.gemm):
         raise SystemExit("give one of --workload or --gemm")
     if args.traffic_record and not args.workload:

@@ -112,3 +112,12 @@ def test_split_spans_pair_each_split_dispatch_with_its_reduction():
             row(6, "gdy::split_reduce<2>", 64, 843_000, 860_000)]
     assert profiling.split_spans(rows, 3584) == [262.0, 260.0]
     assert profiling.split_spans(rows, 512) == []
+
+
+def test_plan_cost_times_every_mode_on_a_host_context():
+    """plan-cost plans real submissions without a GPU and reports positive
+    per-submission and per-GEMM times for each mode."""
+    r = profiling.plan_cost(profiling.TABLE, count=3, repeat=1)
+    assert r["submissions"] == 3 and r["gemms_per_submission"] >= 2
+    for mode in ("sequential", "go", "selector"):
+        assert r["us"][mode]["per_submission"] > 0 and r["us"][mode]["per_gemm"] > 0
