@@ -232,9 +232,13 @@ gdy_status gdy_create(gdy_ctx** out, int device, const char* table_path, int32_t
 
 /*
  * Resource constraint for subsequent launches (Sec. 4.2.1 "RC tuning"):
- * 0 = whole GPU; 128, 64 or 32 = run on the CU-masked pool restricted to
- * that many CUs (needs use_cu_masks at create).  Other values:
- * GDY_ERR_INVALID_ARG.
+ * 0 = whole GPU; 128, 64 or 32 = launches that go to pool streams run on
+ * the CU-masked streams restricted to that many CUs (needs use_cu_masks
+ * bit 0 at create).  Pool streams carry every dispatch of GDY_DEFAULT and
+ * GDY_FORCED (the tuner's isolated runs use GDY_FORCED with forced_cd 1)
+ * and the further dispatches of a group; what runs on the caller's origin
+ * stream (GDY_SEQUENTIAL, a group's first dispatch) is not masked.  Other
+ * values: GDY_ERR_INVALID_ARG.
  */
 gdy_status gdy_set_rc(gdy_ctx* ctx, int32_t budget_cus);
 
