@@ -507,6 +507,187 @@ def run_gemm(spec: str, kernel: str, reps: int, dtype: str = "bf16") -> None:
     print("done", spec, kernel, flush=True)
 
 
+# Sec. 6.2's GO-Kernel properties, per GEMM run alone: L2 requests, L2 misses
+# and L2-to-fabric read requests (what each XCD's L2 asks of the Infinity
+# Cache and HBM) -- three TCC counters, one run
+GO_PROP_COUNTERS = ["TCC_REQ_sum", "TCC_MISS_sum", "TCC_EA0_RDREQ_sum"]
+GO_PROP_REPS = 3
+
+
+def go_property_shapes(table: str, sample: int, seed: int = 62) -> dict:
+    """Host part of Sec. 6.2 (no GPU): for every tuned single bf16 NN shape of
+    the table's records, the #waves of the kernel bound for each CD class
+    (Sec. 4.3's feature: #WGs / (CUs x occupancy)) against the isolated one,
+    and whether they differ; plus a seeded sample of shapes with their
+    isolated and CD-16 GO-Kernel variant names, for the counter run."""
+    import numpy as np
+    from paper_2409_02227_amd import gdy
+    rec_path = os.path.splitext(table)[0] + "_records.jsonl"
+    shapes = []
+    with open(rec_path) as f:
+        for line in f:
+            sh = json.loads(line)["shape"]
+            if sh[0] == "bf16" and sh[1] == 0 and sh[2] == 0 and (len(sh) < 7 or sh[6] in (0, 1)):
+                shapes.append(tuple(int(x) for x in sh[3:6]))
+    ctx = gdy.Context(-1, table=table)
+
+    def desc(m, n, k, slot):
+        d = gdy.GemmDesc()
+        d.m, d.n, d.k = m, n, k
+        d.a_type = d.b_type = d.c_type = gdy.BF16
+        d.lda, d.ldb, d.ldc = k, n, n
+        base = (slot + 1) << 40
+        d.a, d.b, d.c = base, base + (1 << 38), base + (2 << 38)
+        d.scale_a = d.scale_b = 1.0
+        d.variant = -1
+        return d
+
+    rows = []
+    for (m, n, k) in shapes:
+        x = ctx.features(desc(m, n, k, 0))
+        waves = [x[3 + 3 * c + 2] for c in range(5)]
+        iso = ctx.plan([desc(m, n, k, 0)], mode="sequential")["variant_of"][0]
+        go = {}
+        for c, cd in ((1, 2), (2, 4), (3, 8), (4, 16)):
+            go[cd] = ctx.plan([desc(m, n, k, j) for j in range(cd)], mode="go")["variant_of"][0]
+        rows.append({"shape": [m, n, k], "waves": waves, "iso": ctx.variant(iso)["name"],
+                     "go": {cd: ctx.variant(v)["name"] for cd, v in go.items()}})
+    ctx.close()
+    summary = {"shapes": len(rows), "per_cd": {}}
+    for c, cd in ((1, 2), (2, 4), (3, 8), (4, 16)):
+        ratio = np.array([r["waves"][c] / r["waves"][0] for r in rows if r["waves"][0] > 0])
+        differs = np.mean([r["go"][cd] != r["iso"] for r in rows])
+        summary["per_cd"][cd] = {"go_kernel_differs": round(float(differs), 3),
+                                 "waves_ratio_below_1": round(float(np.mean(ratio < 1 - 1e-9)), 3),
+                                 "waves_ratio_equal_1": round(float(np.mean(np.abs(ratio - 1) <= 1e-9)), 3),
+                                 "waves_ratio_geomean": round(float(np.exp(np.mean(np.log(ratio)))), 3)}
+    rng = np.random.default_rng(seed)
+    pick = [rows[i] for i in sorted(rng.choice(len(rows), size=min(sample, len(rows)), replace=False))]
+    summary["sample"] = [{"shape": r["shape"], "iso": r["iso"], "go16": r["go"][16],
+                          "waves_iso": r["waves"][0], "waves_go16": r["waves"][4]} for r in pick]
+    return summary
+
+
+def go_run(items: list) -> None:
+    """GPU runner of the counter pass: for each "MxNxK:variant" item, a
+    one-element fill (the marker the reader splits on), then the GEMM alone
+    GO_PROP_REPS times on that variant (forced, one stream)."""
+    import torch
+    from paper_2409_02227_amd import gdy
+    ctx = gdy.Context(0, table=TABLE if os.path.exists(TABLE) else None, max_streams=2)
+    h = gdy._stream_handle(None)
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    ops, arrs = {}, []
+    for it in items:
+        spec, name = it.split(":")
+        m, n, k = (int(x) for x in spec.split("x"))
+        if spec not in ops:
+            a = (torch.rand(m, k, device="cuda", generator=gen) * 2 - 1).to(torch.bfloat16)
+            b = (torch.randn(k, n, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+            ops[spec] = (a, b, torch.empty(m, n, dtype=torch.bfloat16, device="cuda"))
+        vid = ctx.find(name)
+        if vid < 0:
+            raise SystemExit(f"no variant {name}")
+        arrs.append(gdy.descs([gdy.Gemm(*ops[spec], variant=vid)]))
+    marker = torch.empty(1, device="cuda")  # allocated without a kernel: every fill is a marker
+    torch.cuda.synchronize()
+    for arr in arrs:
+        marker.fill_(1.0)
+        for _ in range(GO_PROP_REPS):
+            ctx.execute_descs(arr, 1, gdy.MODES["forced"], 1, h)
+    torch.cuda.synchronize()
+    print("done", len(items), flush=True)
+
+
+def read_segments(d: str) -> list:
+    """Counter rows in dispatch order, split at each fill (marker) dispatch:
+    per segment after a marker, the sums of the library's dispatches."""
+    rows = {}
+    for f in glob.glob(os.path.join(d, "*counter_collection.csv")):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                row = rows.setdefault(int(r["Dispatch_Id"]), {"kernel": r["Kernel_Name"]})
+                row[r["Counter_Name"]] = row.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    segs = None
+    for i in sorted(rows):
+        r = rows[i]
+        if "FillFunctor" in r["kernel"]:
+            segs = (segs or []) + [{}]
+        elif segs is not None and "gdy::" in r["kernel"]:
+            for c, v in r.items():
+                if c != "kernel":
+                    segs[-1][c] = segs[-1].get(c, 0.0) + v
+    return segs or []
+
+
+def go_properties(args) -> dict:
+    import numpy as np
+    res = go_property_shapes(args.table, args.sample)
+    if args.counters:
+        out_dir = os.path.abspath(args.raw)
+        os.makedirs(out_dir, exist_ok=True)
+        items = []
+        for s in res["sample"]:
+            spec = "x".join(str(x) for x in s["shape"])
+            items += [f"{spec}:{s['iso']}", f"{spec}:{s['go16']}"]
+        cmd = [_python(), "-m", "paper_2409_02227_amd.profiling", "go-run", *items]
+        d = run_pass(out_dir, "l2", GO_PROP_COUNTERS, cmd, args.timeout)
+        segs = read_segments(d)
+        if len(segs) != len(items):
+            raise RuntimeError(f"{len(segs)} marked segments for {len(items)} runs; see {d}")
+        ratios = {c: [] for c in GO_PROP_COUNTERS}
+        ratios_total = {c: [] for c in GO_PROP_COUNTERS}
+        for j, s in enumerate(res["sample"]):
+            iso, go = segs[2 * j], segs[2 * j + 1]
+            s["counters_iso"] = {c: iso.get(c, 0.0) / GO_PROP_REPS for c in GO_PROP_COUNTERS}
+            s["counters_go16"] = {c: go.get(c, 0.0) / GO_PROP_REPS for c in GO_PROP_COUNTERS}
+            for c in GO_PROP_COUNTERS:
+                a, b = s["counters_iso"][c], s["counters_go16"][c]
+                if a > 0 and b > 0 and s["waves_iso"] > 0 and s["waves_go16"] > 0:
+                    ratios_total[c].append(b / a)
+                    ratios[c].append((b / s["waves_go16"]) / (a / s["waves_iso"]))
+        res["counter_ratios"] = {
+            c: {"per_gemm_geomean": round(float(np.exp(np.mean(np.log(ratios_total[c])))), 3),
+                "per_gemm_below_1": round(float(np.mean(np.array(ratios_total[c]) < 1)), 3),
+                "per_wave_geomean": round(float(np.exp(np.mean(np.log(ratios[c])))), 3),
+                "per_wave_below_1": round(float(np.mean(np.array(ratios[c]) < 1)), 3)}
+            for c in GO_PROP_COUNTERS if ratios[c]}
+        if not args.keep_raw:
+            prune(d)
+    res["command"] = " ".join(shlex.quote(x) for x in ["python3", "-m", "paper_2409_02227_amd.profiling", *sys.argv[1:]])
+    return res
+
+
+def write_go_properties(path: str, res: dict) -> None:
+    lines = ["# GO-Kernel properties (Sec. 6.2): waves and L2 traffic against the isolated kernels", "",
+             "Command (on the MI355X, from the repository root):", "", f"    {res['command']}", "",
+             f"Tuned single bf16 NN shapes of the table's records: {res['shapes']}. #waves is Sec. 4.3's feature "
+             "(#WGs / (CUs x occupancy)) of the kernel bound for the CD class, against the isolated kernel's.", "",
+             "| CD | GO-Kernel differs from the isolated one | waves ratio < 1 | = 1 | waves ratio geomean |",
+             "|---|---|---|---|---|"]
+    for cd, v in res["per_cd"].items():
+        lines.append(f"| {cd} | {v['go_kernel_differs']} | {v['waves_ratio_below_1']} | {v['waves_ratio_equal_1']} "
+                     f"| {v['waves_ratio_geomean']} |")
+    if "counter_ratios" in res:
+        lines += ["", f"Counters (rocprofv3 --pmc {' '.join(GO_PROP_COUNTERS)}), each GEMM run alone "
+                  f"{GO_PROP_REPS} times on its isolated kernel and on its CD-16 GO-Kernel, for "
+                  f"{len(res['sample'])} seeded shapes; ratios GO / isolated, per GEMM and per wave:", "",
+                  "| counter | per GEMM geomean | share < 1 | per wave geomean | share < 1 |", "|---|---|---|---|---|"]
+        for c, v in res["counter_ratios"].items():
+            lines.append(f"| {c} | {v['per_gemm_geomean']} | {v['per_gemm_below_1']} | {v['per_wave_geomean']} "
+                         f"| {v['per_wave_below_1']} |")
+        lines += ["", "| shape | isolated | GO (CD 16) | waves iso / GO | L2 req iso / GO | L2 miss iso / GO |",
+                  "|---|---|---|---|---|---|"]
+        for s in res["sample"]:
+            ci, cg = s["counters_iso"], s["counters_go16"]
+            lines.append(f"| {'x'.join(map(str, s['shape']))} | {s['iso']} | {s['go16']} | "
+                         f"{s['waves_iso']:.3f} / {s['waves_go16']:.3f} | "
+                         f"{ci['TCC_REQ_sum']:.3g} / {cg['TCC_REQ_sum']:.3g} | "
+                         f"{ci['TCC_MISS_sum']:.3g} / {cg['TCC_MISS_sum']:.3g} |")
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def plan_cost(table: str, count: int, repeat: int) -> dict:
     """Host time of gdy_plan -- the dynamic logic: features, Eq. 1, grouping,
     variant binding, dispatch forming -- over the first `count` seeded
@@ -580,6 +761,16 @@ def main():
     q.add_argument("--table", default=TABLE)
     q.add_argument("--submissions", type=int, default=200)
     q.add_argument("--repeat", type=int, default=20)
+    g = sub.add_parser("go-properties", help="Sec. 6.2: waves and L2 traffic of GO-Kernels against isolated ones")
+    g.add_argument("--table", default=TABLE)
+    g.add_argument("--sample", type=int, default=24, help="shapes for the counter run")
+    g.add_argument("--counters", action="store_true", help="also run the rocprofv3 counter pass (GPU)")
+    g.add_argument("--raw", default="profiling_raw/go_properties")
+    g.add_argument("--out", help="write the text summary here (profiles/...)")
+    g.add_argument("--timeout", type=int, default=240)
+    g.add_argument("--keep-raw", action="store_true")
+    gr = sub.add_parser("go-run")
+    gr.add_argument("items", nargs="+")
     r = sub.add_parser("run-gemm")
     r.add_argument("spec")
     r.add_argument("kernel")
@@ -592,6 +783,14 @@ def main():
         return trace(args)
     if args.cmd == "ceilings":
         return ceilings(args)
+    if args.cmd == "go-run":
+        return go_run(args.items)
+    if args.cmd == "go-properties":
+        res = go_properties(args)
+        if args.out:
+            write_go_properties(args.out, res)
+        print(json.dumps({k: v for k, v in res.items() if k != "sample"}), flush=True)
+        return None
     if args.cmd == "plan-cost":
         print(json.dumps(plan_cost(args.table, args.submissions, args.repeat)), flush=True)
         return None

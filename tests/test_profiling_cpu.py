@@ -121,3 +121,28 @@ def test_plan_cost_times_every_mode_on_a_host_context():
     assert r["submissions"] == 3 and r["gemms_per_submission"] >= 2
     for mode in ("sequential", "go", "selector"):
         assert r["us"][mode]["per_submission"] > 0 and r["us"][mode]["per_gemm"] > 0
+
+
+def test_go_properties_segments_split_at_markers(tmp_path):
+    """The counter pass's dispatches are attributed to runs by the fill
+    marker before each run; dispatches before the first marker (operand set-up)
+    and kernels other than the library's are ignored."""
+    rows = []
+    seq = [("at::rand_kernel", 5.0), ("FillFunctor", 1.0), ("gdy::go_gemm_d<A>", 10.0), ("gdy::go_gemm_d<A>", 12.0),
+           ("FillFunctor", 1.0), ("gdy::go_gemm_d<B>", 3.0), ("gdy::split_reduce<2>", 2.0), ("at::other", 7.0)]
+    for i, (name, v) in enumerate(seq):
+        rows.append({"Dispatch_Id": 100 - i * 0 + i, "Kernel_Name": name, "Counter_Name": "TCC_REQ_sum",
+                     "Counter_Value": v})
+    _write_csv(tmp_path / "p_counter_collection.csv", rows)
+    segs = profiling.read_segments(str(tmp_path))
+    assert [s.get("TCC_REQ_sum", 0.0) for s in segs] == [22.0, 5.0]
+
+
+def test_go_property_shapes_host_part():
+    r = profiling.go_property_shapes(profiling.TABLE, sample=3)
+    assert r["shapes"] > 100 and len(r["sample"]) == 3
+    for cd in (2, 4, 8, 16):
+        v = r["per_cd"][cd]
+        assert 0 <= v["waves_ratio_below_1"] <= 1 and 0 < v["waves_ratio_geomean"] <= 1.5
+    for s in r["sample"]:
+        assert s["waves_iso"] > 0 and s["waves_go16"] > 0 and s["iso"].startswith("bf16_nn_")
