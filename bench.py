@@ -56,7 +56,7 @@ WORKLOADS = {
                               "(CU-masked streams) and unpartitioned"),
     "knn_tuning": ("knn", "CD copies (CD = 2, 4, 8, 16) of 40 bf16 shapes whose GO-Kernels a KNN "
                           "table predicts from the 20% of shapes tuned exhaustively"),
-    "selector_accuracy": ("acc", "n copies (n = 2, 4, 8, 16) of bf16 shapes (untuned ones drawn like the "
+    "selector_accuracy": ("acc", "n copies (n = 2, 4, 8, 16) of bf16 (--accuracy-dtype f16: fp16) shapes (untuned ones drawn like the "
                                  "heterogeneous submissions', or --accuracy-set tuned); selector CD against "
                                  "the best CD, selector and GO against default"),
 }
@@ -110,6 +110,8 @@ def parse():
     ap.add_argument("--no-clocks", action="store_true", help="do not sample GPU clocks with amd-smi")
     ap.add_argument("--accuracy-shapes", type=int, default=30,
                     help="selector_accuracy workload: number of shapes")
+    ap.add_argument("--accuracy-dtype", default="bf16", choices=("bf16", "f16"),
+                    help="selector_accuracy: input type of the GEMM sets (Sec. 6.8 reduced precision: f16)")
     ap.add_argument("--accuracy-set", default="untuned", choices=("untuned", "tuned"),
                     help="selector_accuracy workload: shapes drawn like the heterogeneous submissions' "
                          "(none tuned), or a seeded sample of the GO table's bf16 NN shapes")
@@ -437,12 +439,14 @@ def accuracy_bench(args, desc):
     ctx = gdy.Context(0, table=table, max_streams=16)
     handle = gdy._stream_handle(None)
     shapes, seen = [], set()
+    dt_code = {"bf16": "2", "f16": "1"}[args.accuracy_dtype]
+    tdt = {"bf16": torch.bfloat16, "f16": torch.float16}[args.accuracy_dtype]
     if args.accuracy_set == "tuned":
-        # the table's own bf16 NN shapes (M = 2^ceil(log2 M) of the entry)
+        # the table's own NN shapes of the type (M = 2^ceil(log2 M) of the entry)
         tuned = []
         for line in open(table):
             tok = line.split()
-            if tok and tok[0] == "entry" and tok[1:4] == ["2", "0", "0"] and tok[7] == "1":
+            if tok and tok[0] == "entry" and tok[1:4] == [dt_code, "0", "0"] and tok[7] == "1":
                 tuned.append((1 << int(tok[4]), int(tok[5]), int(tok[6])))
         order = np.random.default_rng(46).permutation(len(tuned))
         shapes = [tuned[i] for i in order[:args.accuracy_shapes]]
@@ -461,9 +465,9 @@ def accuracy_bench(args, desc):
         sp = {"selector": [], "go": []}
         sq = {"selector": [], "go": []}
         for (m, nn, k) in shapes:
-            a = (torch.rand(n, m, k, device="cuda", generator=gen) * 2 - 1).to(torch.bfloat16)
-            b = (torch.randn(n, k, nn, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
-            c = torch.empty(n, m, nn, dtype=torch.bfloat16, device="cuda")
+            a = (torch.rand(n, m, k, device="cuda", generator=gen) * 2 - 1).to(tdt)
+            b = (torch.randn(n, k, nn, device="cuda", generator=gen) * 0.02).to(tdt)
+            c = torch.empty(n, m, nn, dtype=tdt, device="cuda")
             gemms = [gdy.Gemm(a[i], b[i], c[i]) for i in range(n)]
             arr = gdy.descs(gemms)
             t_best, cd_best = best_cd_time(ctx, arr, n, args.steps, 2, handle, torch)
@@ -494,8 +498,8 @@ def accuracy_bench(args, desc):
     value = tot_f / tot_t / 1e12
     out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
            "steps": args.steps, "warmup": 2, "ms_per_step": round(1e3 * tot_t / (4 * len(shapes)), 4),
-           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
-           "data": "synthetic (seeded device draws; A ~ U[-1,1], B ~ N(0, 0.02))",
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": args.accuracy_dtype, "data": "synthetic (seeded device draws; A ~ U[-1,1], B ~ N(0, 0.02))",
            "config": {"workload": f"selector_accuracy: {desc}", "mode": "selector", "shapes": len(shapes),
                       "shape_set": args.accuracy_set,
                       "table": os.path.relpath(table, ROOT) if table else None},
