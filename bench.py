@@ -519,9 +519,10 @@ def benefit_shares(speedups) -> dict:
     degraded against default (speedup = default time / mode time), plus the
     geomean and the extremes."""
     v = np.array(speedups, dtype=float)
-    return {"cases": int(v.size), "improved": round(float(np.mean(v > 1 + BENEFIT_BAND)), 4),
-            "unchanged": round(float(np.mean(np.abs(v - 1) <= BENEFIT_BAND)), 4),
-            "degraded": round(float(np.mean(v < 1 - BENEFIT_BAND)), 4),
+    up, down = v > 1 + BENEFIT_BAND, v < 1 - BENEFIT_BAND  # the band's edges count as unchanged
+    return {"cases": int(v.size), "improved": round(float(np.mean(up)), 4),
+            "unchanged": round(float(np.mean(~(up | down))), 4),
+            "degraded": round(float(np.mean(down)), 4),
             "geomean": round(float(np.exp(np.mean(np.log(v)))), 4),
             "min": round(float(v.min()), 4), "max": round(float(v.max()), 4)}
 
