@@ -59,25 +59,30 @@ def build_ceilings() -> str:
     return CEILINGS
 
 
-EXAMPLE = os.path.join(HERE, "examples", "gemm_set")
+EXAMPLES = ("gemm_set", "graph_static")
 
 
-def build_example() -> str:
-    """examples/gemm_set: a C++ program that drives libgdy through its C-ABI
-    alone (no Python), linked against the in-tree library."""
-    tmp = EXAMPLE + ".tmp"
-    cmd = [_hipcc(), *[f for f in FLAGS if f != "-fPIC"], os.path.join(HERE, "examples", "gemm_set.cpp"),
-           "-L", HERE, "-lgdy", "-Wl,-rpath,$ORIGIN/..", "-o", tmp]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed for examples/gemm_set.cpp:\n{r.stderr}")
-    os.replace(tmp, EXAMPLE)
-    return EXAMPLE
+def build_example() -> list:
+    """examples/gemm_set and examples/graph_static: C++ programs that drive
+    libgdy through its C-ABI alone (no Python), linked against the in-tree
+    library."""
+    out = []
+    for name in EXAMPLES:
+        exe = os.path.join(HERE, "examples", name)
+        tmp = exe + ".tmp"
+        cmd = [_hipcc(), *[f for f in FLAGS if f != "-fPIC"], os.path.join(HERE, "examples", name + ".cpp"),
+               "-L", HERE, "-lgdy", "-Wl,-rpath,$ORIGIN/..", "-o", tmp]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc failed for examples/{name}.cpp:\n{r.stderr}")
+        os.replace(tmp, exe)
+        out.append(exe)
+    return out
 
 
 def build(jobs: int | None = None) -> str:
     """Compile every source and link libgdy.so (always rebuilds), then build
-    the ceiling probe and the C-ABI example program."""
+    the ceiling probe and the C-ABI example programs."""
     os.makedirs(BUILD, exist_ok=True)
     jobs = jobs or min(len(SOURCES), os.cpu_count() or 1)
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
